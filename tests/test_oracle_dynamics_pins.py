@@ -1,0 +1,352 @@
+"""Pins of the pre-LLM scorer oracle (Section 3.1, Eq. 1-4; Algorithm 1).
+
+Each check ties the oracle to something other than itself: library routines
+(torch adaptive pooling, scipy Gaussian filtering), the HSIC form of linear
+CKA and Eq. 1 written in feature space, closed forms of rank-one windows,
+hand-computed examples, brute-force enumeration, and the scene structure the
+generators plant.
+"""
+
+import itertools
+import math
+
+import numpy as np
+import pytest
+import scipy.ndimage
+import torch
+
+import workloads as W
+from oracle import dynamics as OD, widen
+
+
+# -- coarse pass
+
+
+def test_audio_resample_is_adaptive_avg_pool():
+    rng = np.random.default_rng(0)
+    for n_audio, n_frames in ((1500, 120), (25, 2), (7, 5), (13, 13), (3, 8)):
+        xa = rng.standard_normal((n_audio, 6))
+        ours = OD.resample_audio(xa, n_frames)
+        ref = torch.nn.functional.adaptive_avg_pool1d(
+            torch.from_numpy(xa.T.copy())[None], n_frames)[0].T.numpy()
+        np.testing.assert_allclose(ours, ref, rtol=1e-13, atol=1e-15)
+
+
+def test_frame_pool_is_mean_over_tokens():
+    rng = np.random.default_rng(1)
+    x = rng.standard_normal((5 * 7, 3))
+    v = OD.pool_frames(x, 5, 7)
+    for f in range(5):
+        np.testing.assert_allclose(v[f], sum(x[f * 7 + p] for p in range(7)) / 7, rtol=1e-14)
+
+
+def test_window_rows():
+    assert OD.window_rows(0, 10, 3) == (0, 3)
+    assert OD.window_rows(5, 10, 3) == (4, 7)
+    assert OD.window_rows(9, 10, 3) == (7, 10)
+    # Even window: the extra frame lies in the past.
+    assert OD.window_rows(5, 10, 4) == (3, 7)
+    assert OD.window_rows(2, 2, 3) == (0, 2)
+
+
+# -- Eq. 1
+
+
+def _eq1_feature_space(a, v):
+    a = a - a.mean(axis=0)
+    v = v - v.mean(axis=0)
+    num = np.linalg.norm(v.T @ a, "fro") ** 2
+    return num / (np.linalg.norm(a.T @ a, "fro") * np.linalg.norm(v.T @ v, "fro"))
+
+
+def _hsic_cka(a, v):
+    """Kornblith et al. linear CKA: HSIC(K, L) / sqrt(HSIC(K, K) HSIC(L, L))
+    with K = A A^T, L = V V^T on the raw rows and H the centring matrix."""
+    n = a.shape[0]
+    h = np.eye(n) - np.ones((n, n)) / n
+    k, l = a @ a.T, v @ v.T
+
+    def hsic(x, y):
+        return np.trace(x @ h @ y @ h)
+
+    return hsic(k, l) / math.sqrt(hsic(k, k) * hsic(l, l))
+
+
+def test_cka_equals_eq1_in_feature_space_and_hsic_form():
+    rng = np.random.default_rng(2)
+    for w in (2, 3, 4, 6):
+        for _ in range(5):
+            a = rng.standard_normal((w, 11))
+            v = rng.standard_normal((w, 11)) + 0.5 * a
+            c = OD.linear_cka(a, v)
+            assert c == pytest.approx(_eq1_feature_space(a, v), rel=1e-12)
+            assert c == pytest.approx(_hsic_cka(a, v), rel=1e-12)
+            assert 0.0 <= c <= 1.0 + 1e-15
+
+
+def test_cka_invariances_and_special_cases():
+    rng = np.random.default_rng(3)
+    a = rng.standard_normal((4, 9))
+    v = rng.standard_normal((4, 9))
+    c = OD.linear_cka(a, v)
+    assert OD.linear_cka(a, a) == pytest.approx(1.0, rel=1e-14)
+    q, _ = np.linalg.qr(rng.standard_normal((9, 9)))
+    assert OD.linear_cka(a @ q, v) == pytest.approx(c, rel=1e-12)
+    assert OD.linear_cka(3.7 * a, v) == pytest.approx(c, rel=1e-12)
+    assert OD.linear_cka(a + rng.standard_normal(9), v) == pytest.approx(c, rel=1e-12)
+    # Two centred rows are always collinear: CKA = 1.
+    assert OD.linear_cka(a[:2], v[:2]) == pytest.approx(1.0, rel=1e-12)
+    # A constant stack has zero centred Gram: CKA defined as 0.
+    assert OD.linear_cka(np.ones((3, 5)), v[:3]) == 0.0
+
+
+def test_cka_rank_one_closed_form():
+    """A = u a^T, V = t b^T: CKA = (u_c . t_c)^2 / (|u_c|^2 |t_c|^2)."""
+    rng = np.random.default_rng(4)
+    a_dir, b_dir = rng.standard_normal(16), rng.standard_normal(16)
+    spike, trend = np.array([-1.0, 1.0, -1.0]), np.array([0.0, 1.0, 2.0])
+    assert OD.linear_cka(np.outer(spike, a_dir), np.outer(trend, b_dir)) == pytest.approx(0.0, abs=1e-15)
+    alt4, trend4 = np.array([1.0, -1.0, 1.0, -1.0]), np.arange(4.0)
+    # centred: alt4 -> (1,-1,1,-1), trend4 -> (-1.5,-.5,.5,1.5): (u.t)^2 = 4, |u|^2 |t|^2 = 4*5
+    assert OD.linear_cka(np.outer(alt4, a_dir), np.outer(trend4, b_dir)) == pytest.approx(0.2, rel=1e-13)
+    u, t = rng.standard_normal(5), rng.standard_normal(5)
+    uc, tc = u - u.mean(), t - t.mean()
+    want = (uc @ tc) ** 2 / ((uc @ uc) * (tc @ tc))
+    assert OD.linear_cka(np.outer(u, a_dir), np.outer(t, b_dir)) == pytest.approx(want, rel=1e-12)
+
+
+def test_frame_cka_uses_clamped_windows():
+    rng = np.random.default_rng(5)
+    a, v = rng.standard_normal((7, 5)), rng.standard_normal((7, 5))
+    c = OD.frame_cka(a, v, 3)
+    assert c[0] == pytest.approx(_eq1_feature_space(a[0:3], v[0:3]), rel=1e-12)
+    assert c[3] == pytest.approx(_eq1_feature_space(a[2:5], v[2:5]), rel=1e-12)
+    assert c[6] == pytest.approx(_eq1_feature_space(a[4:7], v[4:7]), rel=1e-12)
+
+
+# -- Eq. 2: direct distance and gate
+
+
+def test_direct_distance_closed_form():
+    xa = np.array([[1.0, 0.0, 0.0], [0.0, 1.0, 0.0]])
+    xv = np.array([[2.0, 0.0, 0.0],    # parallel to audio 0: cos 1
+                   [0.0, 0.0, 5.0],    # orthogonal to both: cos 0
+                   [1.0, 1.0, 0.0],    # 45 degrees: cos sqrt(1/2)
+                   [-1.0, -1.0, 0.0]])  # best match cos = -sqrt(1/2)
+    d, best = OD.direct_distance(xv, xa, 2, 2)
+    np.testing.assert_allclose(best, [1.0, 0.0, math.sqrt(0.5), -math.sqrt(0.5)], atol=1e-15)
+    np.testing.assert_allclose(d, [0.5, 1.0], atol=1e-15)
+    np.testing.assert_allclose(OD.minmax(np.array([2.0, 4.0, 3.0])), [0.0, 1.0, 0.5])
+    assert np.all(OD.minmax(np.array([1.0, 1.0])) == 0)
+
+
+def test_gate_switches_on_cka_mean():
+    case = W.dynamics_small("offset")
+    s = case.seqs[0]
+    r = OD.score_sequence(widen(case.xv, "bf16"), widen(case.xa, "bf16"), widen(case.xq, "bf16"),
+                          s.n_frames, s.per_frame, case.params)
+    assert r["gate"] and r["cbar"] < 0.78
+    b = 0.90
+    np.testing.assert_allclose(r["alpha"], (1 - b) * r["cka"] + b * (1 - r["dhat"]), rtol=1e-15)
+    case = W.dynamics_small("shared")
+    s = case.seqs[0]
+    r = OD.score_sequence(widen(case.xv, "bf16"), widen(case.xa, "bf16"), widen(case.xq, "bf16"),
+                          s.n_frames, s.per_frame, case.params)
+    assert not r["gate"] and r["cbar"] > 0.78
+    np.testing.assert_array_equal(r["alpha"], r["cka"])
+
+
+# -- segmentation
+
+
+@pytest.mark.parametrize("n", [1, 2, 3, 5, 9, 40, 119])
+def test_smoothing_matches_scipy(n):
+    rng = np.random.default_rng(n)
+    x = rng.uniform(0.8, 1.0, size=n)
+    for sigma in (1.0, 0.7, 2.0):
+        ref = scipy.ndimage.gaussian_filter1d(x, sigma, mode="reflect", truncate=4.0)
+        np.testing.assert_allclose(OD.gaussian_smooth(x, sigma), ref, rtol=1e-13)
+
+
+def test_single_hard_cut_gives_five_low_positions_and_one_cut():
+    cs = np.full(30, 0.99)
+    cs[12] = 0.0
+    sm = OD.gaussian_smooth(cs, 1.0)
+    assert np.flatnonzero(sm < 0.97).tolist() == [10, 11, 12, 13, 14]
+    seg, _ = OD.segment_ids(sm, 31, 0.97)
+    assert seg.tolist() == [0] * 13 + [1] * 18
+
+
+def test_segments_from_hand_built_runs():
+    sm = np.array([0.99, 0.5, 0.4, 0.6, 0.99, 0.99, 0.1, 0.99, 0.95])
+    seg, margin = OD.segment_ids(sm, 10, 0.97)
+    # runs {1,2,3} (min at 2) and {6} and {8}: cuts after frames 2, 6, 8
+    assert seg.tolist() == [0, 0, 0, 1, 1, 1, 1, 2, 2, 3]
+    assert margin == pytest.approx(0.02)
+    seg, _ = OD.segment_ids(np.full(5, 0.99), 6, 0.97)
+    assert seg.tolist() == [0] * 6
+
+
+# -- Eq. 3 and the frame score
+
+
+def test_relevance_and_segment_score_closed_forms():
+    qbar = np.array([1.0, 0.0])
+    v = np.array([[2.0, 0.0], [-1.0, 0.0], [0.0, 3.0]])
+    np.testing.assert_allclose(OD.relevance(v, qbar), [1.0, 0.0, 0.5])
+    r = np.array([0.2, 0.8, 0.5, 0.4])
+    seg = np.array([0, 0, 0, 1])
+    g = OD.segment_scores(r, seg, 0.5)
+    assert g[0] == pytest.approx(math.sqrt(3) * (0.5 * 0.8 + 0.5 * 0.5))
+    assert g[1] == pytest.approx(0.4)
+
+
+# -- Eq. 4 and the frame budgets
+
+
+def test_visual_budget_hand_values():
+    assert OD.visual_budget(0.5, 1500, 17280) == 7890
+    assert OD.visual_budget(0.35, 1500, 17280) == 5073
+    assert OD.visual_budget(0.1, 1500, 1000) == 0
+    assert OD.visual_budget(1.0, 10, 20) == 20
+
+
+def _brute_apportion(total, q, caps):
+    best, best_key = None, None
+    for alloc in itertools.product(*[range(c + 1) for c in caps]):
+        if sum(alloc) != total:
+            continue
+        key = (sum((a - x) ** 2 for a, x in zip(alloc, q)),
+               tuple(-a for a in alloc))   # on equal error, favour lower indices
+        if best_key is None or key < best_key:
+            best, best_key = alloc, key
+    return list(best)
+
+
+def test_apportion_is_l2_closest_integer_vector_without_binding_caps():
+    rng = np.random.default_rng(6)
+    for _ in range(200):
+        n = int(rng.integers(1, 5))
+        w = rng.uniform(0.05, 1.0, size=n)
+        total = int(rng.integers(0, 9))
+        caps = [total] * n
+        q = [total * x / w.sum() for x in w]
+        alloc, _ = OD.apportion(total, w, caps)
+        assert alloc.tolist() == _brute_apportion(total, q, caps)
+
+
+def _waterfill(total, w, caps):
+    """q*_i = min(cap_i, lam * w_i) with sum q* = total, lam by bisection."""
+    lo, hi = 0.0, 1.0
+    while sum(min(c, hi * x) for x, c in zip(w, caps)) < total:
+        hi *= 2.0
+    for _ in range(200):
+        mid = 0.5 * (lo + hi)
+        if sum(min(c, mid * x) for x, c in zip(w, caps)) < total:
+            lo = mid
+        else:
+            hi = mid
+    return [min(c, hi * x) for x, c in zip(w, caps)]
+
+
+def test_apportion_with_caps_matches_waterfill_brute_force():
+    alloc, _ = OD.apportion(8, [10.0, 1.0, 1.0], [2, 5, 5])
+    assert alloc.tolist() == [2, 3, 3]
+    rng = np.random.default_rng(7)
+    for _ in range(300):
+        n = int(rng.integers(1, 5))
+        w = rng.uniform(0.05, 1.0, size=n) ** 2
+        caps = rng.integers(0, 6, size=n).tolist()
+        total = int(rng.integers(0, sum(caps) + 1))
+        alloc, _ = OD.apportion(total, w, caps)
+        assert int(alloc.sum()) == total
+        assert np.all(alloc >= 0) and np.all(alloc <= caps)
+        qstar = _waterfill(total, w.tolist(), caps)
+        assert alloc.tolist() == _brute_apportion(total, qstar, caps)
+
+
+def test_apportion_is_scale_invariant():
+    # Table S1 writes the segment weight as twice Eq. 3 at lambda = 0.5.
+    w = np.array([0.3, 0.9, 0.45, 0.7])
+    a1, _ = OD.apportion(37, w, [20] * 4)
+    a2, _ = OD.apportion(37, 2 * w, [20] * 4)
+    assert a1.tolist() == a2.tolist()
+
+
+# -- token selection
+
+
+def test_dafps_hand_example():
+    """Four unit tokens at 0, 10, 25 and 90 degrees; density k = 2, coverage 0.8.
+
+    rho = (2.8367, 2.9261, 2.8084, 0.2981): first pick token 1; then
+    (1 - sim) * sqrt(rho) = (0.0256, -, 0.0571, 0.4512) -> token 3; then
+    token 2 (0.0571 > 0.0256); then token 0.
+    """
+    ang = np.radians([0.0, 10.0, 25.0, 90.0])
+    x = np.stack([np.cos(ang), np.sin(ang)], axis=1) * np.array([[1.0], [2.0], [0.5], [3.0]])
+    picks, margin = OD.dafps(x, 4, 2, 0.8, 0.5)
+    assert picks == [1, 3, 2, 0]
+    assert margin > 0.01
+    assert OD.dafps(x, 2, 2, 0.8, 0.5)[0] == [1, 3]
+    assert OD.dafps(x, 0, 2, 0.8, 0.5)[0] == []
+
+
+def _dafps_loops(x, k, dk, cover, power):
+    p = len(x)
+    norm = [math.sqrt(sum(v * v for v in row)) for row in x]
+    s = [[sum(a * b for a, b in zip(x[i], x[j])) / (norm[i] * norm[j]) for j in range(p)] for i in range(p)]
+    rho = []
+    for i in range(p):
+        others = sorted((s[i][j] for j in range(p) if j != i), reverse=True)
+        knn = sum(others[:dk]) / len(others[:dk])
+        cov = sum(1 for j in range(p) if j != i and s[i][j] >= cover)
+        rho.append(max(knn, 0.0) * (1 + cov))
+    picks = [max(range(p), key=lambda i: (rho[i], -i))]
+    while len(picks) < k:
+        cand = [i for i in range(p) if i not in picks]
+        val = {i: (1 - max(s[i][j] for j in picks)) * rho[i] ** power for i in cand}
+        picks.append(max(cand, key=lambda i: (val[i], -i)))
+    return picks
+
+
+def test_dafps_brute_force_loops():
+    rng = np.random.default_rng(8)
+    for trial in range(20):
+        p = int(rng.integers(2, 9))
+        x = rng.standard_normal((p, 4)) + (0.8 if trial % 2 else 0.0)
+        k = int(rng.integers(1, p + 1))
+        assert OD.dafps(x, k, 3, 0.8, 0.5)[0] == _dafps_loops(x.tolist(), k, 3, 0.8, 0.5)
+
+
+def test_dedup_keeps_least_anchor_similar_positions():
+    rng = np.random.default_rng(9)
+    anchor = rng.standard_normal((10, 6))
+    x = anchor + rng.uniform(0, 2, size=(10, 1)) * rng.standard_normal((10, 6))
+    sims = [float(x[i] @ anchor[i] / np.linalg.norm(x[i]) / np.linalg.norm(anchor[i])) for i in range(10)]
+    for k in range(11):
+        want = sorted(sorted(range(10), key=lambda i: (sims[i], i))[:k])
+        assert OD.dedup(x, anchor, k)[0] == want
+
+
+# -- whole scorer on planted clips
+
+
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_scorer_recovers_planted_scenes_and_budgets(structure):
+    case = W.dynamics_small(structure)
+    s = case.seqs[0]
+    r = OD.score_sequence(widen(case.xv, "bf16"), widen(case.xa, "bf16"), widen(case.xq, "bf16"),
+                          s.n_frames, s.per_frame, case.params)
+    starts = [0] + (np.flatnonzero(np.diff(r["segment"])) + 1).tolist()
+    assert starts == s.seg_starts
+    assert r["gate"] == (structure == "offset")
+    bv = OD.visual_budget(0.5, s.n_audio, s.n_frames * s.per_frame)
+    assert r["visual_budget"] == bv == r["kept"].size == int(r["frame_budget"].sum())
+    assert np.all(r["frame_budget"] <= s.per_frame)
+    kept = r["kept"]
+    assert np.all(np.diff(kept) > 0) and kept.min() >= 0 and kept.max() < s.n_frames * s.per_frame
+    per_frame = np.bincount(kept // s.per_frame, minlength=s.n_frames)
+    np.testing.assert_array_equal(per_frame, r["frame_budget"])
+    for key, m in r["margins"].items():
+        assert m > 1e-9, key

@@ -1,0 +1,244 @@
+/*
+ * apack.h -- C ABI of the A-PACK hot path on MI355X (gfx950).
+ *
+ * Two halves of the method of "Deferred Audio Pruning with Local Audio-Visual
+ * Dynamics for Omni-LLMs":
+ *
+ *   apack_score_dynamics  pre-LLM local audio-visual dynamics scorer
+ *                         (Section 3.1, Eq. 1-4; Algorithm 1, first loop)
+ *   apack_prune_layer     in-LLM query-conditioned scoring and per-modality
+ *                         top-k (Section 3.2, Eq. 5-6; Algorithm 1, inner loop)
+ *   apack_compact_kv      gather of the kept rows of the K/V cache, hidden
+ *                         states and position ids (Section 3.2, last
+ *                         sentence; Algorithm 1, "slice their KV-cache entries")
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ * - Tensor arguments are DEVICE pointers on the current HIP device.
+ *   Descriptor arrays (apack_seq, apack_span, apack_av_seq, pointer tables)
+ *   and the n_kept outputs are HOST pointers.
+ * - `stream` is a hipStream_t handle (NULL = the null stream).  Every kernel
+ *   and copy is enqueued on it; calls never synchronise the device.  Device
+ *   outputs are valid once the stream has reached the point of the call;
+ *   host outputs (n_kept, n_kept_visual) are valid when the call returns.
+ * - The caller owns every buffer.  The library allocates no device memory:
+ *   scratch space comes from the caller's `workspace` (size from the
+ *   matching *_query call, 256-byte aligned).  The library keeps no pointer
+ *   after a call returns.  Small host descriptors are copied to the device
+ *   through library-owned pinned staging buffers.
+ * - Errors: arguments are validated on the host before anything is enqueued.
+ *   On error nothing is launched, outputs are untouched, the status is
+ *   returned and apack_last_error() (thread-local) says why.  A failed HIP
+ *   launch or copy returns APACK_E_HIP.
+ * - Concurrent calls are safe when each uses its own workspace and outputs.
+ * - bf16 tensors hold raw bfloat16 values (1 sign, 8 exponent, 7 mantissa
+ *   bits); all inputs must be finite.
+ */
+#ifndef APACK_H
+#define APACK_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum apack_status {
+  APACK_OK = 0,
+  APACK_E_ARG = 1,        /* bad scalar argument or null pointer            */
+  APACK_E_SHAPE = 2,      /* inconsistent sizes, spans or offsets           */
+  APACK_E_DTYPE = 3,      /* unknown dtype or dtype/shape combination       */
+  APACK_E_WORKSPACE = 4,  /* workspace missing, misaligned or too small     */
+  APACK_E_ALIAS = 5,      /* an output overlaps an input                    */
+  APACK_E_HIP = 6,        /* a HIP runtime call failed                      */
+  APACK_E_UNSUPPORTED = 7 /* valid but outside what this build implements  */
+} apack_status;
+
+typedef enum apack_dtype { APACK_BF16 = 0, APACK_F32 = 1 } apack_dtype;
+
+typedef enum apack_modality {
+  APACK_OTHER = 0,  /* text, system and any row not covered by a span */
+  APACK_AUDIO = 1,
+  APACK_VISUAL = 2
+} apack_modality;
+
+/* ------------------------------------------------------------------------ */
+/* Helpers                                                                  */
+/* ------------------------------------------------------------------------ */
+
+const char* apack_version(void);
+const char* apack_last_error(void);   /* message of this thread's last error */
+const char* apack_status_string(apack_status s);
+
+/* k = ceil(keep * n) for the decimal ratio `keep` means (Eq. 6's count
+ * TopK_{ceil((1-P)|S|)}).  The product is formed in binary64 and a slack of
+ * n * 2^-50 absorbs the binary representation error of a decimal ratio with
+ * up to six fractional digits, so 0.55 * 100 gives 55 (a plain binary64
+ * ceiling gives 56).  Exact for n < 2^29.  Returns -1 when keep is outside
+ * [0, 1] or n < 0. */
+int64_t apack_keep_count(double keep, int64_t n);
+
+/* Pre-LLM visual budget (supplement, pre-LLM compression details): the joint
+ * budget B = ceil(r_pre * (n_audio + n_visual)) keeps every audio token and
+ * gives video the rest, B_v = clamp(B - n_audio, 0, n_visual).  Returns -1
+ * on bad arguments. */
+int64_t apack_visual_budget(double r_pre, int64_t n_audio, int64_t n_visual);
+
+/* ------------------------------------------------------------------------ */
+/* In-LLM query-conditioned prune (Section 3.2, Eq. 5 and Eq. 6)            */
+/* ------------------------------------------------------------------------ */
+
+/* A run of rows of one modality, relative to its sequence's first row. */
+typedef struct apack_span {
+  int64_t begin;
+  int64_t len;
+  int32_t modality;  /* APACK_AUDIO, APACK_VISUAL or APACK_OTHER */
+  int32_t reserved;  /* must be 0 */
+} apack_span;
+
+/* One sequence of a (possibly ragged) packed batch at a prune layer. */
+typedef struct apack_seq {
+  int64_t tok_off;          /* first row of the sequence in the packed K     */
+  int64_t n_tokens;         /* rows of the sequence (N)                      */
+  const apack_span* spans;  /* HOST; ascending, disjoint, inside [0, N)      */
+  int32_t n_spans;
+  int32_t reserved;         /* must be 0                                     */
+  int64_t q_off;            /* first query row of the sequence in packed Q   */
+  int64_t q_len;            /* query rows (>= 1); 1 = the paper's last query */
+  double keep[2];           /* keep ratio for [audio, visual], in [0, 1]     */
+  int64_t keep_basis[2];    /* n in ceil(keep*n); 0 = current modality count */
+} apack_seq;
+
+/* Validates `seqs` for a prune step and reports the kept-row count of every
+ * sequence (n_kept, HOST [n_seq], may be NULL) and the workspace size that
+ * apack_prune_layer needs (workspace_bytes, may be NULL). */
+apack_status apack_prune_layer_query(int32_t n_seq, const apack_seq* seqs,
+                                     int32_t hq, int32_t hkv, int32_t d,
+                                     int64_t* n_kept, size_t* workspace_bytes);
+
+/* Scores the candidate rows S (audio and visual rows) of every sequence by
+ * the attention mass of its query rows (Eq. 5), averaged over all hq heads
+ * and q_len query rows, and selects per modality the ceil(keep*n) highest
+ * (Eq. 6 applied within each modality; ties go to the lower row).
+ *
+ *   q       [hq][q_rows][d] query projections of the query span (post-RoPE,
+ *           as the decoder holds them); head h starts at q + h*q_head_stride
+ *           elements, rows are contiguous d-element vectors.
+ *   k       [hkv][k_rows][d] keys of the prune layer (post-RoPE); head g
+ *           starts at k + g*k_head_stride elements.  Query head h reads key
+ *           head h / (hq/hkv).  Logits are q.k / sqrt(d).
+ *   scores  [k_rows] fp32 out: I_j for candidate rows of every sequence,
+ *           0 for its other rows; rows outside every sequence are untouched.
+ *   kept_rows  int32 out: for each sequence in order, the ascending packed
+ *           rows (tok_off + local row) it keeps: every non-candidate row and
+ *           the selected audio and visual rows.  kept_capacity >= sum n_kept.
+ *   n_kept  HOST [n_seq] out (may be NULL).
+ *
+ * dtype: APACK_BF16 or APACK_F32 for both q and k; d must be 64 or 128.
+ * Row counts: q_off+q_len <= q_rows, tok_off+n_tokens <= k_rows, head
+ * strides >= rows*d; sequences may not overlap in k.
+ */
+apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype dtype,
+                               int32_t hq, int32_t hkv, int32_t d,
+                               const void* q, int64_t q_head_stride, int64_t q_rows,
+                               const void* k, int64_t k_head_stride, int64_t k_rows,
+                               float* scores, int32_t* kept_rows, int64_t kept_capacity,
+                               int64_t* n_kept,
+                               void* workspace, size_t workspace_bytes, void* stream);
+
+/* Gathers rows: out[i] = in[src_rows[i]] for i < n_out, on raw bits, for
+ *   - every K and V tensor of n_layers layers, each [hkv][rows][d] with head
+ *     strides head_stride_in / head_stride_out (elements);
+ *   - the hidden states [rows][hidden_dim] (hidden_in/hidden_out, nullable
+ *     pair; hidden_dim 0 when absent);
+ *   - the position ids [pos_rows][rows] int32 (nullable pair; row strides
+ *     pos_stride_in / pos_stride_out elements; 3 rows for TMRoPE ids).
+ * src_rows is a DEVICE int32 array of n_out indices into [0, n_in), usually
+ * apack_prune_layer's kept_rows; an index outside [0, n_in) copies nothing
+ * for that row.  k_in, v_in, k_out, v_out are HOST arrays of n_layers device
+ * pointers (n_layers <= 64).  Outputs may not overlap inputs
+ * (APACK_E_ALIAS): compaction is out of place.
+ */
+apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows, int64_t n_in,
+                              int32_t n_layers,
+                              const void* const* k_in, const void* const* v_in,
+                              void* const* k_out, void* const* v_out,
+                              int32_t hkv, int32_t d, apack_dtype dtype,
+                              int64_t head_stride_in, int64_t head_stride_out,
+                              const void* hidden_in, void* hidden_out, int32_t hidden_dim,
+                              const int32_t* pos_in, int32_t* pos_out, int32_t pos_rows,
+                              int64_t pos_stride_in, int64_t pos_stride_out,
+                              void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Pre-LLM local audio-visual dynamics scorer (Section 3.1)                 */
+/* ------------------------------------------------------------------------ */
+
+/* Hyper-parameters of the pre-LLM stage (Table S1). */
+typedef struct apack_dyn_params {
+  int32_t window;       /* w: frames per CKA window (3)                       */
+  int32_t dafps_k;      /* neighbours in the DA-FPS density (5)               */
+  double tau_gate;      /* CKA gate tau (0.78): fires when mean c_f < tau     */
+  double beta;          /* fine-blend weight beta (0.90), Eq. 2               */
+  double gamma;         /* visual-score weight gamma (0.9)                    */
+  double tau_sim;       /* continuity threshold (0.97)                        */
+  double sigma;         /* continuity smoothing width (1.0)                   */
+  double lambda_seg;    /* peak/sustained balance lambda in Eq. 3 (0.5)       */
+  double cover_thresh;  /* DA-FPS coverage cosine threshold (0.8)             */
+  double dafps_power;   /* power on the DA-FPS density (0.5)                  */
+  double r_pre;         /* pre-LLM joint retention R_pre (0.50)               */
+} apack_dyn_params;
+
+void apack_dyn_params_default(apack_dyn_params* p);
+
+/* One clip of a packed batch. */
+typedef struct apack_av_seq {
+  int32_t n_frames;          /* F                                              */
+  int32_t tokens_per_frame;  /* P (visual tokens of one frame, <= 256)         */
+  int64_t n_audio;           /* N_A (>= 1)                                     */
+  int64_t n_query;           /* query-span rows (>= 1)                         */
+  int64_t vis_off;           /* first row of the clip in packed visual         */
+  int64_t aud_off;           /* first row of the clip in packed audio          */
+  int64_t qry_off;           /* first row of the clip in packed query          */
+} apack_av_seq;
+
+/* Validates and reports each clip's visual budget B_v (n_kept_visual, HOST
+ * [n_seq], may be NULL) and the workspace size apack_score_dynamics needs. */
+apack_status apack_score_dynamics_query(int32_t n_seq, const apack_av_seq* seqs, int32_t dim,
+                                        const apack_dyn_params* p,
+                                        int64_t* n_kept_visual, size_t* workspace_bytes);
+
+/* Per clip: frame pooling and audio resampling (coarse pass), window CKA
+ * c_f (Eq. 1), the gate and direct audio-visual distance (Eq. 2),
+ * continuity segmentation, segment scores (Eq. 3), segment and frame
+ * budgets (Eq. 4) and anchor DA-FPS / non-anchor dedup token selection.
+ *
+ *   visual [visual_rows][dim], audio [audio_rows][dim], query
+ *   [query_rows][dim]: embeddings, row-major, dtype APACK_BF16 or APACK_F32.
+ *   Frame arrays are [sum F], clip s starting at the sum of the previous
+ *   clips' F: frame_cka c_f, frame_score s_f, frame_budget k_f and
+ *   segment_id (0-based within the clip) -- each nullable.
+ *   gate_fired [n_seq] (nullable).
+ *   kept_visual int32 out: for each clip in order, the ascending packed
+ *   visual rows (vis_off + f*P + p) it keeps; kept_capacity >= sum B_v.
+ *   n_kept_visual HOST [n_seq] out (may be NULL).
+ * dim must be a multiple of 8 and at most 8192.
+ */
+apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack_dtype dtype,
+                                  int32_t dim,
+                                  const void* visual, int64_t visual_rows,
+                                  const void* audio, int64_t audio_rows,
+                                  const void* query, int64_t query_rows,
+                                  const apack_dyn_params* p,
+                                  float* frame_cka, float* frame_score, int32_t* frame_budget,
+                                  int32_t* segment_id, uint8_t* gate_fired,
+                                  int32_t* kept_visual, int64_t kept_capacity,
+                                  int64_t* n_kept_visual,
+                                  void* workspace, size_t workspace_bytes, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* APACK_H */

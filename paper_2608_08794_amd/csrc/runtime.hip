@@ -1,0 +1,154 @@
+// Host runtime of libapack: thread-local errors, version, helper counts and
+// the pinned staging pool.
+#include <cmath>
+#include <mutex>
+#include <vector>
+
+#include "common.hpp"
+
+namespace apack {
+
+static thread_local std::string g_error;
+
+apack_status fail(apack_status s, const char* fmt, ...) {
+  char buf[1024];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_error = buf;
+  return s;
+}
+
+void clear_error() { g_error.clear(); }
+
+apack_status launch_status(const char* what) {
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess) return fail(APACK_E_HIP, "launch of %s failed: %s", what, hipGetErrorString(e));
+  return APACK_OK;
+}
+
+// ---------------------------------------------------------------------------
+// Pinned staging pool.  Blocks are reused once the event recorded after their
+// last upload has completed; a busy pool grows instead of waiting.
+// ---------------------------------------------------------------------------
+struct Staging {
+  void* host = nullptr;
+  size_t cap = 0;
+  int device = -1;
+  hipEvent_t done = nullptr;
+  bool busy = false;
+};
+
+static std::mutex g_pool_mu;
+static std::vector<Staging*> g_pool;
+
+apack_status staging_acquire(size_t bytes, Staging** blk, void** host) {
+  int dev = 0;
+  APACK_HIP(hipGetDevice(&dev));
+  std::lock_guard<std::mutex> lk(g_pool_mu);
+  for (Staging* s : g_pool) {
+    if (s->device != dev || s->cap < bytes) continue;
+    if (s->busy) {
+      hipError_t q = hipEventQuery(s->done);
+      if (q == hipErrorNotReady) continue;
+      if (q != hipSuccess) return fail(APACK_E_HIP, "hipEventQuery: %s", hipGetErrorString(q));
+      s->busy = false;
+    }
+    s->busy = true;
+    *blk = s;
+    *host = s->host;
+    return APACK_OK;
+  }
+  auto* s = new Staging();
+  s->cap = align_up(bytes < 65536 ? 65536 : bytes, 65536);
+  s->device = dev;
+  hipError_t e = hipHostMalloc(&s->host, s->cap, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    delete s;
+    return fail(APACK_E_HIP, "hipHostMalloc(%zu): %s", bytes, hipGetErrorString(e));
+  }
+  e = hipEventCreateWithFlags(&s->done, hipEventDisableTiming);
+  if (e != hipSuccess) {
+    (void)hipHostFree(s->host);
+    delete s;
+    return fail(APACK_E_HIP, "hipEventCreate: %s", hipGetErrorString(e));
+  }
+  s->busy = true;
+  g_pool.push_back(s);
+  *blk = s;
+  *host = s->host;
+  return APACK_OK;
+}
+
+apack_status staging_upload(Staging* blk, void* dst, size_t bytes, hipStream_t stream) {
+  hipError_t e = hipMemcpyAsync(dst, blk->host, bytes, hipMemcpyHostToDevice, stream);
+  if (e == hipSuccess) e = hipEventRecord(blk->done, stream);
+  if (e != hipSuccess) {
+    std::lock_guard<std::mutex> lk(g_pool_mu);
+    blk->busy = false;  // nothing was enqueued that still reads the block
+    return fail(APACK_E_HIP, "staging upload: %s", hipGetErrorString(e));
+  }
+  return APACK_OK;
+}
+
+}  // namespace apack
+
+using namespace apack;
+
+extern "C" {
+
+const char* apack_version(void) { return "apack 0.1 (gfx950)"; }
+
+const char* apack_last_error(void) { return g_error.c_str(); }
+
+const char* apack_status_string(apack_status s) {
+  switch (s) {
+    case APACK_OK: return "ok";
+    case APACK_E_ARG: return "bad argument";
+    case APACK_E_SHAPE: return "inconsistent shapes";
+    case APACK_E_DTYPE: return "bad dtype";
+    case APACK_E_WORKSPACE: return "workspace too small or misaligned";
+    case APACK_E_ALIAS: return "output overlaps input";
+    case APACK_E_HIP: return "HIP runtime error";
+    case APACK_E_UNSUPPORTED: return "unsupported configuration";
+  }
+  return "unknown status";
+}
+
+int64_t apack_keep_count(double keep, int64_t n) {
+  if (!(keep >= 0.0 && keep <= 1.0) || n < 0) return -1;
+  const double x = keep * static_cast<double>(n);
+  const double slack = std::ldexp(static_cast<double>(n), -50);
+  int64_t k = static_cast<int64_t>(std::ceil(x - slack));
+  if (k < 0) k = 0;
+  if (k > n) k = n;
+  return k;
+}
+
+int64_t apack_visual_budget(double r_pre, int64_t n_audio, int64_t n_visual) {
+  if (n_audio < 0 || n_visual < 0) return -1;
+  int64_t b = apack_keep_count(r_pre, n_audio + n_visual);
+  if (b < 0) return -1;
+  b -= n_audio;
+  if (b < 0) b = 0;
+  if (b > n_visual) b = n_visual;
+  return b;
+}
+
+void apack_dyn_params_default(apack_dyn_params* p) {
+  if (!p) return;
+  p->window = 3;
+  p->dafps_k = 5;
+  p->tau_gate = 0.78;
+  p->beta = 0.90;
+  p->gamma = 0.9;
+  p->tau_sim = 0.97;
+  p->sigma = 1.0;
+  p->lambda_seg = 0.5;
+  p->cover_thresh = 0.8;
+  p->dafps_power = 0.5;
+  p->r_pre = 0.50;
+}
+
+}  // extern "C"

@@ -1,0 +1,203 @@
+"""CPU-only checks of the C ABI: symbols, host helpers and validation paths.
+
+Validation runs on the host before anything is enqueued, so every error path
+can be forced here with fake device addresses: no call below reaches HIP.
+"""
+
+import ctypes
+import math
+import os
+import re
+from fractions import Fraction
+
+import pytest
+
+from oracle import prune as OP
+from oracle import dynamics as OD
+import paper_2608_08794_amd as A
+from paper_2608_08794_amd import _lib as L
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def _declared_functions():
+    text = open(os.path.join(ROOT, "include", "apack.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(apack_[a-z_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = A.library()
+    names = _declared_functions()
+    assert "apack_prune_layer" in names and "apack_compact_kv" in names and "apack_score_dynamics" in names
+    for name in names:
+        assert hasattr(lib, name), name
+    assert b"gfx950" in lib.apack_version()
+
+
+def test_keep_count_matches_oracle_decimal_ceiling():
+    lib = A.library()
+    for pct in range(0, 101, 5):
+        keep = pct / 100.0
+        for n in list(range(0, 2500)) + [7500, 8640, 17280, 60480, 86400, 93900, 94028, 200000]:
+            assert lib.apack_keep_count(keep, n) == OP.keep_count(keep, n), (keep, n)
+    for keep in (0.123456, 0.333333, 0.999999, 0.000001):
+        for n in (1, 7, 999, 123457, 10**6, 10**8):
+            assert lib.apack_keep_count(keep, n) == math.ceil(Fraction(str(keep)) * n), (keep, n)
+    assert lib.apack_keep_count(-0.1, 10) == -1
+    assert lib.apack_keep_count(1.5, 10) == -1
+    assert lib.apack_keep_count(0.5, -1) == -1
+
+
+def test_visual_budget_matches_oracle():
+    lib = A.library()
+    for r_pre in (0.35, 0.5, 0.51, 0.365, 0.1, 1.0, 0.0):
+        for na, nv in ((1500, 17280), (7500, 86400), (500, 40), (0, 10), (10, 0)):
+            assert lib.apack_visual_budget(r_pre, na, nv) == OD.visual_budget(r_pre, na, nv)
+
+
+def test_default_params_are_table_s1():
+    p = A.apack_dyn_params_default()
+    got = {f: getattr(p, f) for f, _ in A.DynParams._fields_}
+    for key, val in OD.DEFAULTS.items():
+        assert got[key] == val, key
+
+
+# -- validation paths (fake, never dereferenced device addresses) ------------
+
+FAKE = 1 << 40
+
+
+def _seq(spans, n, q_len=4, keep=(0.5, 0.5), basis=(0, 0), tok_off=0, q_off=0, reserved=0):
+    sp = (L.Span * max(1, len(spans)))(*[L.Span(b, l, m, 0) for b, l, m in spans])
+    s = L.Seq(tok_off, n, sp, len(spans), reserved, q_off, q_len,
+              (ctypes.c_double * 2)(*keep), (ctypes.c_int64 * 2)(*basis))
+    return s, sp
+
+
+def _prune(seqs, hq=4, hkv=2, d=64, dtype=0, q=FAKE, k=FAKE + (1 << 34), scores=FAKE + (2 << 34),
+           kept=FAKE + (3 << 34), cap=1 << 20, ws=FAKE + (4 << 34), ws_bytes=1 << 30,
+           q_rows=1 << 12, k_rows=1 << 12, qhs=None, khs=None):
+    arr = (L.Seq * max(1, len(seqs)))(*seqs)
+    qhs = q_rows * d if qhs is None else qhs
+    khs = k_rows * d if khs is None else khs
+    nk = (ctypes.c_int64 * max(1, len(seqs)))()
+    st = A.library().apack_prune_layer(len(seqs), arr, dtype, hq, hkv, d, q, qhs, q_rows, k, khs, k_rows,
+                                       scores, kept, cap, nk, ws, ws_bytes, None)
+    return st, A.library().apack_last_error().decode()
+
+
+def test_prune_query_reports_counts_and_workspace():
+    s, _sp = _seq([(0, 100, 1), (100, 300, 2)], 420, keep=(0.55, 0.3))
+    arr = (L.Seq * 1)(s)
+    nk = (ctypes.c_int64 * 1)()
+    ws = ctypes.c_size_t(0)
+    assert A.library().apack_prune_layer_query(1, arr, 8, 2, 128, nk, ctypes.byref(ws)) == 0
+    assert nk[0] == 20 + 55 + 90
+    assert ws.value > 0 and ws.value % 256 == 0
+
+
+@pytest.mark.parametrize("case,status", [
+    ("hq_not_multiple", 2), ("bad_d", 7), ("bad_dtype", 3), ("span_outside", 2), ("span_unsorted", 2),
+    ("bad_modality", 1), ("keep_range", 1), ("k_exceeds", 1), ("q_len0", 2), ("q_rows", 2),
+    ("k_rows", 2), ("overlap_seqs", 2), ("small_ws", 4), ("misaligned_ws", 4), ("null_ws", 4),
+    ("small_capacity", 2), ("alias", 5), ("reserved", 1), ("misaligned_q", 1), ("null_k", 1),
+])
+def test_prune_validation_errors(case, status):
+    s, sp = _seq([(0, 10, 1), (10, 20, 2)], 40)
+    kw = {}
+    seqs = [s]
+    if case == "hq_not_multiple":
+        kw = dict(hq=6, hkv=4)
+    elif case == "bad_d":
+        kw = dict(d=96)
+    elif case == "bad_dtype":
+        kw = dict(dtype=7)
+    elif case == "span_outside":
+        seqs = [_seq([(30, 20, 2)], 40)[0]]
+    elif case == "span_unsorted":
+        seqs = [_seq([(10, 5, 2), (0, 5, 1)], 40)[0]]
+    elif case == "bad_modality":
+        seqs = [_seq([(0, 5, 3)], 40)[0]]
+    elif case == "keep_range":
+        seqs = [_seq([(0, 5, 1)], 40, keep=(1.2, 0.5))[0]]
+    elif case == "k_exceeds":
+        seqs = [_seq([(0, 5, 1)], 40, keep=(0.5, 0.5), basis=(20, 0))[0]]
+    elif case == "q_len0":
+        seqs = [_seq([(0, 5, 1)], 40, q_len=0)[0]]
+    elif case == "q_rows":
+        kw = dict(q_rows=3)
+    elif case == "k_rows":
+        kw = dict(k_rows=39)
+    elif case == "overlap_seqs":
+        seqs = [s, _seq([(0, 10, 2)], 20, tok_off=30)[0]]
+    elif case == "small_ws":
+        kw = dict(ws_bytes=100)
+    elif case == "misaligned_ws":
+        kw = dict(ws=FAKE + (4 << 34) + 8)
+    elif case == "null_ws":
+        kw = dict(ws=None)
+    elif case == "small_capacity":
+        kw = dict(cap=5)
+    elif case == "alias":
+        kw = dict(scores=FAKE + (1 << 34) + 64)
+    elif case == "reserved":
+        seqs = [_seq([(0, 5, 1)], 40, reserved=1)[0]]
+    elif case == "misaligned_q":
+        kw = dict(q=FAKE + 4)
+    elif case == "null_k":
+        kw = dict(k=None)
+    st, msg = _prune(seqs, **kw)
+    assert st == status, msg
+    assert msg
+
+
+def _compact(n_out=10, n_in=20, layers=1, src=FAKE, kin=None, kout=None, hid=(0, 0, 0), pos=(0, 0, 0),
+             hkv=2, d=64, dtype=0, hs_in=None, hs_out=None):
+    P = ctypes.c_void_p * max(1, layers)
+    base_in = FAKE + (1 << 34)
+    base_out = FAKE + (8 << 34)
+    kin = kin or [base_in + l * (1 << 30) for l in range(layers)]
+    vin = [base_in + (1 << 33) + l * (1 << 30) for l in range(layers)]
+    kout = kout or [base_out + l * (1 << 30) for l in range(layers)]
+    vout = [base_out + (1 << 33) + l * (1 << 30) for l in range(layers)]
+    hs_in = n_in * d if hs_in is None else hs_in
+    hs_out = n_out * d if hs_out is None else hs_out
+    st = A.library().apack_compact_kv(n_out, src, n_in, layers, P(*kin), P(*vin), P(*kout), P(*vout), hkv, d,
+                                      dtype, hs_in, hs_out, hid[0], hid[1], hid[2], pos[0], pos[1], pos[2],
+                                      n_in, n_out, None)
+    return st, A.library().apack_last_error().decode()
+
+
+@pytest.mark.parametrize("case,status", [
+    ("alias_kv", 5), ("alias_outputs", 5), ("alias_hidden", 5), ("too_many_layers", 1), ("null_src", 1),
+    ("bad_dtype", 3), ("stride", 2), ("null_hidden", 1), ("negative", 2),
+])
+def test_compact_validation_errors(case, status):
+    kw = {}
+    if case == "alias_kv":
+        kw = dict(kout=[FAKE + (1 << 34) + 256])
+    elif case == "alias_outputs":
+        kw = dict(layers=2, kout=[FAKE + (8 << 34), FAKE + (8 << 34) + 512])
+    elif case == "alias_hidden":
+        kw = dict(hid=(FAKE + (20 << 34), FAKE + (20 << 34) + 64, 512))
+    elif case == "too_many_layers":
+        kw = dict(layers=65)
+    elif case == "null_src":
+        kw = dict(src=None)
+    elif case == "bad_dtype":
+        kw = dict(dtype=9)
+    elif case == "stride":
+        kw = dict(hs_in=5)
+    elif case == "null_hidden":
+        kw = dict(hid=(None, FAKE + (30 << 34), 64))
+    elif case == "negative":
+        kw = dict(n_out=-1)
+    st, msg = _compact(**kw)
+    assert st == status, msg
+    assert msg
+
+
+def test_compact_with_nothing_to_copy_is_ok_without_device():
+    st, msg = _compact(n_out=0)
+    assert st == 0, msg

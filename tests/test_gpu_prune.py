@@ -1,0 +1,217 @@
+"""GPU parity of the prune path (Section 3.2, Eq. 5-6) against the fp64 oracle.
+
+Through the C ABI (ctypes binding): scores within the stated tolerance
+(2e-3 relative for bf16 inputs, 1e-5 for fp32), kept rows and compacted
+K/V/hidden/positions bit-exact.  The generators plant a score gap at every
+top-k boundary; each case first certifies that gap with the oracle.
+"""
+
+import math
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import prune as OP, widen
+from tests.gpu_util import bits, log, raw_bits, score_tol, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_08794_amd as A
+    A.library()
+
+
+def _run_prune(case, seqs=None):
+    import paper_2608_08794_amd as A
+    seqs = seqs or case.seqs
+    q = to_dev(case.q, case.dtype)
+    k = to_dev(case.k, case.dtype)
+    scores, kept, n_kept = A.apack_prune_layer(q, k, seqs)
+    torch.cuda.synchronize()
+    return scores.cpu().numpy(), kept.cpu().numpy().astype(np.int64), n_kept
+
+
+def _oracle(case, seqs=None):
+    seqs = seqs or case.seqs
+    sd = [dict(tok_off=s.tok_off, n_tokens=s.n_tokens, q_off=s.q_off, q_len=s.q_len, tags=s.tags(),
+               keep=s.keep, keep_basis=s.keep_basis) for s in seqs]
+    return OP.prune_batch(widen(case.q, case.dtype), widen(case.k, case.dtype), sd)
+
+
+def _check_scores(got, want, seqs, dtype):
+    tol = score_tol(dtype)
+    for s in seqs:
+        sl = slice(s.tok_off, s.tok_off + s.n_tokens)
+        tags = s.tags()
+        g, w = got[sl], want[sl]
+        assert np.all(g[tags == 0] == 0.0)
+        c = tags != 0
+        if c.any():
+            rel = np.abs(g[c] - w[c]) / np.abs(w[c])
+            assert rel.max() <= tol, f"max rel err {rel.max():.3g} > {tol}"
+
+
+def _parity(case, seqs=None, min_margin=1e-2):
+    seqs = seqs or case.seqs
+    log(f"[prune] {case.name} dtype={case.dtype} hq={case.hq} hkv={case.hkv} d={case.d} "
+        f"rows={case.k.shape[1]} seqs={len(seqs)}")
+    w_scores, w_kept, w_n, margins = _oracle(case, seqs)
+    if min_margin:
+        assert min(margins) >= min_margin, margins
+    g_scores, g_kept, g_n = _run_prune(case, seqs)
+    assert g_n == w_n
+    np.testing.assert_array_equal(g_kept, w_kept)
+    _check_scores(g_scores, w_scores, seqs, case.dtype)
+    return g_kept
+
+
+@pytest.mark.parametrize("fn", [W.prune_cfg1, W.prune_cfg2, W.prune_cfg3])
+def test_prune_parity_configs_1_to_3(fn):
+    _parity(fn())
+
+
+def _compact_and_check(cache, kept_rows, n_in):
+    import paper_2608_08794_amd as A
+    dt = cache.dtype
+    src = torch.from_numpy(kept_rows.astype(np.int32)).cuda()
+    k_in = [to_dev(x, dt) for x in cache.k_layers]
+    v_in = [to_dev(x, dt) for x in cache.v_layers]
+    n_out = kept_rows.size
+    k_out = [torch.empty((cache.hkv, n_out, cache.d), dtype=k_in[0].dtype, device="cuda") for _ in k_in]
+    v_out = [torch.empty_like(x) for x in k_out]
+    h_in = to_dev(cache.hidden, dt) if cache.hidden is not None else None
+    h_out = torch.empty((n_out, cache.hidden_dim), dtype=h_in.dtype, device="cuda") if h_in is not None else None
+    p_in = torch.from_numpy(cache.pos).cuda() if cache.pos is not None else None
+    p_out = torch.empty((3, n_out), dtype=torch.int32, device="cuda") if p_in is not None else None
+    A.apack_compact_kv(src, n_in, k_in, v_in, k_out, v_out, h_in, h_out, p_in, p_out)
+    torch.cuda.synchronize()
+    for l in range(len(k_in)):
+        np.testing.assert_array_equal(bits(k_out[l]), raw_bits(cache.k_layers[l], dt)[:, kept_rows])
+        np.testing.assert_array_equal(bits(v_out[l]), raw_bits(cache.v_layers[l], dt)[:, kept_rows])
+    if h_in is not None:
+        np.testing.assert_array_equal(bits(h_out), raw_bits(cache.hidden, dt)[kept_rows])
+    if p_in is not None:
+        np.testing.assert_array_equal(p_out.cpu().numpy(), cache.pos[:, kept_rows])
+
+
+@pytest.mark.parametrize("cfg", [1, 2, 3])
+def test_prune_then_compact_configs_1_to_3(cfg):
+    case = {1: W.prune_cfg1, 2: W.prune_cfg2, 3: W.prune_cfg3}[cfg]()
+    kept = _parity(case)
+    cache = W.cfg_cache(cfg, case)
+    log(f"[compact] cfg{cfg} rows {case.k.shape[1]} -> {kept.size}")
+    _compact_and_check(cache, kept, case.k.shape[1])
+
+
+# -- edge cases ---------------------------------------------------------------
+
+
+def _synthetic(dtype, hq, hkv, d, seq_specs, seed, zero_keys=False, dup=None, lift=True):
+    """Small packed batch.  seq_specs: list of (spans, n_tokens, q_len, keep)."""
+    rng = np.random.default_rng(seed)
+    seqs, tok, qrow = [], 0, 0
+    for spans, n, ql, keep in seq_specs:
+        seqs.append(W.PruneSeq(tok, n, spans, qrow, ql, keep))
+        tok += n
+        qrow += ql
+    scale = 1.0 if dtype == "f32" else 1.0 / math.sqrt(d)
+    qf = rng.standard_normal((hq, max(qrow, 1), d), dtype=np.float32) * np.float32(scale)
+    kf = rng.standard_normal((hkv, max(tok, 1), d), dtype=np.float32) * np.float32(scale)
+    top = {}
+    if lift and not zero_keys:
+        qv = W.bf16_bits_to_f32(W.to_bf16_bits(qf)) if dtype == "bf16" else qf
+        for i, s in enumerate(seqs):
+            topi = W._planted_sets(rng, s.tags(), s.keep, s.keep_basis)
+            top[i] = topi
+            if s.q_len == 0:
+                continue
+            dirs = W._group_unit_dirs(qv[:, s.q_off:s.q_off + s.q_len], hkv)
+            rows = np.concatenate([topi[1], topi[2]]).astype(np.int64)
+            if dtype == "f32":
+                n_rep = hq // hkv
+                for g in range(hkv):
+                    qf[g * n_rep:(g + 1) * n_rep, s.q_off:s.q_off + s.q_len] += np.float32(3.0) * dirs[g]
+                W._lift(kf[:, s.tok_off:s.tok_off + s.n_tokens], dirs, rows, 8.0)
+            else:
+                W._lift(kf[:, s.tok_off:s.tok_off + s.n_tokens], dirs, rows, W.LIFT_BF16_BOUNDARY)
+    if zero_keys:
+        kf[:] = 0
+    if dup is not None:
+        for a, b in dup:
+            kf[:, b] = kf[:, a]
+    q = W.to_bf16_bits(qf) if dtype == "bf16" else qf
+    k = W.to_bf16_bits(kf) if dtype == "bf16" else kf
+    return W.PruneCase("synthetic", dtype, hq, hkv, d, q, k, seqs, top)
+
+
+A_, V_, O_ = 1, 2, 0
+
+
+@pytest.mark.parametrize("dtype,d", [("bf16", 64), ("bf16", 128), ("f32", 64), ("f32", 128)])
+def test_ragged_batch_interleaved_spans(dtype, d):
+    specs = [
+        ([(0, 50, V_), (50, 13, A_), (63, 70, V_), (133, 12, A_)], 160, 9, (0.5, 0.3)),
+        ([(3, 200, A_), (210, 333, V_)], 560, 1, (0.35, 0.8)),          # paper's single query row
+        ([], 17, 5, (0.5, 0.5)),                                        # no candidates
+        ([(0, 0, A_)], 0, 3, (0.5, 0.5)),                               # empty sequence
+        ([(0, 700, V_), (700, 64, A_)], 800, 100, (0.7, 0.15)),         # 700 rows per group: 2 row groups
+    ]
+    case = _synthetic(dtype, 14, 2, d, specs, seed=11)
+    _parity(case)
+
+
+def test_exact_ties_keep_lowest_rows():
+    specs = [([(0, 100, A_), (100, 250, V_)], 400, 7, (0.33, 0.5))]
+    case = _synthetic("bf16", 8, 2, 128, specs, seed=12, zero_keys=True)
+    w_scores, w_kept, _, _ = _oracle(case)
+    g_scores, g_kept, _ = _run_prune(case)
+    tags = case.seqs[0].tags()
+    # every candidate score is bitwise identical on the GPU
+    assert len(set(g_scores[tags != 0].tolist())) == 1
+    np.testing.assert_array_equal(g_kept, w_kept)
+    assert w_kept.tolist() == list(range(0, 33)) + list(range(100, 225)) + list(range(350, 400))
+
+
+def test_duplicate_keys_straddling_the_boundary():
+    # The lowest-scoring planted audio row `a` gets a twin `b` outside the
+    # planted set: the twins tie exactly at the k boundary and the lower row
+    # must win.
+    spec = [([(0, 64, A_), (64, 128, V_)], 200, 16, (0.5, 0.5))]
+    base = _synthetic("bf16", 8, 2, 128, spec, seed=13)
+    sc, _, _, _ = _oracle(base)
+    top = base.planted[0][A_]
+    a = int(top[np.argmin(sc[top])])
+    b = int([r for r in range(64) if r not in set(top.tolist())][0])
+    case = _synthetic("bf16", 8, 2, 128, spec, seed=13, dup=[(a, b)])
+    w_scores, w_kept, _, _ = _oracle(case)
+    assert w_scores[a] == w_scores[b]
+    assert (min(a, b) in w_kept) and (max(a, b) not in w_kept)
+    g_scores, g_kept, _ = _run_prune(case)
+    assert g_scores[a] == g_scores[b]
+    np.testing.assert_array_equal(g_kept, w_kept)
+    _check_scores(g_scores, w_scores, case.seqs, "bf16")
+
+
+def test_keep_zero_and_keep_all():
+    specs = [([(0, 90, A_), (90, 310, V_)], 420, 12, (0.0, 1.0)),
+             ([(0, 90, A_), (90, 310, V_)], 420, 12, (1.0, 0.0))]
+    case = _synthetic("bf16", 4, 4, 128, specs, seed=14, lift=False)
+    _parity(case, min_margin=0)
+
+
+def test_cumulative_keep_basis():
+    case = _synthetic("bf16", 8, 2, 128, [([(0, 300, A_), (300, 500, V_)], 830, 20, (0.5, 0.5))], seed=15,
+                      lift=False)
+    s = case.seqs[0]
+    seqs = [W.PruneSeq(s.tok_off, s.n_tokens, s.spans, s.q_off, s.q_len, (0.3, 0.3), (400, 700))]
+    w_scores, w_kept, w_n, _ = _oracle(case, seqs)
+    g_scores, g_kept, g_n = _run_prune(case, seqs)
+    assert g_n == w_n == [30 + 120 + 210]
+    _check_scores(g_scores, w_scores, seqs, "bf16")

@@ -51,8 +51,9 @@ def payload_bits(rng, shape, dtype):
     cleared).  f32: standard normal values.
     """
     if dtype == "bf16":
-        bits = rng.integers(0, 1 << 16, size=shape, dtype=np.uint16)
-        return bits & np.uint16(0xBFFF)
+        n = int(np.prod(shape))
+        words = rng.bit_generator.random_raw((n + 3) // 4).view(np.uint16)[:n]
+        return (words & np.uint16(0xBFFF)).reshape(shape)
     return rng.standard_normal(shape, dtype=np.float32)
 
 

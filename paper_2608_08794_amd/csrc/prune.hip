@@ -14,10 +14,8 @@
 //   k_colsum     pass 2: recomputes the logits with the roles of the MFMA
 //                operands swapped so the per-key sum over query rows is
 //                lane-local, then a fixed-order cross-wave sum through LDS.
-//   k_finalize   sums the per-group partials in a fixed order into I_j.
-//   k_select     per (sequence, modality): 4-pass 8-bit radix select over the
-//                fp32 score bits (scores are >= 0, so the bits are ordered).
-//   k_scan       per sequence: keep mask and ordered compaction of kept rows.
+// The per-group partials are summed into I_j, and the per-modality top-k and
+// ordered kept list are formed, by the kernels of select.hip.
 #include <cfloat>
 #include <cmath>
 #include <vector>
@@ -79,6 +77,8 @@ struct QFrags {
   typename Mma<T>::frag v[2][TileGeom<T, D>::kSteps];
 };
 
+// Rows past the group's end read a clamped, valid row and are zeroed after
+// the (unconditional) loads, so all loads of a lane are in flight together.
 template <class T, int D>
 __device__ __forceinline__ void load_q(QFrags<T, D>& qfr, const T* q, int64_t q_hs, const SeqDev& sq, int g,
                                        int n_rep, int row0, int lane) {
@@ -88,13 +88,17 @@ __device__ __forceinline__ void load_q(QFrags<T, D>& qfr, const T* q, int64_t q_
 #pragma unroll
   for (int rb = 0; rb < 2; ++rb) {
     const int rho = row0 + rb * 32 + (lane & 31);
-    const bool ok = rho < rows;
-    const int h = g * n_rep + (ok ? rho / sq.q_len : 0);
-    const int t = ok ? rho % sq.q_len : 0;
+    const int rc = rho < rows ? rho : rows - 1;
+    const int h = g * n_rep + rc / sq.q_len;
+    const int t = rc % sq.q_len;
     const T* src = q + (int64_t)h * q_hs + (sq.q_off + t) * (int64_t)D + (lane >> 5) * M::lane_k;
 #pragma unroll
     for (int ks = 0; ks < TileGeom<T, D>::kSteps; ++ks)
-      qf[rb][ks] = ok ? *reinterpret_cast<const typename M::frag*>(src + ks * M::kstep) : M::zero();
+      qf[rb][ks] = *reinterpret_cast<const typename M::frag*>(src + ks * M::kstep);
+    if (rho >= rows) {
+#pragma unroll
+      for (int ks = 0; ks < TileGeom<T, D>::kSteps; ++ks) qf[rb][ks] = M::zero();
+    }
   }
 }
 
@@ -132,13 +136,21 @@ __device__ __forceinline__ typename Mma<T>::frag lds_frag(const char* lds, int k
   return *reinterpret_cast<const typename M::frag*>(p);
 }
 
-__device__ __forceinline__ void row_of(const SeqDev& sq, int g, int n_rep, int rho, int& r) {
-  const int h = g * n_rep + rho / sq.q_len;
-  r = h * sq.q_len + rho % sq.q_len;
-}
+// K fragments of one block of 32 keys, read from LDS in one batch.
+template <class T, int D>
+struct KFrags {
+  typename Mma<T>::frag v[TileGeom<T, D>::kSteps];
+  __device__ __forceinline__ void load(const char* lds, int kb, int lane) {
+#pragma unroll
+    for (int ks = 0; ks < TileGeom<T, D>::kSteps; ++ks) v[ks] = lds_frag<T, D>(lds, kb * 32 + (lane & 31), ks, lane);
+  }
+};
+
+__device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
 // ---------------------------------------------------------------------------
 // Pass 1: per query row, online max and sum of exp2 over one key chunk.
+// C = K Q^T: lane (l % 32) owns a query column and 16 key rows per block.
 // ---------------------------------------------------------------------------
 template <class T, int D, int NW>
 __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restrict__ seqs,
@@ -150,15 +162,18 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
                                                          float2* __restrict__ stats) {
   using G = TileGeom<T, D>;
   using M = Mma<T>;
+  constexpr int NKB = kKeyTile / 32;
   __shared__ __attribute__((aligned(16))) char lds[2][G::kTileBytes];
-  __shared__ uint8_t ltag[2][kKeyTile];
+  __shared__ __attribute__((aligned(16))) float lmask[2][kKeyTile];
+  __shared__ int lmasked[2];
 
   const TileDev tl = tiles[blockIdx.x];
   const SeqDev sq = seqs[tl.seq];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rows_g = n_rep * sq.q_len;
+  const int rg_end = min(rows_g, (tl.rg + 1) * sq.rows_per_rg);
   const int row0 = tl.rg * sq.rows_per_rg + wave * 64;
-  const bool active = row0 < rows_g && row0 < (tl.rg + 1) * sq.rows_per_rg;
+  const bool active = row0 < rg_end;
 
   QFrags<T, D> qfr;
   auto& qf = qfr.v;
@@ -179,39 +194,51 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
     const int buf = it & 1;
     const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
     st.store(lds[buf], tid);
-    if (tid < kKeyTile) ltag[buf][tid] = (t0 + tid < key_end) ? tg[t0 + tid] : 0;
+    if (tid < kKeyTile) {
+      const bool cand = (t0 + tid < key_end) && tg[t0 + tid] != 0;
+      lmask[buf][tid] = cand ? 0.0f : -INFINITY;
+      const uint64_t bal = __ballot(!cand);
+      if (tid == 0) lmasked[buf] = bal != 0;
+    }
     __syncthreads();
     if (it + 1 < n_tiles) st.load(kbase, t0 + kKeyTile, key_end, tid);
     if (active) {
+      const bool masked = lmasked[buf] != 0;
 #pragma unroll
-      for (int kb = 0; kb < kKeyTile / 32; ++kb) {
+      for (int kb = 0; kb < NKB; ++kb) {
+        KFrags<T, D> kf;
+        kf.load(lds[buf], kb, lane);
         f32x16 acc[2] = {f32x16{}, f32x16{}};
 #pragma unroll
         for (int ks = 0; ks < G::kSteps; ++ks) {
-          const auto kf = lds_frag<T, D>(lds[buf], kb * 32 + (lane & 31), ks, lane);
-          acc[0] = M::mma(kf, qf[0][ks], acc[0]);
-          acc[1] = M::mma(kf, qf[1][ks], acc[1]);
+          acc[0] = M::mma(kf.v[ks], qf[0][ks], acc[0]);
+          acc[1] = M::mma(kf.v[ks], qf[1][ks], acc[1]);
         }
         // acc[rb][e]: query column (lane % 32) of block rb, key row
         // kb*32 + 8*(e/4) + 4*(lane/32) + e%4.
-        bool valid[16];
+        if (masked) {
 #pragma unroll
-        for (int e = 0; e < 16; ++e)
-          valid[e] = ltag[buf][kb * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)] != 0;
+          for (int i = 0; i < 4; ++i) {
+            const float4 mk = *reinterpret_cast<const float4*>(&lmask[buf][kb * 32 + 8 * i + 4 * (lane >> 5)]);
+#pragma unroll
+            for (int rb = 0; rb < 2; ++rb) {
+              acc[rb][4 * i + 0] += mk.x;
+              acc[rb][4 * i + 1] += mk.y;
+              acc[rb][4 * i + 2] += mk.z;
+              acc[rb][4 * i + 3] += mk.w;
+            }
+          }
+        }
 #pragma unroll
         for (int rb = 0; rb < 2; ++rb) {
-          float x[16];
-          float lmax = -FLT_MAX;
+          float lmax = acc[rb][0];
 #pragma unroll
-          for (int e = 0; e < 16; ++e) {
-            x[e] = valid[e] ? acc[rb][e] * scale_log2 : -INFINITY;
-            lmax = fmaxf(lmax, x[e]);
-          }
-          const float m_new = fmaxf(m_run[rb], lmax);
-          float s = s_run[rb] * exp2f(m_run[rb] - m_new);
+          for (int e = 1; e < 16; ++e) lmax = fmaxf(lmax, acc[rb][e]);
+          const float m_new = fmaxf(m_run[rb], lmax * scale_log2);
+          float s = 0.f;
 #pragma unroll
-          for (int e = 0; e < 16; ++e) s += exp2f(x[e] - m_new);
-          s_run[rb] = s;
+          for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(acc[rb][e], scale_log2, -m_new));
+          s_run[rb] = s_run[rb] * fast_exp2(m_run[rb] - m_new) + s;
           m_run[rb] = m_new;
         }
       }
@@ -223,29 +250,27 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
     const float mo = __shfl_xor(m_run[rb], 32);
     const float so = __shfl_xor(s_run[rb], 32);
     const float mm = fmaxf(m_run[rb], mo);
-    const float ss = s_run[rb] * exp2f(m_run[rb] - mm) + so * exp2f(mo - mm);
+    const float ss = s_run[rb] * fast_exp2(m_run[rb] - mm) + so * fast_exp2(mo - mm);
     const int rho = row0 + rb * 32 + lane;
-    if (lane < 32 && rho < rows_g && rho < (tl.rg + 1) * sq.rows_per_rg) {
-      int r;
-      row_of(sq, tl.g, n_rep, rho, r);
-      stats[sq.stats_off + (int64_t)r * sq.n_chunks + tl.chunk] = make_float2(mm, ss);
-    }
+    if (lane < 32 && rho < rg_end)
+      stats[sq.stats_off + ((int64_t)tl.g * sq.rows_pad + rho) * sq.n_chunks + tl.chunk] = make_float2(mm, ss);
   }
 }
 
 // ---------------------------------------------------------------------------
-// Combine chunk partials of every query row: b_r = M_r + log2(Z_r).
+// Combine chunk partials of every (group, padded row): b = M + log2(Z);
+// padding rows get +inf so they contribute exp2(-inf) = 0 in pass 2.
 // One wave per row; lanes stride the chunks; fixed-order tree merge.
 // ---------------------------------------------------------------------------
 __device__ __forceinline__ void merge(float& m, float& s, float mo, float so) {
   const float mm = fmaxf(m, mo);
-  s = s * exp2f(m - mm) + so * exp2f(mo - mm);
+  s = s * fast_exp2(m - mm) + so * fast_exp2(mo - mm);
   m = mm;
 }
 
 __global__ __launch_bounds__(256) void k_rowreduce(const SeqDev* __restrict__ seqs, int n_seq,
-                                                   int64_t total_rows, const float2* __restrict__ stats,
-                                                   float* __restrict__ bias) {
+                                                   int64_t total_rows, int n_rep,
+                                                   const float2* __restrict__ stats, float* __restrict__ bias) {
   const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
   const int lane = threadIdx.x & 63;
   if (row >= total_rows) return;
@@ -255,10 +280,13 @@ __global__ __launch_bounds__(256) void k_rowreduce(const SeqDev* __restrict__ se
     if (seqs[mid].bias_off <= row) lo = mid; else hi = mid - 1;
   }
   const SeqDev& sq = seqs[lo];
-  const int64_t r = row - sq.bias_off;
-  const float2* p = stats + sq.stats_off + r * sq.n_chunks;
+  const int64_t r = row - sq.bias_off;            // g * rows_pad + rho
+  const int rho = (int)(r % sq.rows_pad);
   float m = -FLT_MAX, s = 0.f;
-  for (int c = lane; c < sq.n_chunks; c += 64) merge(m, s, p[c].x, p[c].y);
+  if (rho < n_rep * sq.q_len) {
+    const float2* p = stats + sq.stats_off + r * sq.n_chunks;
+    for (int c = lane; c < sq.n_chunks; c += 64) merge(m, s, p[c].x, p[c].y);
+  }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) {
     const float mo = __shfl_xor(m, off), so = __shfl_xor(s, off);
@@ -269,11 +297,13 @@ __global__ __launch_bounds__(256) void k_rowreduce(const SeqDev* __restrict__ se
 
 // ---------------------------------------------------------------------------
 // Pass 2: per key, sum over this group's query rows of exp2(x - b_r).
+// C = Q K^T: lane (l % 32) owns a key column and 16 query rows per block.
+// The exponentials of one (key block, row block) run while the MFMAs of
+// the next pair are in flight.
 // ---------------------------------------------------------------------------
 template <class T, int D, int NW>
 __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict__ seqs,
                                                        const TileDev* __restrict__ tiles,
-                                                       const uint8_t* __restrict__ tags,
                                                        const T* __restrict__ q, int64_t q_hs,
                                                        const T* __restrict__ k, int64_t k_hs,
                                                        int n_rep, float scale_log2,
@@ -281,6 +311,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
                                                        float* __restrict__ colpart) {
   using G = TileGeom<T, D>;
   using M = Mma<T>;
+  constexpr int NKB = kKeyTile / 32;
   __shared__ __attribute__((aligned(16))) char lds[2][G::kTileBytes];
   __shared__ float red[2][NW][kKeyTile];
 
@@ -298,18 +329,16 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
   float b[2][16];
   if (active) {
     load_q<T, D>(qfr, q, q_hs, sq, tl.g, n_rep, row0, lane);
+    const float* bb = bias + sq.bias_off + (int64_t)tl.g * sq.rows_pad + row0 + 4 * (lane >> 5);
 #pragma unroll
     for (int rb = 0; rb < 2; ++rb)
 #pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int rho = row0 + rb * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        float v = INFINITY;
-        if (rho < rg_end) {
-          int r;
-          row_of(sq, tl.g, n_rep, rho, r);
-          v = bias[sq.bias_off + r];
-        }
-        b[rb][e] = v;
+      for (int i = 0; i < 4; ++i) {
+        const float4 v = *reinterpret_cast<const float4*>(bb + rb * 32 + 8 * i);
+        b[rb][4 * i + 0] = v.x;
+        b[rb][4 * i + 1] = v.y;
+        b[rb][4 * i + 2] = v.z;
+        b[rb][4 * i + 3] = v.w;
       }
   }
 
@@ -336,23 +365,41 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
     }
     if (it + 1 < n_tiles) st.load(kbase, t0 + kKeyTile, key_end, tid);
     if (active) {
+      float cs[NKB];
+      f32x16 prev;
+      int prev_kb = -1;
 #pragma unroll
-      for (int kb = 0; kb < kKeyTile / 32; ++kb) {
-        f32x16 acc[2] = {f32x16{}, f32x16{}};
+      for (int kb = 0; kb < NKB; ++kb) {
+        KFrags<T, D> kf;
+        kf.load(lds[buf], kb, lane);
+        cs[kb] = 0.f;
 #pragma unroll
-        for (int ks = 0; ks < G::kSteps; ++ks) {
-          const auto kf = lds_frag<T, D>(lds[buf], kb * 32 + (lane & 31), ks, lane);
-          acc[0] = M::mma(qf[0][ks], kf, acc[0]);
-          acc[1] = M::mma(qf[1][ks], kf, acc[1]);
+        for (int rb = 0; rb < 2; ++rb) {
+          f32x16 acc = f32x16{};
+#pragma unroll
+          for (int ks = 0; ks < G::kSteps; ++ks) acc = M::mma(qf[rb][ks], kf.v[ks], acc);
+          if (prev_kb >= 0) {
+            // Epilogue of the previous pair: row block 1 - rb.
+            const int prb = 1 - rb;
+            float s = 0.f;
+#pragma unroll
+            for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(prev[e], scale_log2, -b[prb][e]));
+            cs[prev_kb] += s;
+          }
+          prev = acc;
+          prev_kb = kb;
         }
-        // acc[rb][e]: key column kb*32 + lane%32, query row 8*(e/4)+4*(lane/32)+e%4.
-        float cs = 0.f;
+      }
+      {
+        float s = 0.f;
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb)
+        for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(prev[e], scale_log2, -b[1][e]));
+        cs[NKB - 1] += s;
+      }
 #pragma unroll
-          for (int e = 0; e < 16; ++e) cs += exp2f(fmaf(acc[rb][e], scale_log2, -b[rb][e]));
-        cs += __shfl_xor(cs, 32);
-        if (lane < 32) red[buf][wave][kb * 32 + lane] = cs;
+      for (int kb = 0; kb < NKB; ++kb) {
+        const float c = cs[kb] + __shfl_xor(cs[kb], 32);
+        if (lane < 32) red[buf][wave][kb * 32 + lane] = c;
       }
     }
   }
@@ -363,209 +410,6 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
     float v = 0.f;
     for (int w = 0; w < n_active; ++w) v += red[buf][w][tid];
     if (key < key_end) out[key] = v;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// I_j = (sum over groups, fixed order) / (Hq * T); 0 for non-candidates.
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(256) void k_finalize(const SeqDev* __restrict__ seqs, int n_seq,
-                                                  int64_t total_tok, const uint8_t* __restrict__ tags,
-                                                  const float* __restrict__ colpart, int hq, int hkv,
-                                                  float* __restrict__ scores) {
-  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i >= total_tok) return;
-  int lo = 0, hi = n_seq - 1;
-  while (lo < hi) {
-    const int mid = (lo + hi + 1) >> 1;
-    if (seqs[mid].tag_off <= i) lo = mid; else hi = mid - 1;
-  }
-  const SeqDev& sq = seqs[lo];
-  const int64_t j = i - sq.tag_off;
-  float v = 0.f;
-  if (tags[i] != 0 && sq.n_cand > 0) {
-    const float* p = colpart + sq.colpart_off + j;
-    const int planes = hkv * sq.n_rg;
-    for (int pl = 0; pl < planes; ++pl) v += p[(int64_t)pl * sq.n_tokens];
-    v = v / (float)(hq * sq.q_len);
-  }
-  scores[sq.tok_off + j] = v;
-}
-
-// ---------------------------------------------------------------------------
-// Block-wide inclusive scan of 32-bit values (blockDim = NT, multiple of 64).
-// ---------------------------------------------------------------------------
-template <int NT>
-__device__ __forceinline__ uint32_t block_incl_scan(uint32_t v, uint32_t* sh_wave, uint32_t& total) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-#pragma unroll
-  for (int off = 1; off < 64; off <<= 1) {
-    const uint32_t o = __shfl_up(v, off);
-    if (lane >= off) v += o;
-  }
-  if (lane == 63) sh_wave[wave] = v;
-  __syncthreads();
-  uint32_t base = 0;
-  total = 0;
-#pragma unroll
-  for (int w = 0; w < NT / 64; ++w) {
-    const uint32_t x = sh_wave[w];
-    if (w < wave) base += x;
-    total += x;
-  }
-  __syncthreads();
-  return v + base;
-}
-
-// ---------------------------------------------------------------------------
-// Radix select of the k-th largest score bits of (sequence, modality).
-// ---------------------------------------------------------------------------
-constexpr int kSelThreads = 1024;
-
-__global__ __launch_bounds__(kSelThreads) void k_select(SeqDev* __restrict__ seqs,
-                                                        const uint8_t* __restrict__ tags,
-                                                        const float* __restrict__ scores) {
-  const int s = blockIdx.x >> 1, mi = blockIdx.x & 1;
-  SeqDev* sq = &seqs[s];
-  if (!sq->select[mi]) return;
-  const uint8_t mod = (uint8_t)(mi + 1);
-  const uint8_t* tg = tags + sq->tag_off;
-  const uint32_t* sb = reinterpret_cast<const uint32_t*>(scores + sq->tok_off);
-  const int64_t n = sq->n_tokens;
-  const int tid = threadIdx.x, lane = tid & 63;
-
-  __shared__ uint32_t hist[256];
-  __shared__ uint32_t sh_wave[kSelThreads / 64];
-  __shared__ uint32_t sh_prefix, sh_kk, sh_eq;
-
-  uint32_t prefix = 0, mask = 0, kk = (uint32_t)sq->k_sel[mi], n_eq = 0;
-  for (int pass = 0; pass < 4; ++pass) {
-    const int shift = 24 - 8 * pass;
-    if (tid < 256) hist[tid] = 0;
-    __syncthreads();
-    for (int64_t base = 0; base < n; base += kSelThreads) {
-      const int64_t i = base + tid;
-      bool part = false;
-      uint32_t digit = 0;
-      if (i < n && tg[i] == mod) {
-        const uint32_t bits = sb[i];
-        if ((bits & mask) == prefix) {
-          part = true;
-          digit = (bits >> shift) & 0xFFu;
-        }
-      }
-      // Wave-aggregated increments for the few most common digits, then
-      // plain atomics for whatever is left.
-      uint64_t act = __ballot(part);
-      for (int round = 0; round < 4 && act; ++round) {
-        const int leader = __ffsll((unsigned long long)act) - 1;
-        const uint32_t ld = __shfl(digit, leader);
-        const uint64_t same = __ballot(part && digit == ld);
-        if (lane == leader) atomicAdd(&hist[ld], (uint32_t)__popcll(same));
-        if (part && digit == ld) part = false;
-        act &= ~same;
-      }
-      if (part) atomicAdd(&hist[digit], 1u);
-    }
-    __syncthreads();
-    // Digit holding the kk-th largest: scan the histogram from digit 255 down.
-    uint32_t v = 0;
-    if (tid < 256) v = hist[255 - tid];
-    uint32_t total;
-    const uint32_t cum = block_incl_scan<kSelThreads>(tid < 256 ? v : 0u, sh_wave, total);
-    if (tid < 256 && cum >= kk && cum - v < kk) {
-      const uint32_t d = 255u - (uint32_t)tid;
-      sh_prefix = prefix | (d << shift);
-      sh_kk = kk - (cum - v);
-      sh_eq = v;
-    }
-    __syncthreads();
-    prefix = sh_prefix;
-    kk = sh_kk;
-    n_eq = sh_eq;
-    mask |= 0xFFu << shift;
-    __syncthreads();
-  }
-  if (tid == 0) {
-    sq->thr[mi] = prefix;
-    sq->need[mi] = (int32_t)kk;
-    sq->all_eq[mi] = (kk == n_eq) ? 1 : 0;
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Keep mask and ordered compaction of the kept rows of one sequence.
-// ---------------------------------------------------------------------------
-constexpr int kScanThreads = 1024;
-constexpr int kScanPer = 4;
-
-__global__ __launch_bounds__(kScanThreads) void k_scan(const SeqDev* __restrict__ seqs,
-                                                       const uint8_t* __restrict__ tags,
-                                                       const float* __restrict__ scores,
-                                                       int32_t* __restrict__ kept) {
-  const SeqDev& sq = seqs[blockIdx.x];
-  const uint8_t* tg = tags + sq.tag_off;
-  const uint32_t* sb = reinterpret_cast<const uint32_t*>(scores + sq.tok_off);
-  const int64_t n = sq.n_tokens;
-  const int tid = threadIdx.x;
-  __shared__ uint32_t sh_wave[kScanThreads / 64];
-  const uint32_t thr[2] = {sq.thr[0], sq.thr[1]};
-  const uint32_t need[2] = {(uint32_t)sq.need[0], (uint32_t)sq.need[1]};
-  const bool ranked = !(sq.all_eq[0] && sq.all_eq[1]);
-  uint32_t carry_eq[2] = {0, 0};
-  uint32_t carry_keep = 0;
-  int32_t* out = kept + sq.out_off;
-
-  for (int64_t base = 0; base < n; base += (int64_t)kScanThreads * kScanPer) {
-    uint8_t mtag[kScanPer];
-    uint32_t bits[kScanPer];
-    uint32_t n_eq_a = 0, n_eq_v = 0;
-#pragma unroll
-    for (int u = 0; u < kScanPer; ++u) {
-      const int64_t i = base + (int64_t)tid * kScanPer + u;
-      mtag[u] = i < n ? tg[i] : 0xFF;
-      bits[u] = i < n ? sb[i] : 0u;
-      if (mtag[u] == 1 && bits[u] == thr[0]) ++n_eq_a;
-      if (mtag[u] == 2 && bits[u] == thr[1]) ++n_eq_v;
-    }
-    uint32_t rank[2] = {0, 0};
-    if (ranked) {
-      uint32_t tot;
-      const uint32_t packed = n_eq_a | (n_eq_v << 16);
-      const uint32_t incl = block_incl_scan<kScanThreads>(packed, sh_wave, tot);
-      const uint32_t excl = incl - packed;
-      rank[0] = carry_eq[0] + (excl & 0xFFFFu);
-      rank[1] = carry_eq[1] + (excl >> 16);
-      carry_eq[0] += tot & 0xFFFFu;
-      carry_eq[1] += tot >> 16;
-    }
-    bool keep[kScanPer];
-    uint32_t n_keep = 0;
-#pragma unroll
-    for (int u = 0; u < kScanPer; ++u) {
-      bool kp;
-      const uint8_t m = mtag[u];
-      if (m == 0xFF) kp = false;
-      else if (m == 0) kp = true;
-      else {
-        const int mi = m - 1;
-        if (bits[u] > thr[mi]) kp = true;
-        else if (bits[u] == thr[mi]) kp = (rank[mi]++ < need[mi]);
-        else kp = false;
-      }
-      keep[u] = kp;
-      n_keep += kp;
-    }
-    uint32_t tot;
-    const uint32_t incl = block_incl_scan<kScanThreads>(n_keep, sh_wave, tot);
-    uint32_t pos = carry_keep + incl - n_keep;
-#pragma unroll
-    for (int u = 0; u < kScanPer; ++u)
-      if (keep[u]) {
-        if (pos < (uint64_t)sq.n_kept) out[pos] = (int32_t)(sq.tok_off + base + (int64_t)tid * kScanPer + u);
-        ++pos;
-      }
-    carry_keep += tot;
   }
 }
 
@@ -583,11 +427,10 @@ apack_status launch_scores_t(const PrunePlan& pl, const DevPtrs& dp, const void*
     APACK_CHECK(launch_status("k_rowstats") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
     const int64_t rows = pl.total_rows;
     hipLaunchKernelGGL(k_rowreduce, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, dp.seqs,
-                       (int)pl.seqs.size(), rows, dp.stats, dp.bias);
+                       (int)pl.seqs.size(), rows, n_rep, dp.stats, dp.bias);
     APACK_CHECK(launch_status("k_rowreduce") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
     hipLaunchKernelGGL((k_colsum<T, D, NW>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles,
-                       dp.tags, (const T*)q, q_hs, (const T*)k, k_hs, n_rep, scale_log2, dp.bias,
-                       dp.colpart);
+                       (const T*)q, q_hs, (const T*)k, k_hs, n_rep, scale_log2, dp.bias, dp.colpart);
     APACK_CHECK(launch_status("k_colsum") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
   }
   return APACK_OK;
@@ -600,6 +443,7 @@ apack_status launch_scores_d(const PrunePlan& pl, const DevPtrs& dp, const void*
     case 1: return launch_scores_t<T, D, 1>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
     case 2: return launch_scores_t<T, D, 2>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
     case 4: return launch_scores_t<T, D, 4>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
+    case 7: return launch_scores_t<T, D, 7>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
     default: return launch_scores_t<T, D, 8>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
   }
 }
@@ -618,21 +462,8 @@ apack_status launch_prune(const PrunePlan& pl, const DevPtrs& dp, apack_dtype dt
     st = d == 64 ? launch_scores_d<float, 64>(pl, dp, q, q_hs, k, k_hs, n_rep, stream)
                  : launch_scores_d<float, 128>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
   if (st != APACK_OK) return st;
-  const int n_seq = (int)pl.seqs.size();
-  if (pl.total_tok > 0) {
-    hipLaunchKernelGGL(k_finalize, dim3((unsigned)((pl.total_tok + 255) / 256)), dim3(256), 0, stream,
-                       dp.seqs, n_seq, pl.total_tok, dp.tags, dp.colpart, hq, hkv, scores);
-    if ((st = launch_status("k_finalize")) != APACK_OK) return st;
-  }
-  if (pl.any_select) {
-    hipLaunchKernelGGL(k_select, dim3(2 * n_seq), dim3(kSelThreads), 0, stream, dp.seqs, dp.tags, scores);
-    if ((st = launch_status("k_select")) != APACK_OK) return st;
-  }
-  if (pl.total_tok > 0) {
-    hipLaunchKernelGGL(k_scan, dim3(n_seq), dim3(kScanThreads), 0, stream, dp.seqs, dp.tags, scores, kept);
-    if ((st = launch_status("k_scan")) != APACK_OK) return st;
-  }
-  return APACK_OK;
+  if (pl.total_tok == 0) return APACK_OK;
+  return launch_select(pl, dp, hq, hkv, scores, kept, stream);
 }
 
 }  // namespace apack

@@ -73,6 +73,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
         sd.need[m] = (int32_t)cnt[m];
       }
       sd.all_eq[m] = 1;
+      sd.kk[m] = (uint32_t)k_m[m];
       pl.any_select |= sd.select[m] != 0;
     }
     sd.n_cand = (int32_t)(cnt[0] + cnt[1]);
@@ -83,15 +84,19 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     kept += pl.n_kept[s];
     sd.tag_off = tag;
     tag += a.n_tokens;
+    sd.n_ftiles = (int32_t)((a.n_tokens + kRowTile - 1) / kRowTile);
+    for (int f = 0; f < sd.n_ftiles; ++f) pl.ftiles.push_back({s, f});
+    pl.max_tokens = std::max<int64_t>(pl.max_tokens, a.n_tokens);
     // Query-row groups: at most kMaxWaves*64 rows each.
     const int64_t rows_g = (int64_t)n_rep * a.q_len;
     const int64_t cap = (int64_t)kMaxWaves * 64;
     sd.n_rg = (int32_t)((rows_g + cap - 1) / cap);
     const int64_t per = (rows_g + sd.n_rg - 1) / sd.n_rg;
     sd.rows_per_rg = (int32_t)((per + 63) / 64 * 64);
+    sd.rows_pad = sd.n_rg * sd.rows_per_rg;
     waves = std::max<int>(waves, sd.rows_per_rg / 64);
     sd.bias_off = rows;
-    rows += (int64_t)hq * a.q_len;
+    rows += (int64_t)hkv * sd.rows_pad;
     if (sd.n_cand > 0) weighted += a.n_tokens * (int64_t)hkv * sd.n_rg;
   }
   // Sequences may not overlap in K (their scores would collide).
@@ -114,7 +119,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     sd.chunk = (int32_t)ch;
     sd.n_chunks = (int32_t)((sd.n_tokens + ch - 1) / ch);
     sd.stats_off = stats;
-    stats += (int64_t)hq * sd.q_len * sd.n_chunks;
+    stats += (int64_t)hkv * sd.rows_pad * sd.n_chunks;
     sd.colpart_off = colpart;
     colpart += (int64_t)hkv * sd.n_rg * sd.n_tokens;
     // Tiles: chunks of one (g, rg) eight apart so that both query-row
@@ -124,7 +129,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
         for (int rg = 0; rg < sd.n_rg; ++rg)
           for (int c = c0; c < std::min(c0 + 8, sd.n_chunks); ++c) pl.tiles.push_back({s, g, rg, c});
   }
-  pl.waves = waves <= 1 ? 1 : waves <= 2 ? 2 : waves <= 4 ? 4 : 8;
+  pl.waves = waves <= 1 ? 1 : waves <= 2 ? 2 : waves <= 4 ? 4 : waves == 7 ? 7 : 8;
   pl.total_tok = tag;
   pl.total_rows = rows;
   pl.total_stats = stats;
@@ -135,6 +140,8 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
   c.take<SeqDev>(pl.seqs.size());
   pl.off_tiles = c.used;
   c.take<TileDev>(pl.tiles.size());
+  pl.off_ftiles = c.used;
+  c.take<FTileDev>(pl.ftiles.size());
   pl.off_tags = c.used;
   c.take<uint8_t>(pl.total_tok);
   pl.blob_bytes = c.used;
@@ -144,6 +151,10 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
   c.take<float>(pl.total_rows);
   pl.off_colpart = c.used;
   c.take<float>(pl.total_colpart);
+  pl.off_hist = c.used;
+  c.take<uint32_t>(pl.any_select ? pl.seqs.size() * 2 * 2048 : 0);
+  pl.off_cnt = c.used;
+  c.take<uint32_t>(3 * pl.ftiles.size());
   pl.ws_bytes = std::max<size_t>(c.used, kAlign);
   return APACK_OK;
 }
@@ -215,6 +226,8 @@ apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype
   char* h = static_cast<char*>(host);
   std::memcpy(h, pl.seqs.data(), pl.seqs.size() * sizeof(SeqDev));
   if (!pl.tiles.empty()) std::memcpy(h + pl.off_tiles, pl.tiles.data(), pl.tiles.size() * sizeof(TileDev));
+  if (!pl.ftiles.empty())
+    std::memcpy(h + pl.off_ftiles, pl.ftiles.data(), pl.ftiles.size() * sizeof(FTileDev));
   uint8_t* tags = reinterpret_cast<uint8_t*>(h + pl.off_tags);
   std::memset(tags, 0, pl.total_tok);
   for (int s = 0; s < n_seq; ++s)
@@ -229,6 +242,9 @@ apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype
   DevPtrs dp;
   dp.seqs = reinterpret_cast<SeqDev*>(ws);
   dp.tiles = reinterpret_cast<TileDev*>(ws + pl.off_tiles);
+  dp.ftiles = reinterpret_cast<FTileDev*>(ws + pl.off_ftiles);
+  dp.hist = reinterpret_cast<uint32_t*>(ws + pl.off_hist);
+  dp.cnt = reinterpret_cast<uint32_t*>(ws + pl.off_cnt);
   dp.tags = reinterpret_cast<uint8_t*>(ws + pl.off_tags);
   dp.stats = reinterpret_cast<float2*>(ws + pl.off_stats);
   dp.bias = reinterpret_cast<float*>(ws + pl.off_bias);

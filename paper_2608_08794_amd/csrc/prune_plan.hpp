@@ -10,6 +10,7 @@ namespace apack {
 
 constexpr int kKeyTile = 64;     // keys per LDS stage of the score kernels
 constexpr int kMaxWaves = 8;     // waves per score workgroup (64 query rows each)
+constexpr int kRowTile = 1024;   // rows per workgroup of the select and compaction kernels
 
 // Per-sequence descriptor on the device (uploaded once per call).  The
 // select kernel fills thr / need / all_eq for modalities it ranks.
@@ -20,12 +21,13 @@ struct SeqDev {
   int64_t out_off;      // first slot in kept_rows
   int64_t n_kept;       // kept rows of the sequence (bound on the scan's writes)
   int64_t tag_off;      // first byte of the sequence in the tag array
-  int64_t stats_off;    // first (max, sum) partial: [row][chunk]
-  int64_t bias_off;     // first b_r entry, rows h*q_len + t
+  int64_t stats_off;    // first (max, sum) partial: [g][rows_pad][chunk]
+  int64_t bias_off;     // first b entry: [g][rows_pad], row rho = (h % n_rep)*q_len + t
   int64_t colpart_off;  // first per-group column partial: [g*n_rg + rg][n_tokens]
   int32_t q_len;
   int32_t n_rg;         // query-row groups per KV head
   int32_t rows_per_rg;  // rows per group (multiple of 64)
+  int32_t rows_pad;     // n_rg * rows_per_rg
   int32_t chunk;        // keys per score workgroup (multiple of kKeyTile)
   int32_t n_chunks;
   int32_t n_cand;
@@ -35,6 +37,14 @@ struct SeqDev {
   uint32_t thr[2];      // threshold bits: rows above are kept
   int32_t need[2];      // rows equal to thr kept, lowest rows first
   int32_t all_eq[2];    // every row equal to thr is kept
+  uint32_t prefix[2];   // radix digits chosen so far
+  uint32_t kk[2];       // rank of the k-th value inside the chosen bucket
+  uint32_t done_cnt;    // row tiles finished in the current select pass
+  int32_t n_ftiles;     // row tiles of the sequence
+};
+
+struct FTileDev {
+  int32_t seq, idx;     // sequence and row tile within it (rows idx*kRowTile ...)
 };
 
 struct TileDev {
@@ -44,30 +54,38 @@ struct TileDev {
 struct PrunePlan {
   std::vector<SeqDev> seqs;
   std::vector<TileDev> tiles;
+  std::vector<FTileDev> ftiles;
   std::vector<int64_t> n_kept;
   int64_t total_tok = 0;    // sum of n_tokens (tag bytes)
-  int64_t total_rows = 0;   // sum of hq * q_len
+  int64_t max_tokens = 0;   // longest sequence
+  int64_t total_rows = 0;   // sum of hkv * rows_pad (padded query rows)
   int64_t total_stats = 0;  // (max, sum) partials
   int64_t total_colpart = 0;
   int64_t total_kept = 0;
   int waves = 1;
   bool any_select = false;
   // Workspace layout (byte offsets).
-  size_t off_seqs = 0, off_tiles = 0, off_tags = 0, blob_bytes = 0;
-  size_t off_stats = 0, off_bias = 0, off_colpart = 0, ws_bytes = 0;
+  size_t off_seqs = 0, off_tiles = 0, off_ftiles = 0, off_tags = 0, blob_bytes = 0;
+  size_t off_stats = 0, off_bias = 0, off_colpart = 0, off_hist = 0, off_cnt = 0, ws_bytes = 0;
 };
 
 struct DevPtrs {
   SeqDev* seqs;
   TileDev* tiles;
   uint8_t* tags;
+  FTileDev* ftiles;
   float2* stats;
   float* bias;
   float* colpart;
+  uint32_t* hist;       // [n_seq][2][2048] radix histograms
+  uint32_t* cnt;        // [n_ftiles][3] per-tile keep counts
 };
 
 apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, int32_t hkv, int32_t d,
                               PrunePlan& plan);
+
+apack_status launch_select(const PrunePlan& pl, const DevPtrs& dp, int hq, int hkv, float* scores, int32_t* kept,
+                           hipStream_t stream);
 
 apack_status launch_prune(const PrunePlan& pl, const DevPtrs& dp, apack_dtype dt, int d, int hq, int hkv,
                           const void* q, int64_t q_hs, const void* k, int64_t k_hs, float* scores,

@@ -215,3 +215,11 @@ def test_cumulative_keep_basis():
     g_scores, g_kept, g_n = _run_prune(case, seqs)
     assert g_n == w_n == [30 + 120 + 210]
     _check_scores(g_scores, w_scores, seqs, "bf16")
+
+
+def test_long_sequence_beyond_register_resident_select():
+    # 120k rows: longer than the fused select-and-scan kernel holds in
+    # registers, so the streaming select and scan kernels run.
+    specs = [([(0, 20000, A_), (20000, 99000, V_)], 120000, 3, (0.4, 0.25))]
+    case = _synthetic("bf16", 2, 1, 64, specs, seed=16)
+    _parity(case)

@@ -35,6 +35,30 @@ def log(msg):
     print(f"[bench] {msg}", file=sys.stderr, flush=True)
 
 
+def measured_traffic():
+    """Per-launch HBM bytes of k_gather from the committed rocprofv3 counter
+    summary, or None when the gather source has changed since it was taken."""
+    import hashlib
+    path = os.path.join(ROOT, "profiles", "k_gather_traffic_progressive7b.md")
+    try:
+        text = open(path).read()
+    except OSError:
+        return None
+    vals = {}
+    for line in text.splitlines():
+        line = line.strip()
+        for key in ("traffic_bytes_per_launch", "source", "source_sha256"):
+            if line.startswith(key + ":"):
+                vals[key] = line.split(":", 1)[1].strip()
+    try:
+        src = open(os.path.join(ROOT, vals["source"]), "rb").read()
+    except (KeyError, OSError):
+        return None
+    if hashlib.sha256(src).hexdigest() != vals.get("source_sha256"):
+        return None
+    return float(vals["traffic_bytes_per_launch"])
+
+
 def to_dev(x):
     import torch
     return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).cuda()
@@ -46,6 +70,9 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
+                    help="only run a plain device copy of MIB mebibytes three times (reference for HBM "
+                         "byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print("bench.py measures one GPU: the prune path needs no collective, and runs with "
@@ -61,6 +88,15 @@ def main():
         sys.exit(2)
     A.library()
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        n = args.copy_calibration * (1 << 20)
+        src = torch.ones(n, dtype=torch.uint8, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_calibration_bytes": n, "copies": 3}))
+        return
 
     t0 = time.time()
     case = W.progressive_case()
@@ -186,7 +222,8 @@ def main():
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
-            "traffic": None,
+            "traffic": measured_traffic(),
+            "algorithmic_bytes_per_launch": round(sum(gather_bytes) / len(gather_bytes)),
         },
         "per_prune_step_ms": {"score_select": [round(x, 4) for x in p_ms], "compact": [round(x, 4) for x in g_ms]},
         "algorithmic_bytes_per_step": step_bytes,

@@ -71,10 +71,10 @@ struct TileGeom {
   static constexpr int kSteps = D / Mma<T>::kstep;
 };
 
-// Query fragments of the 64 rows a wave owns (two blocks of 32), loaded once.
+// Query fragments of the rows a wave owns (kRB blocks of 32), loaded once.
 template <class T, int D>
 struct QFrags {
-  typename Mma<T>::frag v[2][TileGeom<T, D>::kSteps];
+  typename Mma<T>::frag v[kRB][TileGeom<T, D>::kSteps];
 };
 
 // Rows past the group's end read a clamped, valid row and are zeroed after
@@ -86,7 +86,7 @@ __device__ __forceinline__ void load_q(QFrags<T, D>& qfr, const T* q, int64_t q_
   auto& qf = qfr.v;
   const int rows = n_rep * sq.q_len;
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
+  for (int rb = 0; rb < kRB; ++rb) {
     const int rho = row0 + rb * 32 + (lane & 31);
     const int rc = rho < rows ? rho : rows - 1;
     const int h = g * n_rep + rc / sq.q_len;
@@ -172,7 +172,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rows_g = n_rep * sq.q_len;
   const int rg_end = min(rows_g, (tl.rg + 1) * sq.rows_per_rg);
-  const int row0 = tl.rg * sq.rows_per_rg + wave * 64;
+  const int row0 = tl.rg * sq.rows_per_rg + wave * kRowsPerWave;
   const bool active = row0 < rg_end;
 
   QFrags<T, D> qfr;
@@ -186,7 +186,12 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   const T* kbase = k + (int64_t)tl.g * k_hs + sq.tok_off * D;
   const uint8_t* tg = tags + sq.tag_off;
 
-  float m_run[2] = {-FLT_MAX, -FLT_MAX}, s_run[2] = {0.f, 0.f};
+  float m_run[kRB], s_run[kRB];
+#pragma unroll
+  for (int rb = 0; rb < kRB; ++rb) {
+    m_run[rb] = -FLT_MAX;
+    s_run[rb] = 0.f;
+  }
 
   KStage<T, D, NW> st;
   st.load(kbase, key_begin, key_end, tid);
@@ -208,12 +213,13 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
       for (int kb = 0; kb < NKB; ++kb) {
         KFrags<T, D> kf;
         kf.load(lds[buf], kb, lane);
-        f32x16 acc[2] = {f32x16{}, f32x16{}};
+        f32x16 acc[kRB];
 #pragma unroll
-        for (int ks = 0; ks < G::kSteps; ++ks) {
-          acc[0] = M::mma(kf.v[ks], qf[0][ks], acc[0]);
-          acc[1] = M::mma(kf.v[ks], qf[1][ks], acc[1]);
-        }
+        for (int rb = 0; rb < kRB; ++rb) acc[rb] = f32x16{};
+#pragma unroll
+        for (int ks = 0; ks < G::kSteps; ++ks)
+#pragma unroll
+          for (int rb = 0; rb < kRB; ++rb) acc[rb] = M::mma(kf.v[ks], qf[rb][ks], acc[rb]);
         // acc[rb][e]: query column (lane % 32) of block rb, key row
         // kb*32 + 8*(e/4) + 4*(lane/32) + e%4.
         if (masked) {
@@ -221,7 +227,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
           for (int i = 0; i < 4; ++i) {
             const float4 mk = *reinterpret_cast<const float4*>(&lmask[buf][kb * 32 + 8 * i + 4 * (lane >> 5)]);
 #pragma unroll
-            for (int rb = 0; rb < 2; ++rb) {
+            for (int rb = 0; rb < kRB; ++rb) {
               acc[rb][4 * i + 0] += mk.x;
               acc[rb][4 * i + 1] += mk.y;
               acc[rb][4 * i + 2] += mk.z;
@@ -230,7 +236,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
           }
         }
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
+        for (int rb = 0; rb < kRB; ++rb) {
           float lmax = acc[rb][0];
 #pragma unroll
           for (int e = 1; e < 16; ++e) lmax = fmaxf(lmax, acc[rb][e]);
@@ -246,7 +252,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   }
   if (!active) return;
 #pragma unroll
-  for (int rb = 0; rb < 2; ++rb) {
+  for (int rb = 0; rb < kRB; ++rb) {
     const float mo = __shfl_xor(m_run[rb], 32);
     const float so = __shfl_xor(s_run[rb], 32);
     const float mm = fmaxf(m_run[rb], mo);
@@ -320,18 +326,18 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int rows_g = n_rep * sq.q_len;
   const int rg_end = min(rows_g, (tl.rg + 1) * sq.rows_per_rg);
-  const int row0 = tl.rg * sq.rows_per_rg + wave * 64;
+  const int row0 = tl.rg * sq.rows_per_rg + wave * kRowsPerWave;
   const bool active = row0 < rg_end;
-  const int n_active = (rg_end - tl.rg * sq.rows_per_rg + 63) / 64;
+  const int n_active = (rg_end - tl.rg * sq.rows_per_rg + kRowsPerWave - 1) / kRowsPerWave;
 
   QFrags<T, D> qfr;
   auto& qf = qfr.v;
-  float b[2][16];
+  float b[kRB][16];
   if (active) {
     load_q<T, D>(qfr, q, q_hs, sq, tl.g, n_rep, row0, lane);
     const float* bb = bias + sq.bias_off + (int64_t)tl.g * sq.rows_pad + row0 + 4 * (lane >> 5);
 #pragma unroll
-    for (int rb = 0; rb < 2; ++rb)
+    for (int rb = 0; rb < kRB; ++rb)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
         const float4 v = *reinterpret_cast<const float4*>(bb + rb * 32 + 8 * i);
@@ -367,33 +373,33 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
     if (active) {
       float cs[NKB];
       f32x16 prev;
-      int prev_kb = -1;
+      int prev_kb = -1, prev_rb = 0;
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
         KFrags<T, D> kf;
         kf.load(lds[buf], kb, lane);
         cs[kb] = 0.f;
 #pragma unroll
-        for (int rb = 0; rb < 2; ++rb) {
+        for (int rb = 0; rb < kRB; ++rb) {
           f32x16 acc = f32x16{};
 #pragma unroll
           for (int ks = 0; ks < G::kSteps; ++ks) acc = M::mma(qf[rb][ks], kf.v[ks], acc);
           if (prev_kb >= 0) {
-            // Epilogue of the previous pair: row block 1 - rb.
-            const int prb = 1 - rb;
+            // Epilogue of the previous (key block, row block) pair.
             float s = 0.f;
 #pragma unroll
-            for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(prev[e], scale_log2, -b[prb][e]));
+            for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(prev[e], scale_log2, -b[prev_rb][e]));
             cs[prev_kb] += s;
           }
           prev = acc;
           prev_kb = kb;
+          prev_rb = rb;
         }
       }
       {
         float s = 0.f;
 #pragma unroll
-        for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(prev[e], scale_log2, -b[1][e]));
+        for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(prev[e], scale_log2, -b[kRB - 1][e]));
         cs[NKB - 1] += s;
       }
 #pragma unroll

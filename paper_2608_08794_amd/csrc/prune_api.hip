@@ -87,14 +87,14 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     sd.n_ftiles = (int32_t)((a.n_tokens + kRowTile - 1) / kRowTile);
     for (int f = 0; f < sd.n_ftiles; ++f) pl.ftiles.push_back({s, f});
     pl.max_tokens = std::max<int64_t>(pl.max_tokens, a.n_tokens);
-    // Query-row groups: at most kMaxWaves*64 rows each.
+    // Query-row groups: at most kMaxWaves * kRowsPerWave rows each.
     const int64_t rows_g = (int64_t)n_rep * a.q_len;
-    const int64_t cap = (int64_t)kMaxWaves * 64;
+    const int64_t cap = (int64_t)kMaxWaves * kRowsPerWave;
     sd.n_rg = (int32_t)((rows_g + cap - 1) / cap);
     const int64_t per = (rows_g + sd.n_rg - 1) / sd.n_rg;
-    sd.rows_per_rg = (int32_t)((per + 63) / 64 * 64);
+    sd.rows_per_rg = (int32_t)((per + kRowsPerWave - 1) / kRowsPerWave * kRowsPerWave);
     sd.rows_pad = sd.n_rg * sd.rows_per_rg;
-    waves = std::max<int>(waves, sd.rows_per_rg / 64);
+    waves = std::max<int>(waves, sd.rows_per_rg / kRowsPerWave);
     sd.bias_off = rows;
     rows += (int64_t)hkv * sd.rows_pad;
     if (sd.n_cand > 0) weighted += a.n_tokens * (int64_t)hkv * sd.n_rg;
@@ -109,7 +109,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
       APACK_CHECK(r[i].first >= r[i - 1].second, APACK_E_SHAPE, "sequences overlap in k");
   }
   // Keys per workgroup: aim for ~4 workgroups per CU over the whole call.
-  const int64_t target = 1024;
+  const int64_t target = APACK_TILE_TARGET;
   for (int s = 0; s < n_seq; ++s) {
     SeqDev& sd = pl.seqs[s];
     if (sd.n_cand == 0) continue;

@@ -8,8 +8,19 @@
 
 namespace apack {
 
-constexpr int kKeyTile = 64;     // keys per LDS stage of the score kernels
-constexpr int kMaxWaves = 8;     // waves per score workgroup (64 query rows each)
+#ifndef APACK_KEY_TILE
+#define APACK_KEY_TILE 64
+#endif
+#ifndef APACK_ROW_BLOCKS
+#define APACK_ROW_BLOCKS 2
+#endif
+#ifndef APACK_TILE_TARGET
+#define APACK_TILE_TARGET 1024
+#endif
+constexpr int kKeyTile = APACK_KEY_TILE;       // keys per LDS stage of the score kernels
+constexpr int kRB = APACK_ROW_BLOCKS;          // 32-row query blocks held by one wave
+constexpr int kRowsPerWave = 32 * kRB;
+constexpr int kMaxWaves = 8;                   // waves per score workgroup
 constexpr int kRowTile = 1024;   // rows per workgroup of the select and compaction kernels
 
 // Per-sequence descriptor on the device (uploaded once per call).  The

@@ -278,9 +278,13 @@ def apportion(total, weights, caps):
     leftover units go to the largest fractional parts, lowest index first on
     ties.  All-zero weights among the free items share equally.
 
-    Returns (alloc int array, margin): margin is the smallest distance of a
-    quota from an integer or from its cap, and the fractional-part gap at
-    the remainder cut.
+    Returns (alloc int array, margin).  The only decision that can change
+    the allocation under a tiny perturbation of the quotas is the order of
+    fractional parts at the remainder cut, so margin is the gap between the
+    last fractional part that receives a unit and the first that does not.
+    A quota just below an integer has fractional part near 1 and receives a
+    unit that restores its floor, and a quota at its cap ends at the cap
+    whether it is fixed or free, so neither is a decision boundary.
     """
     w = np.asarray(weights, dtype=np.float64)
     caps = np.asarray(caps, dtype=np.int64)
@@ -306,14 +310,10 @@ def apportion(total, weights, caps):
     alloc = np.zeros(n, dtype=np.int64)
     alloc[fixed] = caps[fixed]
     free_idx = np.flatnonzero(~fixed)
-    for i in free_idx:
-        margin = min(margin, abs(caps[i] - quota[i]))
     if free_idx.size:
         fl = np.floor(quota[free_idx])
         alloc[free_idx] = fl.astype(np.int64)
         frac = quota[free_idx] - fl
-        for fr in frac:
-            margin = min(margin, fr, 1.0 - fr)
         left = total - int(alloc.sum())
         order = sorted(range(free_idx.size), key=lambda i: (-frac[i], i))
         for i in order[:left]:

@@ -1,0 +1,966 @@
+// Pre-LLM local audio-visual dynamics scorer (Section 3.1, Eq. 1-4; the
+// first loop of Algorithm 1) on gfx950.
+//
+//   k_pool       coarse pass: frame means v_f, audio-bin means a_f (adaptive
+//                pooling onto the frame axis) and the query mean, in fp64
+//   k_band       band Gram v_f.v_{f+d}, a_f.a_{f+d} (d < w), v_f.q, q.q
+//   k_cka        Eq. 1 per frame from the centred w x w window Grams, the
+//                clip mean and the gate of Eq. 2
+//   k_norms      squared norms of every visual and audio token (fp64)
+//   k_gate_gemm  only where the gate fired: X_A . X_V^T on bf16 MFMA, scaled
+//                by 1/|a_j|, max over audio tokens in-lane, merged across
+//                tiles by atomicMax on order-preserving uint keys
+//   k_plan       one workgroup per clip: direct distance, Eq. 2 blend,
+//                continuity smoothing and cuts, Eq. 3 segment scores, frame
+//                scores, Eq. 4 segment budgets and frame budgets (capped
+//                largest remainder), anchors and output offsets
+//   k_gram       fp64 cosine Gram of the tokens of every anchor frame
+//   k_dafps      one wave per anchor frame: density-aware farthest-point
+//                sampling
+//   k_dedup      one workgroup per non-anchor frame: keep the positions least
+//                similar to the anchor
+//
+// Every discrete decision (gate, cuts, budgets, DA-FPS argmax, dedup ranks)
+// is taken in fp64, as in the oracle.  The gate GEMM accumulates in fp32.
+#include <algorithm>
+#include <cfloat>
+#include <cmath>
+
+#include "common.hpp"
+#include "dynamics_plan.hpp"
+
+namespace apack {
+namespace {
+
+typedef unsigned short bf16_t;
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+
+constexpr int kBlk = 256;
+
+__device__ __forceinline__ double widen(bf16_t x) { return (double)__uint_as_float((uint32_t)x << 16); }
+__device__ __forceinline__ double widen(float x) { return (double)x; }
+
+// 8 consecutive elements as doubles (16- or 32-byte aligned loads).
+__device__ __forceinline__ void load8(const bf16_t* p, double (&o)[8]) {
+  const uint4 u = *reinterpret_cast<const uint4*>(p);
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    o[2 * i] = (double)__uint_as_float(w[i] << 16);
+    o[2 * i + 1] = (double)__uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+__device__ __forceinline__ void load8(const float* p, double (&o)[8]) {
+  const float4 a = reinterpret_cast<const float4*>(p)[0];
+  const float4 b = reinterpret_cast<const float4*>(p)[1];
+  o[0] = a.x; o[1] = a.y; o[2] = a.z; o[3] = a.w;
+  o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
+}
+
+__device__ __forceinline__ double wave_sum(double v) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
+  return v;
+}
+
+// Block-wide reductions (kBlk threads; every thread gets the result).
+__device__ double block_sum(double v, double* sh) {
+  v = wave_sum(v);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sh[wave] = v;
+  __syncthreads();
+  double t = 0.0;
+  for (int w = 0; w < kBlk / 64; ++w) t += sh[w];
+  __syncthreads();
+  return t;
+}
+__device__ double block_max(double v, double* sh) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off));
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  __syncthreads();
+  if (lane == 0) sh[wave] = v;
+  __syncthreads();
+  double t = sh[0];
+  for (int w = 1; w < kBlk / 64; ++w) t = fmax(t, sh[w]);
+  __syncthreads();
+  return t;
+}
+__device__ double block_min(double v, double* sh) { return -block_max(-v, sh); }
+
+// ---------------------------------------------------------------------------
+// Coarse pass (Section 3.1): v_f, a_f and the query mean.
+// grid.x: every frame of every clip, then one block per clip for the query.
+// grid.y: 2048-element slices of the embedding (8 per thread).
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ __launch_bounds__(kBlk) void k_pool(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
+                                               int64_t total_frames, int dim, const T* __restrict__ xv,
+                                               const T* __restrict__ xa, const T* __restrict__ xq,
+                                               double* __restrict__ v, double* __restrict__ a,
+                                               double* __restrict__ q) {
+  const int d0 = (blockIdx.y * kBlk + threadIdx.x) * 8;
+  if (d0 >= dim) return;
+  double acc[8], o[8];
+  if ((int64_t)blockIdx.x < total_frames) {
+    const FrameDev fr = frames[blockIdx.x];
+    const ClipDev c = clips[fr.clip];
+    const int64_t frame = c.frame_off + fr.f;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+    const T* base = xv + (c.vis_off + (int64_t)fr.f * c.per_frame) * dim + d0;
+    for (int p = 0; p < c.per_frame; ++p) {
+      load8(base + (int64_t)p * dim, o);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += o[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) v[frame * dim + d0 + e] = acc[e] / (double)c.per_frame;
+    // Adaptive average-pool bin of the audio rows for this frame.
+    const int64_t lo = ((int64_t)fr.f * c.n_audio) / c.n_frames;
+    const int64_t hi = (((int64_t)fr.f + 1) * c.n_audio + c.n_frames - 1) / c.n_frames;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+    for (int64_t r = lo; r < hi; ++r) {
+      load8(xa + (c.aud_off + r) * dim + d0, o);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += o[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) a[frame * dim + d0 + e] = hi > lo ? acc[e] / (double)(hi - lo) : 0.0;
+  } else {
+    const int ci = (int)(blockIdx.x - total_frames);
+    const ClipDev c = clips[ci];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
+    for (int64_t r = 0; r < c.n_query; ++r) {
+      load8(xq + (c.qry_off + r) * dim + d0, o);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc[e] += o[e];
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q[(int64_t)ci * dim + d0 + e] = acc[e] / (double)c.n_query;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Band Gram entries of one frame: v_f.v_{f+d}, a_f.a_{f+d} for d < w, v_f.q
+// (and q.q for the first frame of the clip).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlk) void k_band(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
+                                               int dim, int w, const double* __restrict__ v,
+                                               const double* __restrict__ a, const double* __restrict__ q,
+                                               double* __restrict__ band_v, double* __restrict__ band_a,
+                                               double* __restrict__ vq, double* __restrict__ qq) {
+  __shared__ double sh[kBlk / 64][2 * kMaxWindow + 2];
+  const FrameDev fr = frames[blockIdx.x];
+  const ClipDev c = clips[fr.clip];
+  const int64_t f0 = c.frame_off + fr.f;
+  const int nd = min(max(w, 2), c.n_frames - fr.f);  // partners f .. f+nd-1 (f+1 for continuity)
+  const double* qv = q + (int64_t)fr.clip * dim;
+  double acc[2 * kMaxWindow + 2];
+#pragma unroll
+  for (int i = 0; i < 2 * kMaxWindow + 2; ++i) acc[i] = 0.0;
+  for (int d = threadIdx.x; d < dim; d += kBlk) {
+    const double vf = v[f0 * dim + d], af = a[f0 * dim + d], qd = qv[d];
+#pragma unroll
+    for (int dd = 0; dd < kMaxWindow; ++dd) {
+      if (dd < nd) {
+        acc[dd] += vf * v[(f0 + dd) * dim + d];
+        acc[kMaxWindow + dd] += af * a[(f0 + dd) * dim + d];
+      }
+    }
+    acc[2 * kMaxWindow] += vf * qd;
+    acc[2 * kMaxWindow + 1] += qd * qd;
+  }
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int i = 0; i < 2 * kMaxWindow + 2; ++i) {
+    const double s = wave_sum(acc[i]);
+    if (lane == 0) sh[wave][i] = s;
+  }
+  __syncthreads();
+  const int i = threadIdx.x;
+  if (i < 2 * kMaxWindow + 2) {
+    double s = 0.0;
+    for (int ww = 0; ww < kBlk / 64; ++ww) s += sh[ww][i];
+    if (i < kMaxWindow) {
+      if (i < nd) band_v[f0 * kMaxWindow + i] = s;
+    } else if (i < 2 * kMaxWindow) {
+      if (i - kMaxWindow < nd) band_a[f0 * kMaxWindow + (i - kMaxWindow)] = s;
+    } else if (i == 2 * kMaxWindow) {
+      vq[f0] = s;
+    } else if (fr.f == 0) {
+      qq[fr.clip] = s;
+    }
+  }
+}
+
+// Gram entry (i, j) of frames i, j of a clip from the band (|i - j| < w).
+__device__ __forceinline__ double band_at(const double* band, int64_t f0, int i, int j) {
+  return i <= j ? band[(f0 + i) * kMaxWindow + (j - i)] : band[(f0 + j) * kMaxWindow + (i - j)];
+}
+
+// ---------------------------------------------------------------------------
+// Eq. 1 per frame over its clamped window, the clip mean and the gate.
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w, double tau,
+                                              const double* __restrict__ band_v, const double* __restrict__ band_a,
+                                              double* __restrict__ cka, float* __restrict__ frame_cka,
+                                              uint8_t* __restrict__ gate_out) {
+  __shared__ double sh[kBlk / 64];
+  ClipDev* c = &clips[blockIdx.x];
+  const int F = c->n_frames;
+  const int64_t f0 = c->frame_off;
+  const int ww = F <= w ? F : w;
+  double sum = 0.0;
+  for (int f = threadIdx.x; f < F; f += kBlk) {
+    int lo = 0;
+    if (F > w) lo = min(max(f - w / 2, 0), F - w);
+    // Centred Grams K = H G H of the window rows lo .. lo+ww-1.
+    double ga[kMaxWindow][kMaxWindow], gv[kMaxWindow][kMaxWindow];
+    double ra[kMaxWindow], rv[kMaxWindow], ta = 0.0, tv = 0.0;
+    for (int i = 0; i < ww; ++i) {
+      ra[i] = rv[i] = 0.0;
+      for (int j = 0; j < ww; ++j) {
+        ga[i][j] = band_at(band_a, f0, lo + i, lo + j);
+        gv[i][j] = band_at(band_v, f0, lo + i, lo + j);
+        ra[i] += ga[i][j];
+        rv[i] += gv[i][j];
+      }
+      ra[i] /= ww;
+      rv[i] /= ww;
+      ta += ra[i];
+      tv += rv[i];
+    }
+    ta /= ww;
+    tv /= ww;
+    double num = 0.0, na = 0.0, nv = 0.0;
+    for (int i = 0; i < ww; ++i)
+      for (int j = 0; j < ww; ++j) {
+        const double ka = ga[i][j] - ra[i] - ra[j] + ta;
+        const double kv = gv[i][j] - rv[i] - rv[j] + tv;
+        num += ka * kv;
+        na += ka * ka;
+        nv += kv * kv;
+      }
+    const double den = sqrt(na) * sqrt(nv);
+    const double cf = den == 0.0 ? 0.0 : num / den;
+    cka[f0 + f] = cf;
+    if (frame_cka) frame_cka[f0 + f] = (float)cf;
+    sum += cf;
+  }
+  sum = block_sum(sum, sh);
+  if (threadIdx.x == 0) {
+    const int fired = (F > 0 && sum / F < tau) ? 1 : 0;
+    c->gate = fired;
+    if (gate_out) gate_out[blockIdx.x] = (uint8_t)fired;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Squared norms of every visual row and audio row (one wave per row); the
+// visual max-cosine keys start at 0 (below every real key).
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ __launch_bounds__(kBlk) void k_norms(int64_t n_vis, int64_t n_aud, int dim, const T* __restrict__ xv,
+                                                const T* __restrict__ xa, double* __restrict__ nv,
+                                                double* __restrict__ na, uint32_t* __restrict__ maxkey) {
+  const int64_t row = (int64_t)blockIdx.x * (kBlk / 64) + (threadIdx.x >> 6);
+  const int lane = threadIdx.x & 63;
+  if (row >= n_vis + n_aud) return;
+  const T* p = row < n_vis ? xv + row * dim : xa + (row - n_vis) * dim;
+  double acc = 0.0, o[8];
+  for (int d = lane * 8; d < dim; d += 64 * 8) {
+    load8(p + d, o);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc += o[e] * o[e];
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    if (row < n_vis) {
+      nv[row] = acc;
+      maxkey[row] = 0u;
+    } else {
+      na[row - n_vis] = acc;
+    }
+  }
+}
+
+__device__ __forceinline__ uint32_t order_key(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
+
+// ---------------------------------------------------------------------------
+// Gate GEMM: for every visual token i, max_j (x_A[j] . x_V[i]) / |x_A[j]|.
+// C = X_A X_V^T in 128 x 128 tiles (4 waves, 64 x 64 each), K through
+// padded, double-buffered LDS in steps of 64 elements.
+// ---------------------------------------------------------------------------
+template <class T> struct GMma;
+template <> struct GMma<bf16_t> {
+  using frag = bf16x8;
+  static constexpr int kstep = 16, lane_k = 8;
+  static __device__ __forceinline__ f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
+  }
+};
+template <> struct GMma<float> {
+  using frag = float;
+  static constexpr int kstep = 2, lane_k = 1;
+  static __device__ __forceinline__ f32x16 mma(frag a, frag b, f32x16 c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+};
+
+constexpr int kGB = 128;   // tile rows and columns
+constexpr int kGK = 64;    // K elements per LDS stage
+
+template <class T>
+__global__ __launch_bounds__(kBlk) void k_gate_gemm(const ClipDev* __restrict__ clips,
+                                                    const GemmTileDev* __restrict__ tiles, int dim,
+                                                    const T* __restrict__ xv, const T* __restrict__ xa,
+                                                    const double* __restrict__ na, uint32_t* __restrict__ maxkey) {
+  using M = GMma<T>;
+  constexpr int kRowBytes = kGK * (int)sizeof(T);
+  constexpr int kPitch = kRowBytes + 16;
+  constexpr int kUnits = kRowBytes / 16;          // 16-byte units per tile row
+  constexpr int kPer = kGB * kUnits / kBlk;       // units per thread per tile
+  constexpr int kEl = 16 / (int)sizeof(T);        // elements per unit
+  __shared__ __attribute__((aligned(16))) char lds_a[2][kGB * kPitch];
+  __shared__ __attribute__((aligned(16))) char lds_b[2][kGB * kPitch];
+
+  const GemmTileDev tl = tiles[blockIdx.x];
+  const ClipDev c = clips[tl.clip];
+  if (!c.gate) return;
+  const int64_t n_a = c.n_audio, n_v = (int64_t)c.n_frames * c.per_frame;
+  const T* A = xa + c.aud_off * dim;
+  const T* B = xv + c.vis_off * dim;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wr = wave >> 1, wc = wave & 1;
+
+  uint4 ra[kPer], rb[kPer];
+  auto gload = [&](int k0) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int u = tid + i * kBlk;
+      const int row = u / kUnits, col = u % kUnits;
+      const int kk = k0 + col * kEl;
+      uint4 x = make_uint4(0, 0, 0, 0), y = make_uint4(0, 0, 0, 0);
+      if (tl.m0 + row < n_a && kk < dim) x = *reinterpret_cast<const uint4*>(A + (tl.m0 + row) * (int64_t)dim + kk);
+      if (tl.n0 + row < n_v && kk < dim) y = *reinterpret_cast<const uint4*>(B + (tl.n0 + row) * (int64_t)dim + kk);
+      ra[i] = x;
+      rb[i] = y;
+    }
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < kPer; ++i) {
+      const int u = tid + i * kBlk;
+      const int row = u / kUnits, col = u % kUnits;
+      *reinterpret_cast<uint4*>(lds_a[buf] + row * kPitch + col * 16) = ra[i];
+      *reinterpret_cast<uint4*>(lds_b[buf] + row * kPitch + col * 16) = rb[i];
+    }
+  };
+  auto frag = [&](const char* lds, int row, int ks) {
+    const char* p = lds + row * kPitch + (ks * M::kstep + (lane >> 5) * M::lane_k) * (int)sizeof(T);
+    return *reinterpret_cast<const typename M::frag*>(p);
+  };
+
+  f32x16 acc[2][2];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
+  const int n_k = (dim + kGK - 1) / kGK;
+  gload(0);
+  for (int it = 0; it < n_k; ++it) {
+    const int buf = it & 1;
+    lstore(buf);
+    __syncthreads();
+    if (it + 1 < n_k) gload((it + 1) * kGK);
+#pragma unroll
+    for (int ks = 0; ks < kGK / M::kstep; ++ks) {
+      typename M::frag fa[2], fb[2];
+#pragma unroll
+      for (int i = 0; i < 2; ++i) {
+        fa[i] = frag(lds_a[buf], wr * 64 + i * 32 + (lane & 31), ks);
+        fb[i] = frag(lds_b[buf], wc * 64 + i * 32 + (lane & 31), ks);
+      }
+#pragma unroll
+      for (int i = 0; i < 2; ++i)
+#pragma unroll
+        for (int j = 0; j < 2; ++j) acc[i][j] = M::mma(fa[i], fb[j], acc[i][j]);
+    }
+  }
+  // Epilogue: acc[i][j][e] is audio row wr*64 + i*32 + 8*(e/4) + 4*(lane/32) + e%4,
+  // visual column wc*64 + j*32 + lane%32.
+  float inv[2][16];
+#pragma unroll
+  for (int i = 0; i < 2; ++i)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) {
+      const int64_t r = tl.m0 + wr * 64 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+      float s = -INFINITY;  // rows past the clip's audio never win the max
+      if (r < n_a) {
+        const double nn = na[c.aud_off + r];
+        s = nn > 0.0 ? (float)(1.0 / sqrt(nn)) : 0.0f;
+      }
+      inv[i][e] = s;
+    }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 2; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float x = inv[i][e] == -INFINITY ? -INFINITY : acc[i][j][e] * inv[i][e];
+        m = fmaxf(m, x);
+      }
+    m = fmaxf(m, __shfl_xor(m, 32));
+    const int64_t col = tl.n0 + wc * 64 + j * 32 + (lane & 31);
+    if (lane < 32 && col < n_v && m > -INFINITY) atomicMax(&maxkey[c.vis_off + col], order_key(m));
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Capped largest-remainder apportionment of `total` over items [0, n) with
+// weights w[i] and caps cap[i] (block-wide; scratch arrays in global memory).
+// Water-filling first (items whose quota exceeds their cap are fixed at the
+// cap, the rest re-shared), then floors and the leftover units to the
+// largest fractional parts, lower index first on ties.
+// ---------------------------------------------------------------------------
+__device__ void apportion(int64_t total, int n, const double* w, const int64_t* cap, int32_t* fixed,
+                          double* quota, int64_t* alloc, double* sh) {
+  for (int i = threadIdx.x; i < n; i += kBlk) fixed[i] = 0;
+  __syncthreads();
+  for (int round = 0; round <= n; ++round) {
+    double fixed_caps = 0.0, sw = 0.0, nfree = 0.0;
+    for (int i = threadIdx.x; i < n; i += kBlk) {
+      if (fixed[i]) fixed_caps += (double)cap[i];
+      else {
+        sw += w[i];
+        nfree += 1.0;
+      }
+    }
+    fixed_caps = block_sum(fixed_caps, sh);
+    sw = block_sum(sw, sh);
+    nfree = block_sum(nfree, sh);
+    const double remaining = (double)total - fixed_caps;
+    double over = 0.0;
+    for (int i = threadIdx.x; i < n; i += kBlk) {
+      if (fixed[i]) continue;
+      const double qv = sw > 0.0 ? remaining * w[i] / sw : remaining / nfree;
+      quota[i] = qv;
+      if (qv > (double)cap[i]) over += 1.0;
+    }
+    over = block_sum(over, sh);
+    if (over == 0.0) break;
+    for (int i = threadIdx.x; i < n; i += kBlk)
+      if (!fixed[i] && quota[i] > (double)cap[i]) fixed[i] = 1;
+    __syncthreads();
+  }
+  double used = 0.0;
+  for (int i = threadIdx.x; i < n; i += kBlk) {
+    const int64_t a = fixed[i] ? cap[i] : (int64_t)floor(quota[i]);
+    alloc[i] = a;
+    used += (double)a;
+  }
+  used = block_sum(used, sh);
+  const int64_t left = total - (int64_t)used;
+  for (int i = threadIdx.x; i < n; i += kBlk) {
+    if (fixed[i]) continue;
+    const double fi = quota[i] - floor(quota[i]);
+    int64_t rank = 0;
+    for (int j = 0; j < n; ++j) {
+      if (fixed[j] || j == i) continue;
+      const double fj = quota[j] - floor(quota[j]);
+      if (fj > fi || (fj == fi && j < i)) ++rank;
+    }
+    if (rank < left) alloc[i] += 1;
+  }
+  __syncthreads();
+}
+
+// ---------------------------------------------------------------------------
+// Per-clip plan: scores, segments and budgets.  Scratch arrays hold
+// (sum F + n_clips) entries; clip c uses the F_c + 1 entries starting at
+// frame_off + c.
+// ---------------------------------------------------------------------------
+struct PlanScratch {
+  double *d, *alpha, *cont, *smooth, *rel, *score, *g, *quota, *fquota;
+  int64_t *cap, *alloc, *fcap, *falloc;
+  int32_t *fixed, *ffixed, *start;
+};
+
+__global__ __launch_bounds__(kBlk) void k_plan(ClipDev* __restrict__ clips, DynParamsDev prm,
+                                               const double* __restrict__ cka, const double* __restrict__ band_v,
+                                               const double* __restrict__ vq, const double* __restrict__ qq,
+                                               const double* __restrict__ nv, const uint32_t* __restrict__ maxkey,
+                                               FramePlanDev* __restrict__ plan, PlanScratch scr,
+                                               float* __restrict__ frame_score, int32_t* __restrict__ frame_budget,
+                                               int32_t* __restrict__ segment_id) {
+  __shared__ double sh[kBlk / 64];
+  __shared__ int n_seg_sh;
+  ClipDev* cp = &clips[blockIdx.x];
+  const ClipDev c = *cp;
+  const int F = c.n_frames, P = c.per_frame;
+  if (F == 0) return;
+  const int64_t f0 = c.frame_off;
+  const int64_t o = f0 + blockIdx.x;
+  double* d = scr.d + o;
+  double* alpha = scr.alpha + o;
+  double* cont = scr.cont + o;
+  double* smooth = scr.smooth + o;
+  double* rel = scr.rel + o;
+  double* score = scr.score + o;
+  double* g = scr.g + o;
+  double* quota = scr.quota + o;
+  double* fquota = scr.fquota + o;
+  int64_t* cap = scr.cap + o;
+  int64_t* alloc = scr.alloc + o;
+  int64_t* fcap = scr.fcap + o;
+  int64_t* falloc = scr.falloc + o;
+  int32_t* fixed = scr.fixed + o;
+  int32_t* ffixed = scr.ffixed + o;
+  int32_t* start = scr.start + o;
+
+  // Direct distance and the Eq. 2 blend.
+  if (c.gate) {
+    double lo = INFINITY, hi = -INFINITY;
+    for (int f = threadIdx.x; f < F; f += kBlk) {
+      double sm = 0.0;
+      for (int p = 0; p < P; ++p) {
+        const int64_t row = c.vis_off + (int64_t)f * P + p;
+        const double nn = nv[row];
+        sm += nn > 0.0 ? (double)key_value(maxkey[row]) * (1.0 / sqrt(nn)) : 0.0;
+      }
+      const double df = 1.0 - sm / P;
+      d[f] = df;
+      lo = fmin(lo, df);
+      hi = fmax(hi, df);
+    }
+    lo = block_min(lo, sh);
+    hi = block_max(hi, sh);
+    for (int f = threadIdx.x; f < F; f += kBlk) {
+      const double dh = hi == lo ? 0.0 : (d[f] - lo) / (hi - lo);
+      alpha[f] = (1.0 - prm.beta) * cka[f0 + f] + prm.beta * (1.0 - dh);
+      plan[f0 + f].dist = d[f];
+    }
+  } else {
+    for (int f = threadIdx.x; f < F; f += kBlk) {
+      alpha[f] = cka[f0 + f];
+      plan[f0 + f].dist = 0.0;
+    }
+  }
+  // Continuity cs_f = cos(v_f, v_{f+1}), its Gaussian smoothing (half-sample
+  // symmetric ends, truncated at 4 sigma) and the relevance r_f.
+  const double qn = sqrt(qq[blockIdx.x]);
+  for (int f = threadIdx.x; f < F; f += kBlk) {
+    const double nx = sqrt(band_v[(f0 + f) * kMaxWindow]);
+    if (f + 1 < F) {
+      const double ny = sqrt(band_v[(f0 + f + 1) * kMaxWindow]);
+      cont[f] = (nx == 0.0 || ny == 0.0) ? 0.0 : band_v[(f0 + f) * kMaxWindow + 1] / (nx * ny);
+    }
+    const double cs = (nx == 0.0 || qn == 0.0) ? 0.0 : vq[f0 + f] / (nx * qn);
+    rel[f] = (1.0 + cs) / 2.0;
+  }
+  __syncthreads();
+  const int n = F - 1;
+  const int radius = (int)(4.0 * prm.sigma + 0.5);
+  for (int i = threadIdx.x; i < n; i += kBlk) {
+    double wsum = 0.0;
+    for (int k = -radius; k <= radius; ++k) wsum += exp(-0.5 * ((k / prm.sigma) * (k / prm.sigma)));
+    double acc = 0.0;
+    for (int k = -radius; k <= radius; ++k) {
+      const double wt = exp(-0.5 * ((k / prm.sigma) * (k / prm.sigma))) / wsum;
+      int j = (i + k) % (2 * n);
+      if (j < 0) j += 2 * n;
+      if (j >= n) j = 2 * n - 1 - j;
+      acc += wt * cont[j];
+    }
+    smooth[i] = acc;
+  }
+  __syncthreads();
+  // Cuts: one per maximal run below tau_sim, after the run's minimum.
+  if (threadIdx.x == 0) {
+    int ns = 0;
+    start[ns++] = 0;
+    int f = 0;
+    while (f < n) {
+      if (smooth[f] < prm.tau_sim) {
+        int e = f, best = f;
+        while (e + 1 < n && smooth[e + 1] < prm.tau_sim) {
+          ++e;
+          if (smooth[e] < smooth[best]) best = e;
+        }
+        start[ns++] = best + 1;
+        f = e + 1;
+      } else {
+        ++f;
+      }
+    }
+    start[ns] = F;
+    n_seg_sh = ns;
+    cp->n_seg = ns;
+  }
+  __syncthreads();
+  const int n_seg = n_seg_sh;
+  // Segment scores g_m (Eq. 3) and caps |G_m| P.
+  for (int m = threadIdx.x; m < n_seg; m += kBlk) {
+    const int b = start[m], e = start[m + 1];
+    double mx = -INFINITY, sm = 0.0;
+    for (int f = b; f < e; ++f) {
+      mx = fmax(mx, rel[f]);
+      sm += rel[f];
+    }
+    const int len = e - b;
+    g[m] = sqrt((double)len) * (prm.lambda_seg * mx + (1.0 - prm.lambda_seg) * (sm / len));
+    cap[m] = (int64_t)len * P;
+  }
+  __syncthreads();
+  double gmax = -INFINITY;
+  for (int m = threadIdx.x; m < n_seg; m += kBlk) gmax = fmax(gmax, g[m]);
+  gmax = block_max(gmax, sh);
+  // Frame scores s_f = gamma u_f + (1 - gamma) alpha_f with u_f = g_m / max g.
+  for (int m = threadIdx.x; m < n_seg; m += kBlk) {
+    const int b = start[m], e = start[m + 1];
+    const double u = g[m] / gmax;
+    for (int f = b; f < e; ++f) {
+      const double sv = prm.gamma * u + (1.0 - prm.gamma) * alpha[f];
+      score[f] = sv;
+      plan[f0 + f].score = sv;
+      plan[f0 + f].seg = m;
+      plan[f0 + f].anchor = b;
+      plan[f0 + f].is_anchor = f == b ? 1 : 0;
+      if (frame_score) frame_score[f0 + f] = (float)sv;
+      if (segment_id) segment_id[f0 + f] = m;
+    }
+  }
+  __syncthreads();
+  // Segment budgets (Eq. 4), capped at |G_m| P; then frame budgets within
+  // each segment by s_f, capped at P.
+  apportion(c.budget, n_seg, g, cap, fixed, quota, alloc, sh);
+  for (int m = 0; m < n_seg; ++m) {
+    const int b = start[m], e = start[m + 1];
+    for (int i = threadIdx.x; i < e - b; i += kBlk) fcap[i] = P;
+    __syncthreads();
+    apportion(alloc[m], e - b, score + b, fcap, ffixed, fquota, falloc, sh);
+    for (int i = threadIdx.x; i < e - b; i += kBlk) plan[f0 + b + i].budget = (int32_t)falloc[i];
+    __syncthreads();
+  }
+  // Output offsets: exclusive prefix of k_f over the clip's frames.
+  if (threadIdx.x == 0) {
+    int64_t off = c.kept_off;
+    for (int f = 0; f < F; ++f) {
+      plan[f0 + f].out_off = off;
+      off += plan[f0 + f].budget;
+      if (frame_budget) frame_budget[f0 + f] = plan[f0 + f].budget;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Cosine Gram of an anchor frame's tokens: rows i0 .. i0+7 against all P.
+// ---------------------------------------------------------------------------
+constexpr int kGramRows = 8;
+
+template <class T>
+__global__ __launch_bounds__(kBlk) void k_gram(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
+                                               const FramePlanDev* __restrict__ plan, int dim, int rows_per_block,
+                                               const T* __restrict__ xv, const double* __restrict__ nv,
+                                               double* __restrict__ gram) {
+  extern __shared__ __attribute__((aligned(16))) char smem[];
+  const FrameDev fr = frames[blockIdx.x];
+  const ClipDev c = clips[fr.clip];
+  const int64_t frame = c.frame_off + fr.f;
+  const FramePlanDev fp = plan[frame];
+  if (!fp.is_anchor || fp.budget == 0) return;
+  const int P = c.per_frame;
+  const int i0 = blockIdx.y * rows_per_block;
+  if (i0 >= P) return;
+  const int ni = min(rows_per_block, P - i0);
+  const int64_t row0 = c.vis_off + (int64_t)fr.f * P;
+  T* rows = reinterpret_cast<T*>(smem);
+  for (int u = threadIdx.x * 8; u < ni * dim; u += kBlk * 8) {
+    const int r = u / dim, col = u % dim;
+    const T* src = xv + (row0 + i0 + r) * dim + col;
+#pragma unroll
+    for (int e = 0; e < 8; ++e) rows[r * dim + col + e] = src[e];
+  }
+  __syncthreads();
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  double* g = gram + c.gram_off + (int64_t)fr.f * P * P;
+  for (int j = wave; j < P; j += kBlk / 64) {
+    double acc[kGramRows], o[8];
+#pragma unroll
+    for (int r = 0; r < kGramRows; ++r) acc[r] = 0.0;
+    const T* xj = xv + (row0 + j) * dim;
+    for (int d = lane * 8; d < dim; d += 64 * 8) {
+      load8(xj + d, o);
+#pragma unroll
+      for (int r = 0; r < kGramRows; ++r) {
+        if (r < ni) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[r] += widen(rows[r * dim + d + e]) * o[e];
+        }
+      }
+    }
+    const double nj = sqrt(nv[row0 + j]);
+#pragma unroll
+    for (int r = 0; r < kGramRows; ++r) {
+      const double s = wave_sum(acc[r]);
+      if (lane == 0 && r < ni) {
+        const double ni_ = sqrt(nv[row0 + i0 + r]);
+        g[(int64_t)(i0 + r) * P + j] = (ni_ == 0.0 || nj == 0.0) ? 0.0 : s / (ni_ * nj);
+      }
+    }
+  }
+}
+
+// Lexicographic (value desc, index asc) argmax across a wave.
+__device__ __forceinline__ void wave_argmax(double& v, int& idx) {
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const double ov = __shfl_xor(v, off);
+    const int oi = __shfl_xor(idx, off);
+    if (ov > v || (ov == v && oi < idx)) {
+      v = ov;
+      idx = oi;
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// DA-FPS on an anchor frame (one wave; up to 4 tokens per lane).
+// ---------------------------------------------------------------------------
+__global__ __launch_bounds__(64) void k_dafps(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
+                                              const FramePlanDev* __restrict__ plan, DynParamsDev prm,
+                                              const double* __restrict__ gram, int32_t* __restrict__ kept) {
+  const FrameDev fr = frames[blockIdx.x];
+  const ClipDev c = clips[fr.clip];
+  const int64_t frame = c.frame_off + fr.f;
+  const FramePlanDev fp = plan[frame];
+  if (!fp.is_anchor || fp.budget == 0) return;
+  const int P = c.per_frame, lane = threadIdx.x;
+  const int k = min(fp.budget, P);
+  const double* S = gram + c.gram_off + (int64_t)fr.f * P * P;
+  constexpr int kT = kMaxPerFrame / 64;
+  double rho[kT], wgt[kT], smax[kT];
+  bool taken[kT];
+#pragma unroll
+  for (int t = 0; t < kT; ++t) {
+    const int i = lane + 64 * t;
+    rho[t] = -INFINITY;
+    wgt[t] = 0.0;
+    smax[t] = 0.0;
+    taken[t] = i >= P;
+    if (i >= P) continue;
+    // Mean of the dafps_k largest cosines to other tokens; coverage count.
+    double top[32];
+    int nt = 0, cov = 0;
+    for (int j = 0; j < P; ++j) {
+      if (j == i) continue;
+      const double s = S[(int64_t)i * P + j];
+      if (s >= prm.cover) ++cov;
+      // insert into the descending top list (length <= dafps_k)
+      if (nt < prm.dafps_k) {
+        int pos = nt++;
+        while (pos > 0 && top[pos - 1] < s) {
+          top[pos] = top[pos - 1];
+          --pos;
+        }
+        top[pos] = s;
+      } else if (s > top[nt - 1]) {
+        int pos = nt - 1;
+        while (pos > 0 && top[pos - 1] < s) {
+          top[pos] = top[pos - 1];
+          --pos;
+        }
+        top[pos] = s;
+      }
+    }
+    double knn = 0.0;
+    for (int q = 0; q < nt; ++q) knn += top[q];
+    knn = nt ? knn / nt : 0.0;
+    rho[t] = fmax(knn, 0.0) * (1.0 + cov);
+    wgt[t] = pow(rho[t], prm.power);
+  }
+  // First pick: the densest token.
+  double bv = -INFINITY;
+  int bi = 0x7FFFFFFF;
+#pragma unroll
+  for (int t = 0; t < kT; ++t)
+    if (!taken[t] && (rho[t] > bv || (rho[t] == bv && lane + 64 * t < bi))) {
+      bv = rho[t];
+      bi = lane + 64 * t;
+    }
+  wave_argmax(bv, bi);
+  int pick = bi;
+  for (int n = 0;; ++n) {
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      const int i = lane + 64 * t;
+      if (i == pick) taken[t] = true;
+      if (i < P) smax[t] = n == 0 ? S[(int64_t)pick * P + i] : fmax(smax[t], S[(int64_t)pick * P + i]);
+    }
+    if (n + 1 >= k) break;
+    bv = -INFINITY;
+    bi = 0x7FFFFFFF;
+#pragma unroll
+    for (int t = 0; t < kT; ++t) {
+      if (taken[t]) continue;
+      const double val = (1.0 - smax[t]) * wgt[t];
+      const int i = lane + 64 * t;
+      if (val > bv || (val == bv && i < bi)) {
+        bv = val;
+        bi = i;
+      }
+    }
+    wave_argmax(bv, bi);
+    pick = bi;
+  }
+  // Ascending output of the picked positions.
+  int64_t pos = fp.out_off;
+#pragma unroll
+  for (int t = 0; t < kT; ++t) {
+    const int i = lane + 64 * t;
+    const bool kp = i < P && taken[t];
+    const uint64_t bal = __ballot(kp);
+    if (kp) kept[pos + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(c.vis_off + (int64_t)fr.f * P + i);
+    pos += __popcll(bal);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Non-anchor frames: keep the k_f positions least similar to the anchor
+// token at the same position (lower position first on ties).
+// ---------------------------------------------------------------------------
+template <class T>
+__global__ __launch_bounds__(kBlk) void k_dedup(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
+                                                const FramePlanDev* __restrict__ plan, int dim,
+                                                const T* __restrict__ xv, const double* __restrict__ nv,
+                                                int32_t* __restrict__ kept) {
+  __shared__ double sim[kMaxPerFrame];
+  __shared__ int wcount[kBlk / 64];
+  const FrameDev fr = frames[blockIdx.x];
+  const ClipDev c = clips[fr.clip];
+  const int64_t frame = c.frame_off + fr.f;
+  const FramePlanDev fp = plan[frame];
+  if (fp.is_anchor || fp.budget == 0) return;
+  const int P = c.per_frame;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int64_t rowf = c.vis_off + (int64_t)fr.f * P, rowa = c.vis_off + (int64_t)fp.anchor * P;
+  for (int p = wave; p < P; p += kBlk / 64) {
+    const T* x = xv + (rowf + p) * dim;
+    const T* y = xv + (rowa + p) * dim;
+    double acc = 0.0, o[8], q[8];
+    for (int d = lane * 8; d < dim; d += 64 * 8) {
+      load8(x + d, o);
+      load8(y + d, q);
+#pragma unroll
+      for (int e = 0; e < 8; ++e) acc += o[e] * q[e];
+    }
+    acc = wave_sum(acc);
+    if (lane == 0) {
+      const double nx = sqrt(nv[rowf + p]), ny = sqrt(nv[rowa + p]);
+      sim[p] = (nx == 0.0 || ny == 0.0) ? 0.0 : acc / (nx * ny);
+    }
+  }
+  __syncthreads();
+  const int p = threadIdx.x;
+  bool kp = false;
+  if (p < P) {
+    int rank = 0;
+    for (int q = 0; q < P; ++q)
+      if (sim[q] < sim[p] || (sim[q] == sim[p] && q < p)) ++rank;
+    kp = rank < fp.budget;
+  }
+  const uint64_t bal = __ballot(kp);
+  if (lane == 0) wcount[wave] = __popcll(bal);
+  __syncthreads();
+  int64_t pos = fp.out_off;
+  for (int w = 0; w < wave; ++w) pos += wcount[w];
+  if (kp) kept[pos + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(rowf + p);
+}
+
+template <class T>
+apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& prm, int dim, const T* xv,
+                      const T* xa, const T* xq, float* frame_cka, float* frame_score, int32_t* frame_budget,
+                      int32_t* segment_id, uint8_t* gate_fired, int32_t* kept, int64_t visual_rows,
+                      int64_t audio_rows, hipStream_t s) {
+  apack_status st;
+  const int nf = (int)pl.frames.size(), nc = (int)pl.clips.size();
+  const unsigned dchunks = (unsigned)((dim + kBlk * 8 - 1) / (kBlk * 8));
+  hipLaunchKernelGGL(k_pool<T>, dim3(nf + nc, dchunks), dim3(kBlk), 0, s, dp.clips, dp.frames, (int64_t)nf, dim,
+                     xv, xa, xq, dp.v, dp.a, dp.q);
+  if ((st = launch_status("k_pool")) != APACK_OK) return st;
+  if (nf > 0) {
+    hipLaunchKernelGGL(k_band, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dim, prm.window, dp.v, dp.a, dp.q,
+                       dp.band_v, dp.band_a, dp.vq, dp.qq);
+    if ((st = launch_status("k_band")) != APACK_OK) return st;
+  }
+  hipLaunchKernelGGL(k_cka, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm.window, prm.tau_gate, dp.band_v, dp.band_a,
+                     dp.cka, frame_cka, gate_fired);
+  if ((st = launch_status("k_cka")) != APACK_OK) return st;
+  const int64_t rows = visual_rows + audio_rows;
+  if (rows > 0) {
+    hipLaunchKernelGGL(k_norms<T>, dim3((unsigned)((rows + 3) / 4)), dim3(kBlk), 0, s, visual_rows, audio_rows,
+                       dim, xv, xa, dp.nv, dp.na, dp.maxkey);
+    if ((st = launch_status("k_norms")) != APACK_OK) return st;
+  }
+  if (pl.gemm_tiles > 0) {
+    hipLaunchKernelGGL(k_gate_gemm<T>, dim3((unsigned)pl.gemm_tiles), dim3(kBlk), 0, s, dp.clips, dp.gemm, dim, xv,
+                       xa, dp.na, dp.maxkey);
+    if ((st = launch_status("k_gate_gemm")) != APACK_OK) return st;
+  }
+  PlanScratch scr;
+  {
+    const int64_t n = pl.total_frames + nc;
+    double* b = dp.scratch;
+    scr.d = b; scr.alpha = b + n; scr.cont = b + 2 * n; scr.smooth = b + 3 * n; scr.rel = b + 4 * n;
+    scr.score = b + 5 * n; scr.g = b + 6 * n; scr.quota = b + 7 * n; scr.fquota = b + 8 * n;
+    int64_t* ib = reinterpret_cast<int64_t*>(b + 9 * n);
+    scr.cap = ib; scr.alloc = ib + n; scr.fcap = ib + 2 * n; scr.falloc = ib + 3 * n;
+    int32_t* jb = reinterpret_cast<int32_t*>(ib + 4 * n);
+    scr.fixed = jb; scr.ffixed = jb + n; scr.start = jb + 2 * n;
+  }
+  hipLaunchKernelGGL(k_plan, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm, dp.cka, dp.band_v, dp.vq, dp.qq, dp.nv,
+                     dp.maxkey, dp.plan, scr, frame_score, frame_budget, segment_id);
+  if ((st = launch_status("k_plan")) != APACK_OK) return st;
+  if (nf > 0) {
+    const int rpb = std::max(1, std::min(kGramRows, (int)(65536 / ((size_t)dim * sizeof(T)))));
+    const size_t smem = (size_t)rpb * dim * sizeof(T);
+    const unsigned gy = (unsigned)((pl.max_per_frame + rpb - 1) / rpb);
+    hipLaunchKernelGGL(k_gram<T>, dim3(nf, gy), dim3(kBlk), smem, s, dp.clips, dp.frames, dp.plan, dim, rpb, xv,
+                       dp.nv, dp.gram);
+    if ((st = launch_status("k_gram")) != APACK_OK) return st;
+    hipLaunchKernelGGL(k_dafps, dim3(nf), dim3(64), 0, s, dp.clips, dp.frames, dp.plan, prm, dp.gram, kept);
+    if ((st = launch_status("k_dafps")) != APACK_OK) return st;
+    hipLaunchKernelGGL(k_dedup<T>, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dp.plan, dim, xv, dp.nv, kept);
+    if ((st = launch_status("k_dedup")) != APACK_OK) return st;
+  }
+  return APACK_OK;
+}
+
+}  // namespace
+
+apack_status launch_dynamics(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& prm, apack_dtype dt, int dim,
+                             const void* visual, const void* audio, const void* query, int64_t visual_rows,
+                             int64_t audio_rows, float* frame_cka, float* frame_score, int32_t* frame_budget,
+                             int32_t* segment_id, uint8_t* gate_fired, int32_t* kept, hipStream_t stream) {
+  if (dt == APACK_BF16)
+    return launch_t<bf16_t>(pl, dp, prm, dim, (const bf16_t*)visual, (const bf16_t*)audio, (const bf16_t*)query,
+                            frame_cka, frame_score, frame_budget, segment_id, gate_fired, kept, visual_rows,
+                            audio_rows, stream);
+  return launch_t<float>(pl, dp, prm, dim, (const float*)visual, (const float*)audio, (const float*)query, frame_cka,
+                         frame_score, frame_budget, segment_id, gate_fired, kept, visual_rows, audio_rows, stream);
+}
+
+}  // namespace apack

@@ -1,0 +1,87 @@
+// Host plan and device descriptors of one apack_score_dynamics call.
+#pragma once
+
+#include <cstdint>
+#include <vector>
+
+#include "common.hpp"
+
+namespace apack {
+
+constexpr int kMaxWindow = 16;   // largest CKA window
+constexpr int kMaxPerFrame = 256;
+
+// Per-clip descriptor on the device.
+struct ClipDev {
+  int64_t vis_off, aud_off, qry_off;  // first rows in the packed inputs
+  int64_t n_audio, n_query;
+  int64_t frame_off;                  // first frame in the [sum F] arrays
+  int64_t token_off;                  // first visual token in [sum F*P] arrays (== frame_off * P for uniform P)
+  int64_t kept_off;                   // first slot of the clip in kept_visual
+  int64_t gram_off;                   // first anchor-Gram slot: frame f uses [gram_off + f*P*P ...)
+  int64_t budget;                     // B_v
+  int32_t n_frames, per_frame;
+  int32_t gate;                       // written on the device
+  int32_t n_seg;                      // written on the device
+};
+
+struct DynParamsDev {
+  double tau_gate, beta, gamma, tau_sim, sigma, lambda_seg, cover, power;
+  int32_t window, dafps_k;
+};
+
+// Per-frame work item: clip and frame index within it.
+struct FrameDev {
+  int32_t clip, f;
+};
+
+struct GemmTileDev {
+  int32_t clip, m0, n0, pad;  // audio row block, visual column block
+};
+
+struct DynPlan {
+  std::vector<ClipDev> clips;
+  std::vector<FrameDev> frames;      // one entry per frame of every clip
+  std::vector<int64_t> budgets;
+  int64_t total_frames = 0, total_tokens = 0, total_audio = 0, total_kept = 0, total_gram = 0;
+  int max_per_frame = 1;
+  int64_t gemm_tiles = 0;            // gate GEMM workgroups over all clips
+  std::vector<GemmTileDev> gemm;
+  // Workspace layout (byte offsets).
+  size_t off_clips = 0, off_frames = 0, off_gemm = 0, blob_bytes = 0;
+  size_t off_v = 0, off_a = 0, off_q = 0, off_band_v = 0, off_band_a = 0, off_vq = 0, off_qq = 0;
+  size_t off_cka = 0, off_nv = 0, off_na = 0, off_maxkey = 0, off_plan = 0, off_gram = 0, off_scratch = 0;
+  size_t ws_bytes = 0;
+};
+
+// Per-frame plan written by k_plan and read by the token-selection kernels.
+struct FramePlanDev {
+  double score;        // s_f
+  double dist;         // d_f (0 when the gate did not fire)
+  int32_t seg;         // segment id within the clip
+  int32_t anchor;      // first frame of the segment (clip-local)
+  int32_t budget;      // k_f
+  int32_t is_anchor;
+  int64_t out_off;     // first kept_visual slot of the frame
+};
+
+
+apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim, const apack_dyn_params* p,
+                            DynPlan& plan);
+
+struct DynPtrs {
+  ClipDev* clips;
+  FrameDev* frames;
+  GemmTileDev* gemm;
+  double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *na, *gram, *scratch;
+  uint32_t* maxkey;
+  FramePlanDev* plan;
+};
+
+apack_status launch_dynamics(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& prm, apack_dtype dt,
+                             int dim, const void* visual, const void* audio, const void* query, int64_t visual_rows,
+                             int64_t audio_rows, float* frame_cka,
+                             float* frame_score, int32_t* frame_budget, int32_t* segment_id, uint8_t* gate_fired,
+                             int32_t* kept, hipStream_t stream);
+
+}  // namespace apack

@@ -1,0 +1,141 @@
+"""GPU parity of the pre-LLM scorer (Section 3.1, Eq. 1-4; Algorithm 1)
+against the fp64 oracle, through the C ABI.
+
+Discrete outputs (gate, segment ids, frame budgets, kept visual rows) must
+be bit-exact; frame CKA and frame scores are fp32 casts of fp64 values and
+must agree to fp32 resolution (1e-5 relative where the fp32 gate GEMM feeds
+them).  Each case first certifies with the oracle that every decision sits
+away from its boundary (1e-9 for fp64 decisions, 1e-4 downstream of the
+fp32 gate GEMM).
+"""
+
+import numpy as np
+import pytest
+
+import workloads as W
+from oracle import dynamics as OD, widen
+from tests.gpu_util import log, to_dev
+
+pytestmark = pytest.mark.gpu
+
+torch = pytest.importorskip("torch")
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import paper_2608_08794_amd as A
+    A.library()
+
+
+def _oracle(case, dtype="bf16"):
+    out = []
+    for s in case.seqs:
+        xv = widen(case.xv, dtype)[s.vis_off:s.vis_off + s.n_frames * s.per_frame]
+        xa = widen(case.xa, dtype)[s.aud_off:s.aud_off + s.n_audio]
+        xq = widen(case.xq, dtype)[s.qry_off:s.qry_off + s.n_query]
+        out.append(OD.score_sequence(xv, xa, xq, s.n_frames, s.per_frame, case.params))
+    return out
+
+
+def _certify(results):
+    for r in results:
+        m = r["margins"]
+        assert m["gate"] > 1e-9 and m["segment"] > 1e-9 and m["segment_budget"] > 1e-9, m
+        assert m["dafps"] > 1e-9 and m["dedup"] > 1e-9, m
+        assert m["frame_budget"] > (1e-4 if r["gate"] else 1e-9), m
+
+
+def _run(case, dtype="bf16"):
+    import paper_2608_08794_amd as A
+    xv, xa, xq = (to_dev(x, dtype) for x in (case.xv, case.xa, case.xq))
+    out = A.apack_score_dynamics(xv, xa, xq, case.seqs, case.params)
+    torch.cuda.synchronize()
+    return {k: (v.cpu().numpy() if hasattr(v, "cpu") else v) for k, v in out.items()}
+
+
+def _compare(case, got, want, dtype="bf16"):
+    f0 = 0
+    kept_all = []
+    for i, (s, r) in enumerate(zip(case.seqs, want)):
+        F = s.n_frames
+        sl = slice(f0, f0 + F)
+        assert bool(got["gate"][i]) == r["gate"], f"clip {i}: gate"
+        np.testing.assert_array_equal(got["segment"][sl], r["segment"], err_msg=f"clip {i}: segments")
+        np.testing.assert_array_equal(got["budget"][sl], r["frame_budget"], err_msg=f"clip {i}: budgets")
+        np.testing.assert_allclose(got["cka"][sl], r["cka"].astype(np.float32), rtol=1e-6, atol=1e-7)
+        tol = 1e-5 if r["gate"] else 1e-6
+        np.testing.assert_allclose(got["score"][sl], r["score"].astype(np.float32), rtol=tol, atol=1e-7)
+        assert got["n_kept"][i] == r["kept"].size
+        kept_all.append(r["kept"] + s.vis_off)
+        f0 += F
+    want_kept = np.concatenate(kept_all) if kept_all else np.zeros(0, np.int64)
+    np.testing.assert_array_equal(got["kept"].astype(np.int64), want_kept)
+
+
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_small_clip_parity(structure):
+    case = W.dynamics_small(structure)
+    log(f"[dynamics] small {structure}")
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_small_clip_parity_fp32_inputs(structure):
+    case = W.dynamics_small(structure)
+    f32 = W.DynamicsCase("f32", case.dim, W.bf16_bits_to_f32(case.xv), W.bf16_bits_to_f32(case.xa),
+                         W.bf16_bits_to_f32(case.xq), case.seqs, case.params)
+    want = _oracle(f32, "f32")
+    _certify(want)
+    _compare(f32, _run(f32, "f32"), want, "f32")
+
+
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_7b_shape_60s_clip_parity(structure):
+    case = W.dynamics_cfg3(structure)
+    log(f"[dynamics] 60 s clip, 3584-d, {structure}")
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+def _packed(parts, params):
+    xv, xa, xq, seqs = [], [], [], []
+    vo = ao = qo = 0
+    for c in parts:
+        s = c.seqs[0]
+        seqs.append(W.AVSeq(s.n_frames, s.per_frame, s.n_audio, s.n_query, vo, ao, qo, s.seg_starts, s.structure))
+        xv.append(c.xv)
+        xa.append(c.xa)
+        xq.append(c.xq)
+        vo += c.xv.shape[0]
+        ao += c.xa.shape[0]
+        qo += c.xq.shape[0]
+    return W.DynamicsCase("bf16", parts[0].dim, np.concatenate(xv), np.concatenate(xa), np.concatenate(xq),
+                          seqs, params)
+
+
+def test_ragged_batch_of_clips_with_edge_shapes():
+    parts = [
+        W.dynamics_small("offset", seed=21, frames=30, per_frame=16, audio=375),
+        W.dynamics_small("shared", seed=22, frames=2, per_frame=7, audio=25),      # F < w
+        W.dynamics_small("shared", seed=23, frames=1, per_frame=5, audio=9),       # one frame
+        W.dynamics_small("offset", seed=24, frames=20, per_frame=70, audio=250),   # P not a multiple of 64
+        W.dynamics_small("shared", seed=25, frames=12, per_frame=256, audio=150),  # largest P
+    ]
+    case = _packed(parts, {"window": 3, "r_pre": 0.5})
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+@pytest.mark.parametrize("r_pre", [1.0, 0.05, 0.6])
+def test_budget_extremes(r_pre):
+    case = W.dynamics_small("offset", seed=31)
+    case.params = {"window": 3, "r_pre": r_pre}
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)

@@ -319,8 +319,19 @@ def apportion(total, weights, caps):
         for i in order[:left]:
             alloc[free_idx[i]] += 1
         if 0 < left < free_idx.size:
-            margin = min(margin, float(frac[order[left - 1]] - frac[order[left]]))
+            margin = min(margin, _cut_gap([frac[i] for i in order], left))
     return alloc, margin
+
+
+def _cut_gap(desc, k):
+    """Gap between the k-th largest value of ``desc`` (sorted descending) and
+    the largest value below it.  Values exactly equal to the k-th are split
+    by index on both sides of any comparison: such ties arise from identical
+    computations (frames sharing a clamped window, identical tokens), which
+    an implementation reproduces bit for bit."""
+    kth = desc[k - 1]
+    below = [x for x in desc[k:] if x < kth]
+    return float(kth - below[0]) if below else math.inf
 
 
 # --------------------------------------------------------------------------
@@ -374,10 +385,10 @@ def dafps(x, k, density_k, cover_thresh, power):
 
 
 def _argmax_lowest(v):
-    """Index of the maximum (lowest index on ties) and the gap to the runner-up."""
+    """Index of the maximum (lowest index on ties) and the gap to the largest
+    value below it (exact ties are split by index, see _cut_gap)."""
     i = int(np.argmax(v))
-    rest = np.delete(v, i)
-    rest = rest[np.isfinite(rest)]
+    rest = v[np.isfinite(v) & (v < v[i])]
     gap = float(v[i] - rest.max()) if rest.size else math.inf
     return i, gap
 
@@ -391,7 +402,7 @@ def dedup(x, anchor, k):
     picks = sorted(order[:k])
     margin = math.inf
     if 0 < k < p:
-        margin = float(sim[order[k]] - sim[order[k - 1]])
+        margin = _cut_gap([-sim[i] for i in order], k)
     return picks, margin
 
 

@@ -223,7 +223,8 @@ apack_status apack_score_dynamics_query(int32_t n_seq, const apack_av_seq* seqs,
  *   kept_visual int32 out: for each clip in order, the ascending packed
  *   visual rows (vis_off + f*P + p) it keeps; kept_capacity >= sum B_v.
  *   n_kept_visual HOST [n_seq] out (may be NULL).
- * dim must be a multiple of 8 and at most 8192.
+ * dim must be a multiple of 8 and at most 16384.  Outputs may overlap neither
+ * the inputs nor each other (APACK_E_ALIAS).
  */
 apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack_dtype dtype,
                                   int32_t dim,

@@ -180,11 +180,15 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   const std::pair<const void*, size_t> outs[] = {{frame_cka, (size_t)nf * 4},   {frame_score, (size_t)nf * 4},
                                                  {frame_budget, (size_t)nf * 4}, {segment_id, (size_t)nf * 4},
                                                  {gate_fired, (size_t)n_seq},    {kept_visual, (size_t)pl.total_kept * 4}};
-  for (const auto& o : outs) {
+  for (size_t i = 0; i < sizeof outs / sizeof outs[0]; ++i) {
+    const auto& o = outs[i];
     if (!o.first) continue;
     APACK_CHECK(!overlaps(o.first, o.second, visual, vb) && !overlaps(o.first, o.second, audio, ab) &&
                     !overlaps(o.first, o.second, query, qb),
                 APACK_E_ALIAS, "an output overlaps an input");
+    for (size_t j = 0; j < i; ++j)
+      APACK_CHECK(!outs[j].first || !overlaps(o.first, o.second, outs[j].first, outs[j].second), APACK_E_ALIAS,
+                  "two outputs overlap");
   }
   APACK_CHECK(workspace && ((uintptr_t)workspace % kAlign) == 0, APACK_E_WORKSPACE,
               "workspace must be non-NULL and %zu-byte aligned", kAlign);

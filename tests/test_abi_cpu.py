@@ -201,3 +201,103 @@ def test_compact_validation_errors(case, status):
 def test_compact_with_nothing_to_copy_is_ok_without_device():
     st, msg = _compact(n_out=0)
     assert st == 0, msg
+
+
+# -- scorer validation (fake device addresses, never dereferenced) ----------
+
+def _av(n_frames=8, per_frame=16, n_audio=100, n_query=4, vis_off=0, aud_off=0, qry_off=0):
+    return L.AVSeq(n_frames, per_frame, n_audio, n_query, vis_off, aud_off, qry_off)
+
+
+def _score(seqs, dim=64, dtype=0, params=None, vis=FAKE, vrows=128, aud=FAKE + (1 << 34), arows=100,
+           qry=FAKE + (2 << 34), qrows=4, outs=None, cap=1 << 20, ws=FAKE + (4 << 34), ws_bytes=1 << 30):
+    p = A.apack_dyn_params_default()
+    for key, val in (params or {}).items():
+        setattr(p, key, val)
+    arr = (L.AVSeq * max(1, len(seqs)))(*seqs)
+    base = FAKE + (8 << 34)
+    outs = outs or [base + i * (1 << 30) for i in range(6)]
+    nk = (ctypes.c_int64 * max(1, len(seqs)))()
+    st = A.library().apack_score_dynamics(len(seqs), arr, dtype, dim, vis, vrows, aud, arows, qry, qrows,
+                                          ctypes.byref(p), *outs, cap, nk, ws, ws_bytes, None)
+    return st, A.library().apack_last_error().decode(), list(nk)
+
+
+def test_score_query_reports_budgets_and_workspace():
+    seqs = [_av(), _av(n_frames=30, per_frame=144, n_audio=750, vis_off=128, aud_off=100, qry_off=4)]
+    arr = (L.AVSeq * 2)(*seqs)
+    p = A.apack_dyn_params_default()
+    nk = (ctypes.c_int64 * 2)()
+    ws = ctypes.c_size_t(0)
+    assert A.library().apack_score_dynamics_query(2, arr, 3584, ctypes.byref(p), nk, ctypes.byref(ws)) == 0
+    assert list(nk) == [OD.visual_budget(0.5, 100, 128), OD.visual_budget(0.5, 750, 30 * 144)]
+    assert ws.value > 0 and ws.value % 256 == 0
+
+
+def test_score_empty_batch_is_ok_without_device():
+    st, msg, _ = _score([])
+    assert st == 0, msg
+
+
+@pytest.mark.parametrize("case,status", [
+    ("window0", 1), ("window17", 1), ("dafps_k", 1), ("sigma", 1), ("beta", 1), ("r_pre", 1), ("cover", 1),
+    ("power", 1), ("tau_nan", 1), ("dim_odd", 2), ("dim_big", 2), ("per_frame", 2), ("no_audio", 2),
+    ("no_query", 2), ("neg_off", 2), ("vis_rows", 2), ("aud_rows", 2), ("qry_rows", 2), ("capacity", 2),
+    ("null_visual", 1), ("misaligned", 1), ("null_kept", 1), ("out_in", 5), ("out_out", 5), ("small_ws", 4),
+    ("misaligned_ws", 4), ("null_ws", 4), ("dtype", 3),
+])
+def test_score_validation_errors(case, status):
+    kw = {}
+    seqs = [_av()]
+    base = FAKE + (8 << 34)
+    outs = [base + i * (1 << 30) for i in range(6)]
+    params = {"window0": {"window": 0}, "window17": {"window": 17}, "dafps_k": {"dafps_k": 33},
+              "sigma": {"sigma": 0.0}, "beta": {"beta": 1.5}, "r_pre": {"r_pre": 1.01},
+              "cover": {"cover_thresh": 1.5}, "power": {"dafps_power": -1.0},
+              "tau_nan": {"tau_gate": float("nan")}}
+    if case in params:
+        kw = dict(params=params[case])
+    elif case == "dim_odd":
+        kw = dict(dim=100)
+    elif case == "dim_big":
+        kw = dict(dim=16392)
+    elif case == "per_frame":
+        seqs = [_av(per_frame=257)]
+    elif case == "no_audio":
+        seqs = [_av(n_audio=0)]
+    elif case == "no_query":
+        seqs = [_av(n_query=0)]
+    elif case == "neg_off":
+        seqs = [_av(aud_off=-1)]
+    elif case == "vis_rows":
+        kw = dict(vrows=127)
+    elif case == "aud_rows":
+        kw = dict(arows=99)
+    elif case == "qry_rows":
+        kw = dict(qrows=3)
+    elif case == "capacity":
+        kw = dict(cap=OD.visual_budget(0.5, 100, 128) - 1)
+    elif case == "null_visual":
+        kw = dict(vis=None)
+    elif case == "misaligned":
+        kw = dict(aud=FAKE + (1 << 34) + 8)
+    elif case == "null_kept":
+        outs[5] = None
+        kw = dict(outs=outs)
+    elif case == "out_in":
+        outs[1] = FAKE + 64
+        kw = dict(outs=outs)
+    elif case == "out_out":
+        outs[3] = outs[0] + 4
+        kw = dict(outs=outs)
+    elif case == "small_ws":
+        kw = dict(ws_bytes=256)
+    elif case == "misaligned_ws":
+        kw = dict(ws=FAKE + (4 << 34) + 16)
+    elif case == "null_ws":
+        kw = dict(ws=None)
+    elif case == "dtype":
+        kw = dict(dtype=4)
+    st, msg, nk = _score(seqs, **kw)
+    assert st == status, (msg, case)
+    assert msg

@@ -62,12 +62,15 @@ template <> struct Mma<float> {
   static __device__ __forceinline__ frag zero() { return 0.0f; }
 };
 
+// Key tiles live in LDS as unpadded rows whose 16-byte chunks are permuted
+// by an XOR with the row index (chunk c of row r sits at c ^ (r & kSwz)), so
+// the 32 rows one fragment read touches fall into distinct bank groups.
 template <class T, int D>
 struct TileGeom {
   static constexpr int kRowBytes = D * (int)sizeof(T);
-  static constexpr int kPitch = kRowBytes + 16;      // padded LDS row (bytes)
-  static constexpr int kUnits = kRowBytes / 16;      // 16-byte units per row
-  static constexpr int kTileBytes = kKeyTile * kPitch;
+  static constexpr int kChunks = kRowBytes / 16;     // 16-byte chunks per row
+  static constexpr int kSwz = (kChunks < 16 ? kChunks : 16) - 1;
+  static constexpr int kTileBytes = kKeyTile * kRowBytes;
   static constexpr int kSteps = D / Mma<T>::kstep;
 };
 
@@ -102,37 +105,46 @@ __device__ __forceinline__ void load_q(QFrags<T, D>& qfr, const T* q, int64_t q_
   }
 }
 
-// Global -> register staging of one key tile (kKeyTile rows of D elements).
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* glb_ptr_t;
+
+// Global -> LDS copy of one key tile (kKeyTile rows of D elements) with
+// 16-byte direct-to-LDS loads: wave-level load j fills LDS bytes
+// [1024 j, 1024 (j+1)), lane t the 16 bytes at 1024 j + 16 t.  Rows past
+// n_rows repeat row n_rows - 1 (valid memory; their results are masked or
+// never written).  Completion is awaited with vmcnt before the barrier.
 template <class T, int D, int NW>
-struct KStage {
+struct KTileLoad {
   using G = TileGeom<T, D>;
-  static constexpr int kPer = (kKeyTile * G::kUnits + NW * kWave - 1) / (NW * kWave);
-  uint4 r[kPer];
-  __device__ __forceinline__ void load(const T* kbase, int64_t row0, int64_t n_rows, int tid) {
+  static constexpr int kLoads = G::kTileBytes / 1024;
+  static constexpr int kPer = (kLoads + NW - 1) / NW;
+  static_assert(G::kTileBytes % 1024 == 0, "tile must be a whole number of 1 KiB loads");
+  __device__ __forceinline__ static void issue(char* lds, const T* kbase, int64_t row0, int64_t n_rows, int wave,
+                                               int lane) {
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
-      const int u = tid + i * NW * kWave;
-      const int row = u / G::kUnits, col = u % G::kUnits;
-      uint4 v = make_uint4(0, 0, 0, 0);
-      if (row < kKeyTile && row0 + row < n_rows)
-        v = *reinterpret_cast<const uint4*>(reinterpret_cast<const char*>(kbase + (row0 + row) * D) + col * 16);
-      r[i] = v;
-    }
-  }
-  __device__ __forceinline__ void store(char* lds, int tid) const {
-#pragma unroll
-    for (int i = 0; i < kPer; ++i) {
-      const int u = tid + i * NW * kWave;
-      const int row = u / G::kUnits, col = u % G::kUnits;
-      if (row < kKeyTile) *reinterpret_cast<uint4*>(lds + row * G::kPitch + col * 16) = r[i];
+      const int j = wave + i * NW;
+      if (j < kLoads) {
+        const int byte = j * 1024 + lane * 16;
+        const int r = byte / G::kRowBytes;
+        const int c = ((byte % G::kRowBytes) >> 4) ^ (r & G::kSwz);
+        int64_t row = row0 + r;
+        if (row >= n_rows) row = n_rows - 1;
+        const char* src = reinterpret_cast<const char*>(kbase + row * D) + c * 16;
+        __builtin_amdgcn_global_load_lds((glb_ptr_t)src, (lds_ptr_t)(lds + j * 1024), 16, 0, 0);
+      }
     }
   }
 };
 
+__device__ __forceinline__ void wait_tile_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
 template <class T, int D>
 __device__ __forceinline__ typename Mma<T>::frag lds_frag(const char* lds, int key, int ks, int lane) {
   using M = Mma<T>;
-  const char* p = lds + key * TileGeom<T, D>::kPitch + (ks * M::kstep + (lane >> 5) * M::lane_k) * (int)sizeof(T);
+  using G = TileGeom<T, D>;
+  const int byte = (ks * M::kstep + (lane >> 5) * M::lane_k) * (int)sizeof(T);
+  const char* p = lds + key * G::kRowBytes + ((((byte >> 4) ^ (key & G::kSwz)) << 4) | (byte & 15));
   return *reinterpret_cast<const typename M::frag*>(p);
 }
 
@@ -147,6 +159,68 @@ struct KFrags {
 };
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
+
+// ---------------------------------------------------------------------------
+// Software pipeline of both passes.  Each wave issues the MFMAs of key
+// block b while its VALU works on the logits of block b-1, so the matrix
+// core and the vector ALU run together; the instruction groups below fix
+// that interleave for the bf16 MFMA (the fp32 MFMA path keeps the
+// compiler's order).
+// ---------------------------------------------------------------------------
+enum : int { kSchedVALU = 0x002, kSchedMFMA = 0x008 };
+
+template <class T, int N_MFMA, int N_PER>
+__device__ __forceinline__ void interleave_hint() {
+  if constexpr (sizeof(T) == 2) {
+#pragma unroll
+    for (int i = 0; i < N_MFMA; ++i) {
+      __builtin_amdgcn_sched_group_barrier(kSchedMFMA, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(kSchedVALU, N_PER, 0);
+    }
+  }
+}
+
+// The next block's K fragments are prefetched into registers for the bf16
+// MFMA (32 VGPRs per block); the fp32 fragments of a block are too large.
+template <class T>
+constexpr bool kPrefetchFrags = sizeof(T) == 2;
+
+__device__ __forceinline__ f32x16 neg_inf16() {
+  f32x16 c;
+#pragma unroll
+  for (int e = 0; e < 16; ++e) c[e] = -INFINITY;
+  return c;
+}
+
+// Accumulator start of one key block in C = K Q^T: 0 for candidate keys and
+// -inf for the rest, so non-candidate logits leave the MFMA as -inf.
+__device__ __forceinline__ f32x16 mask_init(const float* lm, int kb, int lane) {
+  f32x16 c;
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const float4 v = *reinterpret_cast<const float4*>(lm + kb * 32 + 8 * i + 4 * (lane >> 5));
+    c[4 * i + 0] = v.x;
+    c[4 * i + 1] = v.y;
+    c[4 * i + 2] = v.z;
+    c[4 * i + 3] = v.w;
+  }
+  return c;
+}
+
+// Online (max, sum exp2) update of one query row with 16 of its logits.
+// All -inf (masked keys, or the empty first pipeline stage) leaves m and s
+// unchanged.
+__device__ __forceinline__ void row_update(const f32x16& x, float scale, float& m_run, float& s_run) {
+  float lmax = x[0];
+#pragma unroll
+  for (int e = 1; e < 16; ++e) lmax = fmaxf(lmax, x[e]);
+  const float m_new = fmaxf(m_run, lmax * scale);
+  float p[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+  for (int e = 0; e < 16; ++e) p[e & 3] += fast_exp2(fmaf(x[e], scale, -m_new));
+  s_run = fmaf(s_run, fast_exp2(m_run - m_new), (p[0] + p[1]) + (p[2] + p[3]));
+  m_run = m_new;
+}
 
 // ---------------------------------------------------------------------------
 // Pass 1: per query row, online max and sum of exp2 over one key chunk.
@@ -165,7 +239,6 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   constexpr int NKB = kKeyTile / 32;
   __shared__ __attribute__((aligned(16))) char lds[2][G::kTileBytes];
   __shared__ __attribute__((aligned(16))) float lmask[2][kKeyTile];
-  __shared__ int lmasked[2];
 
   const TileDev tl = tiles[blockIdx.x];
   const SeqDev sq = seqs[tl.seq];
@@ -187,72 +260,66 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   const uint8_t* tg = tags + sq.tag_off;
 
   float m_run[kRB], s_run[kRB];
+  f32x16 pend[kRB];  // logits of the block whose VALU work is still due
 #pragma unroll
   for (int rb = 0; rb < kRB; ++rb) {
     m_run[rb] = -FLT_MAX;
     s_run[rb] = 0.f;
+    pend[rb] = neg_inf16();
   }
 
-  KStage<T, D, NW> st;
-  st.load(kbase, key_begin, key_end, tid);
+  if (n_tiles > 0) KTileLoad<T, D, NW>::issue(lds[0], kbase, key_begin, key_end, wave, lane);
   for (int it = 0; it < n_tiles; ++it) {
     const int buf = it & 1;
     const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
-    st.store(lds[buf], tid);
-    if (tid < kKeyTile) {
-      const bool cand = (t0 + tid < key_end) && tg[t0 + tid] != 0;
-      lmask[buf][tid] = cand ? 0.0f : -INFINITY;
-      const uint64_t bal = __ballot(!cand);
-      if (tid == 0) lmasked[buf] = bal != 0;
+    for (int i = tid; i < kKeyTile; i += NW * kWave) {
+      const bool cand = (t0 + i < key_end) && tg[t0 + i] != 0;
+      lmask[buf][i] = cand ? 0.0f : -INFINITY;
     }
+    wait_tile_loads();
     __syncthreads();
-    if (it + 1 < n_tiles) st.load(kbase, t0 + kKeyTile, key_end, tid);
+    if (it + 1 < n_tiles) KTileLoad<T, D, NW>::issue(lds[buf ^ 1], kbase, t0 + kKeyTile, key_end, wave, lane);
     if (active) {
-      const bool masked = lmasked[buf] != 0;
+      // K fragments and mask of block kb+1 are read from LDS while block kb
+      // computes.
+      constexpr int NB = kPrefetchFrags<T> ? 2 : 1;
+      KFrags<T, D> kf[NB];
+      f32x16 init[NB];
+      kf[0].load(lds[buf], 0, lane);
+      init[0] = mask_init(lmask[buf], 0, lane);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
-        KFrags<T, D> kf;
-        kf.load(lds[buf], kb, lane);
-        f32x16 acc[kRB];
+        const int c = kb % NB;
+        if (NB == 1 && kb > 0) {
+          kf[0].load(lds[buf], kb, lane);
+          init[0] = mask_init(lmask[buf], kb, lane);
+        }
+        if (NB == 2 && kb + 1 < NKB) {
+          kf[(kb + 1) % NB].load(lds[buf], kb + 1, lane);
+          init[(kb + 1) % NB] = mask_init(lmask[buf], kb + 1, lane);
+        }
+        f32x16 cur[kRB];
 #pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) acc[rb] = f32x16{};
+        for (int rb = 0; rb < kRB; ++rb) cur[rb] = init[c];
 #pragma unroll
         for (int ks = 0; ks < G::kSteps; ++ks)
 #pragma unroll
-          for (int rb = 0; rb < kRB; ++rb) acc[rb] = M::mma(kf.v[ks], qf[rb][ks], acc[rb]);
-        // acc[rb][e]: query column (lane % 32) of block rb, key row
+          for (int rb = 0; rb < kRB; ++rb) cur[rb] = M::mma(kf[c].v[ks], qf[rb][ks], cur[rb]);
+        // cur[rb][e]: query column (lane % 32) of block rb, key row
         // kb*32 + 8*(e/4) + 4*(lane/32) + e%4.
-        if (masked) {
 #pragma unroll
-          for (int i = 0; i < 4; ++i) {
-            const float4 mk = *reinterpret_cast<const float4*>(&lmask[buf][kb * 32 + 8 * i + 4 * (lane >> 5)]);
+        for (int rb = 0; rb < kRB; ++rb) row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
+        interleave_hint<T, kRB * G::kSteps, 8>();
 #pragma unroll
-            for (int rb = 0; rb < kRB; ++rb) {
-              acc[rb][4 * i + 0] += mk.x;
-              acc[rb][4 * i + 1] += mk.y;
-              acc[rb][4 * i + 2] += mk.z;
-              acc[rb][4 * i + 3] += mk.w;
-            }
-          }
-        }
-#pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) {
-          float lmax = acc[rb][0];
-#pragma unroll
-          for (int e = 1; e < 16; ++e) lmax = fmaxf(lmax, acc[rb][e]);
-          const float m_new = fmaxf(m_run[rb], lmax * scale_log2);
-          float s = 0.f;
-#pragma unroll
-          for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(acc[rb][e], scale_log2, -m_new));
-          s_run[rb] = s_run[rb] * fast_exp2(m_run[rb] - m_new) + s;
-          m_run[rb] = m_new;
-        }
+        for (int rb = 0; rb < kRB; ++rb) pend[rb] = cur[rb];
+        __builtin_amdgcn_sched_barrier(0);  // keep later blocks' LDS reads out of this one
       }
     }
   }
   if (!active) return;
 #pragma unroll
   for (int rb = 0; rb < kRB; ++rb) {
+    row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
     const float mo = __shfl_xor(m_run[rb], 32);
     const float so = __shfl_xor(s_run[rb], 32);
     const float mm = fmaxf(m_run[rb], mo);
@@ -304,9 +371,20 @@ __global__ __launch_bounds__(256) void k_rowreduce(const SeqDev* __restrict__ se
 // ---------------------------------------------------------------------------
 // Pass 2: per key, sum over this group's query rows of exp2(x - b_r).
 // C = Q K^T: lane (l % 32) owns a key column and 16 query rows per block.
-// The exponentials of one (key block, row block) run while the MFMAs of
-// the next pair are in flight.
+// Per-wave column sums of a tile go to one of three LDS slots; the sum over
+// waves of tile t (fixed wave order) is formed at the start of tile t+2,
+// when every wave has finished it, and after the loop for the last two.
 // ---------------------------------------------------------------------------
+template <int NKB, int NW>
+__device__ __forceinline__ void col_flush(float (&red)[3][NW][NKB * 32], int slot, int n_active, int64_t tile0,
+                                          int64_t key_end, float* out, int tid) {
+  for (int i = tid; i < NKB * 32; i += NW * kWave) {
+    float v = 0.f;
+    for (int w = 0; w < n_active; ++w) v += red[slot][w][i];
+    if (tile0 + i < key_end) out[tile0 + i] = v;
+  }
+}
+
 template <class T, int D, int NW>
 __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict__ seqs,
                                                        const TileDev* __restrict__ tiles,
@@ -319,7 +397,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
   __shared__ __attribute__((aligned(16))) char lds[2][G::kTileBytes];
-  __shared__ float red[2][NW][kKeyTile];
+  __shared__ float red[3][NW][kKeyTile];
 
   const TileDev tl = tiles[blockIdx.x];
   const SeqDev sq = seqs[tl.seq];
@@ -355,68 +433,70 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
   const T* kbase = k + (int64_t)tl.g * k_hs + sq.tok_off * D;
   float* out = colpart + sq.colpart_off + (int64_t)(tl.g * sq.n_rg + tl.rg) * sq.n_tokens;
 
-  KStage<T, D, NW> st;
-  st.load(kbase, key_begin, key_end, tid);
+  // The pipeline unit is one (key block, row block) pair: its MFMAs run
+  // while the VALU sums the exponentials of the previous unit into cs, the
+  // running column sum of that unit's key block.
+  f32x16 pend = neg_inf16();
+  float cs = 0.f;
+  auto add_pend = [&](int rb) {
+    float p[4] = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int e = 0; e < 16; ++e) p[e & 3] += fast_exp2(fmaf(pend[e], scale_log2, -b[rb][e]));
+    cs += (p[0] + p[1]) + (p[2] + p[3]);
+  };
+  // Column sums of a finished key block into its tile's slot (lanes < 32).
+  auto flush_block = [&](int slot, int blk) {
+    const float c = cs + __shfl_xor(cs, 32);
+    if (lane < 32) red[slot][wave][blk * 32 + lane] = c;
+    cs = 0.f;
+  };
+
+  if (n_tiles > 0) KTileLoad<T, D, NW>::issue(lds[0], kbase, key_begin, key_end, wave, lane);
   for (int it = 0; it < n_tiles; ++it) {
     const int buf = it & 1;
     const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
-    st.store(lds[buf], tid);
+    wait_tile_loads();
     __syncthreads();
-    // Reduce the previous tile's per-wave sums (its buffer is now stable).
-    if (it > 0 && tid < kKeyTile) {
-      const int64_t key = t0 - kKeyTile + tid;
-      float v = 0.f;
-      for (int w = 0; w < n_active; ++w) v += red[buf ^ 1][w][tid];
-      if (key < key_end) out[key] = v;
-    }
-    if (it + 1 < n_tiles) st.load(kbase, t0 + kKeyTile, key_end, tid);
+    if (it >= 2) col_flush<NKB, NW>(red, (it - 2) % 3, n_active, t0 - 2 * kKeyTile, key_end, out, tid);
+    if (it + 1 < n_tiles) KTileLoad<T, D, NW>::issue(lds[buf ^ 1], kbase, t0 + kKeyTile, key_end, wave, lane);
     if (active) {
-      float cs[NKB];
-      f32x16 prev;
-      int prev_kb = -1, prev_rb = 0;
+      const int slot = it % 3, prev_slot = (it + 2) % 3;
+      // K fragments of block kb+1 are read from LDS while block kb computes.
+      constexpr int NB = kPrefetchFrags<T> ? 2 : 1;
+      KFrags<T, D> kf[NB];
+      kf[0].load(lds[buf], 0, lane);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
-        KFrags<T, D> kf;
-        kf.load(lds[buf], kb, lane);
-        cs[kb] = 0.f;
+        const int c = kb % NB;
+        if (NB == 1 && kb > 0) kf[0].load(lds[buf], kb, lane);
+        if (NB == 2 && kb + 1 < NKB) kf[(kb + 1) % NB].load(lds[buf], kb + 1, lane);
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) {
-          f32x16 acc = f32x16{};
+          f32x16 cur = f32x16{};
 #pragma unroll
-          for (int ks = 0; ks < G::kSteps; ++ks) acc = M::mma(qf[rb][ks], kf.v[ks], acc);
-          if (prev_kb >= 0) {
-            // Epilogue of the previous (key block, row block) pair.
-            float s = 0.f;
-#pragma unroll
-            for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(prev[e], scale_log2, -b[prev_rb][e]));
-            cs[prev_kb] += s;
-          }
-          prev = acc;
-          prev_kb = kb;
-          prev_rb = rb;
+          for (int ks = 0; ks < G::kSteps; ++ks) cur = M::mma(qf[rb][ks], kf[c].v[ks], cur);
+          // cur[e]: key column kb*32 + (lane % 32), query row
+          // rb*32 + 8*(e/4) + 4*(lane/32) + e%4 of this wave.
+          // The pending unit is the previous one; for the first unit of the
+          // first tile it is all -inf and writes zeros to a slot no tile has
+          // used yet.
+          add_pend(rb == 0 ? kRB - 1 : rb - 1);
+          if (rb == 0) flush_block(kb == 0 ? prev_slot : slot, kb == 0 ? NKB - 1 : kb - 1);
+          interleave_hint<T, G::kSteps, 7>();
+          pend = cur;
+          __builtin_amdgcn_sched_barrier(0);
         }
-      }
-      {
-        float s = 0.f;
-#pragma unroll
-        for (int e = 0; e < 16; ++e) s += fast_exp2(fmaf(prev[e], scale_log2, -b[kRB - 1][e]));
-        cs[NKB - 1] += s;
-      }
-#pragma unroll
-      for (int kb = 0; kb < NKB; ++kb) {
-        const float c = cs[kb] + __shfl_xor(cs[kb], 32);
-        if (lane < 32) red[buf][wave][kb * 32 + lane] = c;
       }
     }
   }
-  __syncthreads();
-  if (n_tiles > 0 && tid < kKeyTile) {
-    const int buf = (n_tiles - 1) & 1;
-    const int64_t key = key_begin + (int64_t)(n_tiles - 1) * kKeyTile + tid;
-    float v = 0.f;
-    for (int w = 0; w < n_active; ++w) v += red[buf][w][tid];
-    if (key < key_end) out[key] = v;
+  if (active && n_tiles > 0) {
+    add_pend(kRB - 1);
+    flush_block((n_tiles - 1) % 3, NKB - 1);
   }
+  __syncthreads();
+  const int64_t last0 = key_begin + (int64_t)(n_tiles - 1) * kKeyTile;
+  if (n_tiles >= 2) col_flush<NKB, NW>(red, (n_tiles - 2) % 3, n_active, last0 - kKeyTile, key_end, out, tid);
+  if (n_tiles >= 1) col_flush<NKB, NW>(red, (n_tiles - 1) % 3, n_active, last0, key_end, out, tid);
 }
 
 // ---------------------------------------------------------------------------

@@ -108,7 +108,9 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     for (size_t i = 1; i < r.size(); ++i)
       APACK_CHECK(r[i].first >= r[i - 1].second, APACK_E_SHAPE, "sequences overlap in k");
   }
-  // Keys per workgroup: aim for ~4 workgroups per CU over the whole call.
+  // Keys per workgroup: about one score workgroup per CU over the whole
+  // call (one 7- or 8-wave workgroup fills a CU), so the chip runs a single
+  // round and each workgroup loads its query fragments once.
   const int64_t target = APACK_TILE_TARGET;
   for (int s = 0; s < n_seq; ++s) {
     SeqDev& sd = pl.seqs[s];

@@ -9,13 +9,13 @@
 namespace apack {
 
 #ifndef APACK_KEY_TILE
-#define APACK_KEY_TILE 64
+#define APACK_KEY_TILE 128
 #endif
 #ifndef APACK_ROW_BLOCKS
 #define APACK_ROW_BLOCKS 2
 #endif
 #ifndef APACK_TILE_TARGET
-#define APACK_TILE_TARGET 1024
+#define APACK_TILE_TARGET 256
 #endif
 constexpr int kKeyTile = APACK_KEY_TILE;       // keys per LDS stage of the score kernels
 constexpr int kRB = APACK_ROW_BLOCKS;          // 32-row query blocks held by one wave

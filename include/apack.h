@@ -157,8 +157,10 @@ apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype
  * src_rows is a DEVICE int32 array of n_out indices into [0, n_in), usually
  * apack_prune_layer's kept_rows; an index outside [0, n_in) copies nothing
  * for that row.  k_in, v_in, k_out, v_out are HOST arrays of n_layers device
- * pointers (n_layers <= 64).  Outputs may not overlap inputs
- * (APACK_E_ALIAS): compaction is out of place.
+ * pointers (n_layers <= 64); v_in and v_out may both be NULL, and then only
+ * the n_layers tensors of k_in move (any [hkv][rows][d] planes: a single
+ * layer's K, or V tensors passed in the K slots).  Outputs may not overlap
+ * inputs (APACK_E_ALIAS): compaction is out of place.
  */
 apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows, int64_t n_in,
                               int32_t n_layers,

@@ -234,19 +234,22 @@ def apack_compact_kv(src_rows, n_in, k_in=(), v_in=(), k_out=(), v_out=(), hidde
     the hidden states [rows, H] and the position ids [P, rows]."""
     n_out = int(src_rows.numel())
     n_layers = len(k_in)
-    if not (len(v_in) == len(k_out) == len(v_out) == n_layers):
-        raise ApackError(1, "k_in, v_in, k_out and v_out need one tensor per layer")
+    k_only = n_layers > 0 and len(v_in) == 0 and len(v_out) == 0
+    if len(k_out) != n_layers or (not k_only and not (len(v_in) == len(v_out) == n_layers)):
+        raise ApackError(1, "k_in, v_in, k_out and v_out need one tensor per layer (or empty v_in and v_out)")
     tabs = [(ctypes.c_void_p * max(1, n_layers))() for _ in range(4)]
     hkv = d = 0
     hs_in = hs_out = 0
     code = APACK_BF16
     for l in range(n_layers):
-        for tab, t in zip(tabs, (k_in[l], v_in[l], k_out[l], v_out[l])):
+        planes = (k_in[l], k_out[l]) if k_only else (k_in[l], v_in[l], k_out[l], v_out[l])
+        for tab, t in zip((tabs[0], tabs[2]) if k_only else tabs, planes):
             tab[l] = t.data_ptr()
         hkv, _, d = k_in[l].shape
         hs_in, hs_out = _heads_rows(k_in[l], "k_in"), _heads_rows(k_out[l], "k_out")
-        for t in (v_in[l], v_out[l]):
-            _heads_rows(t, "v")
+        if not k_only:
+            for t in (v_in[l], v_out[l]):
+                _heads_rows(t, "v")
         code = _dtype_code(k_in[l])
     hid = 0
     if hidden_in is not None:
@@ -262,7 +265,8 @@ def apack_compact_kv(src_rows, n_in, k_in=(), v_in=(), k_out=(), v_out=(), hidde
         if pos_in.stride(1) != 1 or pos_out.stride(1) != 1:
             raise ApackError(2, "position ids must have unit column stride")
     _check(library().apack_compact_kv(
-        n_out, _ptr(src_rows), int(n_in), n_layers, tabs[0], tabs[1], tabs[2], tabs[3],
+        n_out, _ptr(src_rows), int(n_in), n_layers, tabs[0], None if k_only else tabs[1], tabs[2],
+        None if k_only else tabs[3],
         hkv, d, code, hs_in, hs_out, _ptr(hidden_in), _ptr(hidden_out), hid,
         _ptr(pos_in), _ptr(pos_out), prow, ps_in, ps_out, _stream(stream)))
 

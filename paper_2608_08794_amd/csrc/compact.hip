@@ -125,8 +125,11 @@ extern "C" apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows,
   APACK_CHECK(hidden_dim >= 0 && pos_rows >= 0, APACK_E_ARG, "negative hidden_dim or pos_rows");
   APACK_CHECK(n_out == 0 || src_rows, APACK_E_ARG, "src_rows is NULL");
   const size_t es = dtype_size(dtype);
+  // v_in and v_out may both be NULL: then only the n_layers K planes move.
+  const bool has_v = v_in != nullptr || v_out != nullptr;
   if (n_layers > 0) {
-    APACK_CHECK(k_in && v_in && k_out && v_out, APACK_E_ARG, "K/V pointer tables must be non-NULL");
+    APACK_CHECK(k_in && k_out, APACK_E_ARG, "K pointer tables must be non-NULL");
+    APACK_CHECK(!has_v || (v_in && v_out), APACK_E_ARG, "v_in and v_out must both be NULL or both be set");
     APACK_CHECK(hkv > 0 && d > 0, APACK_E_SHAPE, "hkv and d must be positive");
     APACK_CHECK(head_stride_in >= n_in * d && head_stride_out >= n_out * d, APACK_E_SHAPE,
                 "head strides must be >= rows * d");
@@ -144,11 +147,14 @@ extern "C" apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows,
   const size_t kv_in_bytes = n_layers ? (size_t)((hkv - 1) * head_stride_in + n_in * d) * es : 0;
   const size_t kv_out_bytes = n_layers ? (size_t)((hkv - 1) * head_stride_out + n_out * d) * es : 0;
   for (int l = 0; l < n_layers; ++l) {
-    APACK_CHECK(k_in[l] && v_in[l] && k_out[l] && v_out[l], APACK_E_ARG, "layer %d: NULL K/V pointer", l);
+    APACK_CHECK(k_in[l] && k_out[l] && (!has_v || (v_in[l] && v_out[l])), APACK_E_ARG,
+                "layer %d: NULL K/V pointer", l);
     ins.emplace_back(k_in[l], kv_in_bytes);
-    ins.emplace_back(v_in[l], kv_in_bytes);
     outs.emplace_back(k_out[l], kv_out_bytes);
-    outs.emplace_back(v_out[l], kv_out_bytes);
+    if (has_v) {
+      ins.emplace_back(v_in[l], kv_in_bytes);
+      outs.emplace_back(v_out[l], kv_out_bytes);
+    }
   }
   if (has_h) {
     ins.emplace_back(hidden_in, (size_t)n_in * hidden_dim * es);
@@ -176,7 +182,8 @@ extern "C" apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows,
   if (n_layers) {
     wide &= kv_row_bytes % 16 == 0 && (head_stride_in * (int64_t)es) % 16 == 0 &&
             (head_stride_out * (int64_t)es) % 16 == 0;
-    for (int l = 0; l < n_layers; ++l) wide &= al16(k_in[l]) && al16(v_in[l]) && al16(k_out[l]) && al16(v_out[l]);
+    for (int l = 0; l < n_layers; ++l)
+      wide &= al16(k_in[l]) && al16(k_out[l]) && (!has_v || (al16(v_in[l]) && al16(v_out[l])));
   }
   if (has_h) wide &= ((int64_t)hidden_dim * (int64_t)es) % 16 == 0 && al16(hidden_in) && al16(hidden_out);
   auto al4 = [](const void* p) { return ((uintptr_t)p % 4) == 0; };
@@ -184,7 +191,7 @@ extern "C" apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows,
     APACK_CHECK(kv_row_bytes % 4 == 0 && ((int64_t)hidden_dim * (int64_t)es) % 4 == 0, APACK_E_UNSUPPORTED,
                 "row sizes must be multiples of 4 bytes");
     for (int l = 0; l < n_layers; ++l)
-      APACK_CHECK(al4(k_in[l]) && al4(v_in[l]) && al4(k_out[l]) && al4(v_out[l]), APACK_E_ARG,
+      APACK_CHECK(al4(k_in[l]) && al4(k_out[l]) && (!has_v || (al4(v_in[l]) && al4(v_out[l]))), APACK_E_ARG,
                   "K/V pointers must be 4-byte aligned");
     if (has_h) APACK_CHECK(al4(hidden_in) && al4(hidden_out), APACK_E_ARG, "hidden must be 4-byte aligned");
   }
@@ -195,7 +202,7 @@ extern "C" apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows,
   a.src = src_rows;
   a.n_out = n_out;
   a.n_in = n_in;
-  a.n_tensors = 2 * n_layers;
+  a.n_tensors = (has_v ? 2 : 1) * n_layers;
   a.heads = n_layers ? hkv : 1;
   if (n_layers) {
     a.row_units = kv_row_bytes / ub;
@@ -205,10 +212,15 @@ extern "C" apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows,
     a.kv_items_per_plane = (n_out + a.kv_rows_per_item - 1) / a.kv_rows_per_item;
     a.kv_items = a.kv_items_per_plane * a.n_tensors * hkv;
     for (int l = 0; l < n_layers; ++l) {
-      a.in[2 * l] = k_in[l];
-      a.in[2 * l + 1] = v_in[l];
-      a.out[2 * l] = k_out[l];
-      a.out[2 * l + 1] = v_out[l];
+      if (has_v) {
+        a.in[2 * l] = k_in[l];
+        a.in[2 * l + 1] = v_in[l];
+        a.out[2 * l] = k_out[l];
+        a.out[2 * l + 1] = v_out[l];
+      } else {
+        a.in[l] = k_in[l];
+        a.out[l] = k_out[l];
+      }
     }
     APACK_CHECK(a.row_units <= kItemUnits, APACK_E_UNSUPPORTED, "K/V rows longer than %d bytes",
                 (int)(kItemUnits * ub));

@@ -8,20 +8,23 @@
 // Kernels (all on the caller's stream, no host synchronisation):
 //   k_rowstats   pass 1: per query row, online (max, sum exp2) over a chunk
 //                of keys; logits from MFMA with Q fragments resident in VGPRs
-//                and K tiles staged through padded, double-buffered LDS.
-//   k_rowreduce  combines the chunk partials of every query row (fixed order)
+//                and K tiles staged through LDS.  The last chunk of each row
+//                group to finish combines the chunk partials (fixed order)
 //                into b_r = max_r + log2(Z_r).
 //   k_colsum     pass 2: recomputes the logits with the roles of the MFMA
 //                operands swapped so the per-key sum over query rows is
 //                lane-local, then a fixed-order cross-wave sum through LDS.
-// The per-group partials are summed into I_j, and the per-modality top-k and
-// ordered kept list are formed, by the kernels of select.hip.
+//                The last workgroup of each key chunk sums the per-group
+//                partials into I_j and counts its first radix digit.
+// The remaining radix digits, the per-modality top-k and the ordered kept
+// list are formed by the kernels of select.hip.
 #include <cfloat>
 #include <cmath>
 #include <vector>
 
 #include "common.hpp"
 #include "prune_plan.hpp"
+#include "radix.hpp"
 
 namespace apack {
 namespace {
@@ -169,9 +172,17 @@ __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_ex
 // ---------------------------------------------------------------------------
 enum : int { kSchedVALU = 0x002, kSchedMFMA = 0x008 };
 
+// VALU instructions placed after each MFMA of a block (0: no placement).
+#ifndef APACK_RS_VALU_PER_MFMA
+#define APACK_RS_VALU_PER_MFMA 8
+#endif
+#ifndef APACK_CS_VALU_PER_MFMA
+#define APACK_CS_VALU_PER_MFMA 7
+#endif
+
 template <class T, int N_MFMA, int N_PER>
 __device__ __forceinline__ void interleave_hint() {
-  if constexpr (sizeof(T) == 2) {
+  if constexpr (sizeof(T) == 2 && N_PER > 0) {
 #pragma unroll
     for (int i = 0; i < N_MFMA; ++i) {
       __builtin_amdgcn_sched_group_barrier(kSchedMFMA, 1, 0);
@@ -222,6 +233,13 @@ __device__ __forceinline__ void row_update(const f32x16& x, float scale, float& 
   m_run = m_new;
 }
 
+// Fixed-order combination of two (max, sum exp2) partials of one row.
+__device__ __forceinline__ void merge(float& m, float& s, float mo, float so) {
+  const float mm = fmaxf(m, mo);
+  s = s * fast_exp2(m - mm) + so * fast_exp2(mo - mm);
+  m = mm;
+}
+
 // ---------------------------------------------------------------------------
 // Pass 1: per query row, online max and sum of exp2 over one key chunk.
 // C = K Q^T: lane (l % 32) owns a query column and 16 key rows per block.
@@ -233,7 +251,9 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
                                                          const T* __restrict__ q, int64_t q_hs,
                                                          const T* __restrict__ k, int64_t k_hs,
                                                          int n_rep, float scale_log2,
-                                                         float2* __restrict__ stats) {
+                                                         float2* __restrict__ stats, float* __restrict__ bias,
+                                                         uint32_t* __restrict__ ctr, uint32_t* __restrict__ zero,
+                                                         int64_t zero_n) {
   using G = TileGeom<T, D>;
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
@@ -247,6 +267,14 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   const int rg_end = min(rows_g, (tl.rg + 1) * sq.rows_per_rg);
   const int row0 = tl.rg * sq.rows_per_rg + wave * kRowsPerWave;
   const bool active = row0 < rg_end;
+
+  // This workgroup's share of clearing the radix histograms used by the
+  // score finalisation at the end of the pass-2 kernel.
+  {
+    const int64_t per = (zero_n + gridDim.x - 1) / gridDim.x;
+    const int64_t z0 = (int64_t)blockIdx.x * per, z1 = min(zero_n, z0 + per);
+    for (int64_t i = z0 + tid; i < z1; i += NW * kWave) zero[i] = 0;
+  }
 
   QFrags<T, D> qfr;
   auto& qf = qfr.v;
@@ -309,63 +337,43 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
         // kb*32 + 8*(e/4) + 4*(lane/32) + e%4.
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
-        interleave_hint<T, kRB * G::kSteps, 8>();
+        interleave_hint<T, kRB * G::kSteps, APACK_RS_VALU_PER_MFMA>();
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) pend[rb] = cur[rb];
         __builtin_amdgcn_sched_barrier(0);  // keep later blocks' LDS reads out of this one
       }
     }
   }
-  if (!active) return;
+  if (active) {
 #pragma unroll
-  for (int rb = 0; rb < kRB; ++rb) {
-    row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
-    const float mo = __shfl_xor(m_run[rb], 32);
-    const float so = __shfl_xor(s_run[rb], 32);
-    const float mm = fmaxf(m_run[rb], mo);
-    const float ss = s_run[rb] * fast_exp2(m_run[rb] - mm) + so * fast_exp2(mo - mm);
-    const int rho = row0 + rb * 32 + lane;
-    if (lane < 32 && rho < rg_end)
-      stats[sq.stats_off + ((int64_t)tl.g * sq.rows_pad + rho) * sq.n_chunks + tl.chunk] = make_float2(mm, ss);
+    for (int rb = 0; rb < kRB; ++rb) {
+      row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
+      const float mo = __shfl_xor(m_run[rb], 32);
+      const float so = __shfl_xor(s_run[rb], 32);
+      const float mm = fmaxf(m_run[rb], mo);
+      const float ss = s_run[rb] * fast_exp2(m_run[rb] - mm) + so * fast_exp2(mo - mm);
+      const int rho = row0 + rb * 32 + lane;
+      if (lane < 32 && rho < rg_end)
+        st_agent(&stats[sq.stats_off + ((int64_t)tl.g * sq.rows_pad + rho) * sq.n_chunks + tl.chunk],
+                 make_float2(mm, ss));
+    }
   }
-}
-
-// ---------------------------------------------------------------------------
-// Combine chunk partials of every (group, padded row): b = M + log2(Z);
-// padding rows get +inf so they contribute exp2(-inf) = 0 in pass 2.
-// One wave per row; lanes stride the chunks; fixed-order tree merge.
-// ---------------------------------------------------------------------------
-__device__ __forceinline__ void merge(float& m, float& s, float mo, float so) {
-  const float mm = fmaxf(m, mo);
-  s = s * fast_exp2(m - mm) + so * fast_exp2(mo - mm);
-  m = mm;
-}
-
-__global__ __launch_bounds__(256) void k_rowreduce(const SeqDev* __restrict__ seqs, int n_seq,
-                                                   int64_t total_rows, int n_rep,
-                                                   const float2* __restrict__ stats, float* __restrict__ bias) {
-  const int64_t row = (int64_t)blockIdx.x * 4 + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= total_rows) return;
-  int lo = 0, hi = n_seq - 1;
-  while (lo < hi) {  // last sequence whose bias_off <= row
-    const int mid = (lo + hi + 1) >> 1;
-    if (seqs[mid].bias_off <= row) lo = mid; else hi = mid - 1;
+  // The last chunk of this (group, row group) to finish combines every
+  // chunk's partials of its rows, in chunk order, into b = M + log2(Z);
+  // padding rows get +inf so they contribute exp2(-inf) = 0 in pass 2.
+  if (!arrive_last<NW * kWave>(ctr + sq.ctr_off + tl.g * sq.n_rg + tl.rg, (uint32_t)sq.n_chunks)) return;
+  const int r_lo = tl.rg * sq.rows_per_rg;
+  for (int rho = r_lo + tid; rho < r_lo + sq.rows_per_rg; rho += NW * kWave) {
+    float m = -FLT_MAX, s = 0.f;
+    if (rho < rows_g) {
+      const float2* p = stats + sq.stats_off + ((int64_t)tl.g * sq.rows_pad + rho) * sq.n_chunks;
+      for (int c = 0; c < sq.n_chunks; ++c) {
+        const float2 v = ld_agent(p + c);
+        merge(m, s, v.x, v.y);
+      }
+    }
+    bias[sq.bias_off + (int64_t)tl.g * sq.rows_pad + rho] = (s > 0.f) ? m + log2f(s) : INFINITY;
   }
-  const SeqDev& sq = seqs[lo];
-  const int64_t r = row - sq.bias_off;            // g * rows_pad + rho
-  const int rho = (int)(r % sq.rows_pad);
-  float m = -FLT_MAX, s = 0.f;
-  if (rho < n_rep * sq.q_len) {
-    const float2* p = stats + sq.stats_off + r * sq.n_chunks;
-    for (int c = lane; c < sq.n_chunks; c += 64) merge(m, s, p[c].x, p[c].y);
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const float mo = __shfl_xor(m, off), so = __shfl_xor(s, off);
-    merge(m, s, mo, so);
-  }
-  if (lane == 0) bias[row] = (s > 0.f) ? m + log2f(s) : INFINITY;
 }
 
 // ---------------------------------------------------------------------------
@@ -381,18 +389,20 @@ __device__ __forceinline__ void col_flush(float (&red)[3][NW][NKB * 32], int slo
   for (int i = tid; i < NKB * 32; i += NW * kWave) {
     float v = 0.f;
     for (int w = 0; w < n_active; ++w) v += red[slot][w][i];
-    if (tile0 + i < key_end) out[tile0 + i] = v;
+    if (tile0 + i < key_end) st_agent(&out[tile0 + i], v);
   }
 }
 
 template <class T, int D, int NW>
-__global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict__ seqs,
+__global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs,
                                                        const TileDev* __restrict__ tiles,
+                                                       const uint8_t* __restrict__ tags,
                                                        const T* __restrict__ q, int64_t q_hs,
                                                        const T* __restrict__ k, int64_t k_hs,
-                                                       int n_rep, float scale_log2,
+                                                       int n_rep, int hkv, float scale_log2,
                                                        const float* __restrict__ bias,
-                                                       float* __restrict__ colpart) {
+                                                       float* __restrict__ colpart, float* __restrict__ scores,
+                                                       uint32_t* __restrict__ hist, uint32_t* __restrict__ ctr) {
   using G = TileGeom<T, D>;
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
@@ -482,7 +492,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
           // used yet.
           add_pend(rb == 0 ? kRB - 1 : rb - 1);
           if (rb == 0) flush_block(kb == 0 ? prev_slot : slot, kb == 0 ? NKB - 1 : kb - 1);
-          interleave_hint<T, G::kSteps, 7>();
+          interleave_hint<T, G::kSteps, APACK_CS_VALU_PER_MFMA>();
           pend = cur;
           __builtin_amdgcn_sched_barrier(0);
         }
@@ -497,6 +507,44 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
   const int64_t last0 = key_begin + (int64_t)(n_tiles - 1) * kKeyTile;
   if (n_tiles >= 2) col_flush<NKB, NW>(red, (n_tiles - 2) % 3, n_active, last0 - kKeyTile, key_end, out, tid);
   if (n_tiles >= 1) col_flush<NKB, NW>(red, (n_tiles - 1) % 3, n_active, last0, key_end, out, tid);
+
+  // The last workgroup of this key chunk (over groups and row groups) forms
+  // I_j = (sum of the per-group partials, fixed order) / (Hq * T), 0 for
+  // non-candidates, and counts the first radix digit; the last chunk of the
+  // sequence picks the digit's bin.  The descriptor is read again here
+  // rather than kept live across the main loop.
+  SeqDev* sr = &seqs[tl.seq];
+  const int planes = hkv * sr->n_rg;
+  if (!arrive_last<NW * kWave>(ctr + sr->ctr_off + planes + tl.chunk, (uint32_t)planes)) return;
+  const bool sel = sr->select[0] || sr->select[1];
+  uint32_t* lh = reinterpret_cast<uint32_t*>(&lds[0][0]);  // 2 x 2048 bins; the key tiles are done
+  if (sel) {
+    for (int b = tid; b < 2 * kRadixBins; b += NW * kWave) lh[b] = 0;
+    __syncthreads();
+  }
+  const uint8_t* tg = tags + sr->tag_off;
+  const float denom = (float)(n_rep * hkv * sr->q_len);
+  const float* cp = colpart + sr->colpart_off;
+  const int64_t n_tok = sr->n_tokens;
+  float* sc = scores + sr->tok_off;
+  const int32_t sel_m[2] = {sr->select[0], sr->select[1]};
+  for (int64_t j = key_begin + tid; j < key_end; j += NW * kWave) {
+    const uint8_t m = tg[j];
+    float v = 0.f;
+    if (m != 0) {
+      float acc = 0.f;
+      for (int pl = 0; pl < planes; ++pl) acc += ld_agent(cp + (int64_t)pl * n_tok + j);
+      v = acc / denom;
+      if ((m == 1 || m == 2) && sel_m[m - 1]) atomicAdd(&lh[(m - 1) * kRadixBins + (clamp_bits(v) >> 20)], 1u);
+    }
+    sc[j] = v;
+  }
+  if (!sel) return;
+  __syncthreads();
+  uint32_t* gh = hist + (int64_t)tl.seq * 2 * kRadixBins;
+  merge_hist<NW * kWave>(lh, gh);
+  if (arrive_last<NW * kWave>(ctr + sr->ctr_off + planes + sr->n_chunks, (uint32_t)sr->n_chunks))
+    pick_bins<NW * kWave>(sr, gh, 0);
 }
 
 // ---------------------------------------------------------------------------
@@ -504,19 +552,17 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(const SeqDev* __restrict_
 // ---------------------------------------------------------------------------
 template <class T, int D, int NW>
 apack_status launch_scores_t(const PrunePlan& pl, const DevPtrs& dp, const void* q, int64_t q_hs,
-                             const void* k, int64_t k_hs, int n_rep, hipStream_t stream) {
+                             const void* k, int64_t k_hs, int n_rep, int hkv, float* scores, hipStream_t stream) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   const int nt = (int)pl.tiles.size();
   if (nt > 0) {
     hipLaunchKernelGGL((k_rowstats<T, D, NW>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles,
-                       dp.tags, (const T*)q, q_hs, (const T*)k, k_hs, n_rep, scale_log2, dp.stats);
+                       dp.tags, (const T*)q, q_hs, (const T*)k, k_hs, n_rep, scale_log2, dp.stats, dp.bias,
+                       dp.ctr, dp.hist, pl.any_select ? select_hist_words((int64_t)pl.seqs.size()) : (int64_t)0);
     APACK_CHECK(launch_status("k_rowstats") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
-    const int64_t rows = pl.total_rows;
-    hipLaunchKernelGGL(k_rowreduce, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream, dp.seqs,
-                       (int)pl.seqs.size(), rows, n_rep, dp.stats, dp.bias);
-    APACK_CHECK(launch_status("k_rowreduce") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
-    hipLaunchKernelGGL((k_colsum<T, D, NW>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles,
-                       (const T*)q, q_hs, (const T*)k, k_hs, n_rep, scale_log2, dp.bias, dp.colpart);
+    hipLaunchKernelGGL((k_colsum<T, D, NW>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles, dp.tags,
+                       (const T*)q, q_hs, (const T*)k, k_hs, n_rep, hkv, scale_log2, dp.bias, dp.colpart, scores,
+                       dp.hist, dp.ctr);
     APACK_CHECK(launch_status("k_colsum") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
   }
   return APACK_OK;
@@ -524,13 +570,13 @@ apack_status launch_scores_t(const PrunePlan& pl, const DevPtrs& dp, const void*
 
 template <class T, int D>
 apack_status launch_scores_d(const PrunePlan& pl, const DevPtrs& dp, const void* q, int64_t q_hs,
-                             const void* k, int64_t k_hs, int n_rep, hipStream_t stream) {
+                             const void* k, int64_t k_hs, int n_rep, int hkv, float* scores, hipStream_t stream) {
   switch (pl.waves) {
-    case 1: return launch_scores_t<T, D, 1>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
-    case 2: return launch_scores_t<T, D, 2>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
-    case 4: return launch_scores_t<T, D, 4>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
-    case 7: return launch_scores_t<T, D, 7>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
-    default: return launch_scores_t<T, D, 8>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
+    case 1: return launch_scores_t<T, D, 1>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
+    case 2: return launch_scores_t<T, D, 2>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
+    case 4: return launch_scores_t<T, D, 4>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
+    case 7: return launch_scores_t<T, D, 7>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
+    default: return launch_scores_t<T, D, 8>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
   }
 }
 
@@ -542,14 +588,14 @@ apack_status launch_prune(const PrunePlan& pl, const DevPtrs& dp, apack_dtype dt
   const int n_rep = hq / hkv;
   apack_status st;
   if (dt == APACK_BF16)
-    st = d == 64 ? launch_scores_d<bf16_t, 64>(pl, dp, q, q_hs, k, k_hs, n_rep, stream)
-                 : launch_scores_d<bf16_t, 128>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
+    st = d == 64 ? launch_scores_d<bf16_t, 64>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream)
+                 : launch_scores_d<bf16_t, 128>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
   else
-    st = d == 64 ? launch_scores_d<float, 64>(pl, dp, q, q_hs, k, k_hs, n_rep, stream)
-                 : launch_scores_d<float, 128>(pl, dp, q, q_hs, k, k_hs, n_rep, stream);
+    st = d == 64 ? launch_scores_d<float, 64>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream)
+                 : launch_scores_d<float, 128>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
   if (st != APACK_OK) return st;
   if (pl.total_tok == 0) return APACK_OK;
-  return launch_select(pl, dp, hq, hkv, scores, kept, stream);
+  return launch_select(pl, dp, scores, kept, stream);
 }
 
 }  // namespace apack

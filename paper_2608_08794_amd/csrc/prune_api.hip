@@ -124,6 +124,8 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     stats += (int64_t)hkv * sd.rows_pad * sd.n_chunks;
     sd.colpart_off = colpart;
     colpart += (int64_t)hkv * sd.n_rg * sd.n_tokens;
+    sd.ctr_off = (int32_t)pl.total_ctr;
+    pl.total_ctr += (int64_t)hkv * sd.n_rg + sd.n_chunks + 1;
     // Tiles: chunks of one (g, rg) eight apart so that both query-row
     // groups of a key chunk land on the same XCD's L2.
     for (int g = 0; g < hkv; ++g)
@@ -146,6 +148,8 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
   c.take<FTileDev>(pl.ftiles.size());
   pl.off_tags = c.used;
   c.take<uint8_t>(pl.total_tok);
+  pl.off_ctr = c.used;
+  c.take<uint32_t>(pl.total_ctr);
   pl.blob_bytes = c.used;
   pl.off_stats = c.used;
   c.take<float2>(pl.total_stats);
@@ -154,7 +158,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
   pl.off_colpart = c.used;
   c.take<float>(pl.total_colpart);
   pl.off_hist = c.used;
-  c.take<uint32_t>(pl.any_select ? pl.seqs.size() * 2 * 2048 : 0);
+  c.take<uint32_t>(pl.any_select ? select_hist_words((int64_t)pl.seqs.size()) : 0);
   pl.off_cnt = c.used;
   c.take<uint32_t>(3 * pl.ftiles.size());
   pl.ws_bytes = std::max<size_t>(c.used, kAlign);
@@ -238,6 +242,7 @@ apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype
       if (sp.modality != APACK_OTHER)
         std::memset(tags + pl.seqs[s].tag_off + sp.begin, sp.modality, (size_t)sp.len);
     }
+  std::memset(h + pl.off_ctr, 0, pl.total_ctr * sizeof(uint32_t));
   hipStream_t hs = static_cast<hipStream_t>(stream);
   char* ws = static_cast<char*>(workspace);
   if ((st = staging_upload(blk, ws, pl.blob_bytes, hs)) != APACK_OK) return st;
@@ -247,6 +252,7 @@ apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype
   dp.ftiles = reinterpret_cast<FTileDev*>(ws + pl.off_ftiles);
   dp.hist = reinterpret_cast<uint32_t*>(ws + pl.off_hist);
   dp.cnt = reinterpret_cast<uint32_t*>(ws + pl.off_cnt);
+  dp.ctr = reinterpret_cast<uint32_t*>(ws + pl.off_ctr);
   dp.tags = reinterpret_cast<uint8_t*>(ws + pl.off_tags);
   dp.stats = reinterpret_cast<float2*>(ws + pl.off_stats);
   dp.bias = reinterpret_cast<float*>(ws + pl.off_bias);

@@ -52,6 +52,7 @@ struct SeqDev {
   uint32_t kk[2];       // rank of the k-th value inside the chosen bucket
   uint32_t done_cnt;    // row tiles finished in the current select pass
   int32_t n_ftiles;     // row tiles of the sequence
+  int32_t ctr_off;      // arrival counters: [hkv*n_rg row groups][n_chunks key chunks][1]
 };
 
 struct FTileDev {
@@ -73,10 +74,11 @@ struct PrunePlan {
   int64_t total_stats = 0;  // (max, sum) partials
   int64_t total_colpart = 0;
   int64_t total_kept = 0;
+  int64_t total_ctr = 0;    // arrival counters (zeroed by the upload)
   int waves = 1;
   bool any_select = false;
   // Workspace layout (byte offsets).
-  size_t off_seqs = 0, off_tiles = 0, off_ftiles = 0, off_tags = 0, blob_bytes = 0;
+  size_t off_seqs = 0, off_tiles = 0, off_ftiles = 0, off_tags = 0, off_ctr = 0, blob_bytes = 0;
   size_t off_stats = 0, off_bias = 0, off_colpart = 0, off_hist = 0, off_cnt = 0, ws_bytes = 0;
 };
 
@@ -90,12 +92,15 @@ struct DevPtrs {
   float* colpart;
   uint32_t* hist;       // [n_seq][2][2048] radix histograms
   uint32_t* cnt;        // [n_ftiles][3] per-tile keep counts
+  uint32_t* ctr;        // arrival counters of the score kernels
 };
 
 apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, int32_t hkv, int32_t d,
                               PrunePlan& plan);
 
-apack_status launch_select(const PrunePlan& pl, const DevPtrs& dp, int hq, int hkv, float* scores, int32_t* kept,
+int64_t select_hist_words(int64_t n_seq);   // radix histogram words of n_seq sequences
+
+apack_status launch_select(const PrunePlan& pl, const DevPtrs& dp, float* scores, int32_t* kept,
                            hipStream_t stream);
 
 apack_status launch_prune(const PrunePlan& pl, const DevPtrs& dp, apack_dtype dt, int d, int hq, int hkv,

@@ -153,7 +153,7 @@ def test_prune_validation_errors(case, status):
 
 
 def _compact(n_out=10, n_in=20, layers=1, src=FAKE, kin=None, kout=None, hid=(0, 0, 0), pos=(0, 0, 0),
-             hkv=2, d=64, dtype=0, hs_in=None, hs_out=None):
+             hkv=2, d=64, dtype=0, hs_in=None, hs_out=None, v_tables=(True, True)):
     P = ctypes.c_void_p * max(1, layers)
     base_in = FAKE + (1 << 34)
     base_out = FAKE + (8 << 34)
@@ -163,7 +163,9 @@ def _compact(n_out=10, n_in=20, layers=1, src=FAKE, kin=None, kout=None, hid=(0,
     vout = [base_out + (1 << 33) + l * (1 << 30) for l in range(layers)]
     hs_in = n_in * d if hs_in is None else hs_in
     hs_out = n_out * d if hs_out is None else hs_out
-    st = A.library().apack_compact_kv(n_out, src, n_in, layers, P(*kin), P(*vin), P(*kout), P(*vout), hkv, d,
+    vin_t = P(*vin) if v_tables[0] else None
+    vout_t = P(*vout) if v_tables[1] else None
+    st = A.library().apack_compact_kv(n_out, src, n_in, layers, P(*kin), vin_t, P(*kout), vout_t, hkv, d,
                                       dtype, hs_in, hs_out, hid[0], hid[1], hid[2], pos[0], pos[1], pos[2],
                                       n_in, n_out, None)
     return st, A.library().apack_last_error().decode()
@@ -171,7 +173,8 @@ def _compact(n_out=10, n_in=20, layers=1, src=FAKE, kin=None, kout=None, hid=(0,
 
 @pytest.mark.parametrize("case,status", [
     ("alias_kv", 5), ("alias_outputs", 5), ("alias_hidden", 5), ("too_many_layers", 1), ("null_src", 1),
-    ("bad_dtype", 3), ("stride", 2), ("null_hidden", 1), ("negative", 2),
+    ("bad_dtype", 3), ("stride", 2), ("null_hidden", 1), ("negative", 2), ("half_v_tables", 1),
+    ("k_only_alias", 5),
 ])
 def test_compact_validation_errors(case, status):
     kw = {}
@@ -193,9 +196,18 @@ def test_compact_validation_errors(case, status):
         kw = dict(hid=(None, FAKE + (30 << 34), 64))
     elif case == "negative":
         kw = dict(n_out=-1)
+    elif case == "half_v_tables":
+        kw = dict(v_tables=(True, False))
+    elif case == "k_only_alias":
+        kw = dict(v_tables=(False, False), kout=[FAKE + (1 << 34) + 256])
     st, msg = _compact(**kw)
     assert st == status, msg
     assert msg
+
+
+def test_compact_k_only_validates_without_device():
+    st, msg = _compact(n_out=0, layers=3, v_tables=(False, False))
+    assert st == 0, msg
 
 
 def test_compact_with_nothing_to_copy_is_ok_without_device():

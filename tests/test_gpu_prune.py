@@ -110,6 +110,22 @@ def test_prune_then_compact_configs_1_to_3(cfg):
     _compact_and_check(cache, kept, case.k.shape[1])
 
 
+def test_compact_k_only_planes():
+    # v_in / v_out empty: only the tensors passed as K move (here a K plane
+    # and a V plane in the K slots), bit-exactly.
+    import paper_2608_08794_amd as A
+    case = W.prune_cfg2()
+    kept = _parity(case)
+    cache = W.cfg_cache(2, case)
+    planes_in = [to_dev(cache.k_layers[0], "bf16"), to_dev(cache.v_layers[0], "bf16")]
+    src = torch.from_numpy(kept.astype(np.int32)).cuda()
+    outs = [torch.empty((x.shape[0], kept.size, x.shape[2]), dtype=x.dtype, device="cuda") for x in planes_in]
+    A.apack_compact_kv(src, case.k.shape[1], planes_in, (), outs, ())
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(bits(outs[0]), raw_bits(cache.k_layers[0], "bf16")[:, kept])
+    np.testing.assert_array_equal(bits(outs[1]), raw_bits(cache.v_layers[0], "bf16")[:, kept])
+
+
 # -- edge cases ---------------------------------------------------------------
 
 

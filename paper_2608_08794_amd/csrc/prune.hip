@@ -367,9 +367,15 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
     float m = -FLT_MAX, s = 0.f;
     if (rho < rows_g) {
       const float2* p = stats + sq.stats_off + ((int64_t)tl.g * sq.rows_pad + rho) * sq.n_chunks;
-      for (int c = 0; c < sq.n_chunks; ++c) {
-        const float2 v = ld_agent(p + c);
-        merge(m, s, v.x, v.y);
+      // Loads in batches (all in flight together), merged in chunk order.
+      constexpr int CB = 16;
+      for (int c0 = 0; c0 < sq.n_chunks; c0 += CB) {
+        float2 v[CB];
+#pragma unroll
+        for (int i = 0; i < CB; ++i) v[i] = c0 + i < sq.n_chunks ? ld_agent(p + c0 + i) : make_float2(0.f, 0.f);
+#pragma unroll
+        for (int i = 0; i < CB; ++i)
+          if (c0 + i < sq.n_chunks) merge(m, s, v[i].x, v[i].y);
       }
     }
     bias[sq.bias_off + (int64_t)tl.g * sq.rows_pad + rho] = (s > 0.f) ? m + log2f(s) : INFINITY;
@@ -528,16 +534,46 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   const int64_t n_tok = sr->n_tokens;
   float* sc = scores + sr->tok_off;
   const int32_t sel_m[2] = {sr->select[0], sr->select[1]};
-  for (int64_t j = key_begin + tid; j < key_end; j += NW * kWave) {
-    const uint8_t m = tg[j];
-    float v = 0.f;
-    if (m != 0) {
-      float acc = 0.f;
-      for (int pl = 0; pl < planes; ++pl) acc += ld_agent(cp + (int64_t)pl * n_tok + j);
-      v = acc / denom;
-      if ((m == 1 || m == 2) && sel_m[m - 1]) atomicAdd(&lh[(m - 1) * kRadixBins + (clamp_bits(v) >> 20)], 1u);
+  // KB keys per thread and PB planes at a time are loaded together, then
+  // summed in plane order.
+  constexpr int KB = 4, PB = 8;
+  for (int64_t j0 = key_begin + tid; j0 < key_end; j0 += (int64_t)KB * NW * kWave) {
+    uint8_t mt[KB];
+    float acc[KB];
+#pragma unroll
+    for (int b = 0; b < KB; ++b) {
+      const int64_t j = j0 + (int64_t)b * NW * kWave;
+      mt[b] = j < key_end ? tg[j] : (uint8_t)0;
+      acc[b] = 0.f;
     }
-    sc[j] = v;
+    for (int p0 = 0; p0 < planes; p0 += PB) {
+      float v[KB][PB];
+#pragma unroll
+      for (int b = 0; b < KB; ++b)
+#pragma unroll
+        for (int i = 0; i < PB; ++i) {
+          const int64_t j = j0 + (int64_t)b * NW * kWave;
+          v[b][i] = (j < key_end && mt[b] != 0 && p0 + i < planes) ? ld_agent(cp + (int64_t)(p0 + i) * n_tok + j)
+                                                                   : 0.f;
+        }
+#pragma unroll
+      for (int b = 0; b < KB; ++b)
+#pragma unroll
+        for (int i = 0; i < PB; ++i)
+          if (p0 + i < planes) acc[b] += v[b][i];
+    }
+#pragma unroll
+    for (int b = 0; b < KB; ++b) {
+      const int64_t j = j0 + (int64_t)b * NW * kWave;
+      if (j >= key_end) continue;
+      const uint8_t m = mt[b];
+      float v = 0.f;
+      if (m != 0) {
+        v = acc[b] / denom;
+        if ((m == 1 || m == 2) && sel_m[m - 1]) atomicAdd(&lh[(m - 1) * kRadixBins + (clamp_bits(v) >> 20)], 1u);
+      }
+      sc[j] = v;
+    }
   }
   if (!sel) return;
   __syncthreads();

@@ -70,6 +70,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--no-cpu-baseline", action="store_true", help="skip the CPU oracle timing")
+    ap.add_argument("--no-other-configs", action="store_true", help="skip the config 2 and 3 measurements")
+    ap.add_argument("--ragged", action="store_true", help="also time the ragged batch of 8 clips (config 5)")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MIB",
                     help="only run a plain device copy of MIB mebibytes three times (reference for HBM "
                          "byte counters) and exit")
@@ -229,36 +231,181 @@ def main():
         "algorithmic_bytes_per_step": step_bytes,
     }
 
+    if not args.no_other_configs:
+        del k_in, v_in, h_in, p_in, queries, steps
+        torch.cuda.empty_cache()
+        result["other_configs"] = other_configs(torch, A, W, args.ragged)
     if not args.no_cpu_baseline:
-        result["cpu_baseline"] = cpu_baseline(case, steps[0])
+        result["cpu_baseline"] = cpu_baseline(case)
     print(json.dumps(result), flush=True)
 
 
-def cpu_baseline(case, st):
-    """fp64 oracle on prune step 1 of the same workload (bounded sample)."""
+def _time_calls(torch, fn, flush, reps=20, warmup=5):
+    """Median device time of fn() over reps, cold (a 512 MiB write before
+    each repetition evicts the 256 MB Infinity Cache) and warm."""
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    out = {}
+    for mode in ("cold", "warm"):
+        ms = []
+        for _ in range(reps):
+            if mode == "cold":
+                flush.fill_(1)
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ms.append(a.elapsed_time(b))
+        out[mode] = float(np.median(ms))
+    return out
+
+
+def _prune_bytes(case, n_kept, n_layers, hidden_dim, e=2):
+    """Algorithmic bytes of one prune + compaction: K over S, Q, scores and
+    kept rows written, one read and one write of every kept row's K/V,
+    hidden state and position ids, and one read of the kept list."""
+    cand = sum(int((s.tags() != 0).sum()) for s in case.seqs)
+    q_rows = sum(s.q_len for s in case.seqs)
+    row = n_layers * 2 * case.hkv * case.d * e + hidden_dim * e + 3 * 4
+    return cand, (cand * case.hkv * case.d * e + case.hq * q_rows * case.d * e + 4 * cand + 4 * n_kept
+                  + n_kept * (2 * row + 4))
+
+
+def other_configs(torch, A, W, with_ragged):
+    """Configs 2, 3 (and 5 with --ragged): the whole launch sequence timed
+    as one, median of 20 after 5 warm-ups, cold and warm."""
+    import workloads as W  # noqa: F811
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    res = {}
+
+    def dev(x):
+        return torch.from_numpy(np.ascontiguousarray(x).view(np.int16)).view(torch.bfloat16).cuda()
+
+    def prune_compact(case, cache):
+        q, k = dev(case.q), dev(case.k)
+        v, hid = dev(cache.v_layers[0]), dev(cache.hidden)
+        pos = torch.from_numpy(cache.pos).cuda()
+        n_kept, wsb = A.apack_prune_layer_query(case.seqs, case.hq, case.hkv, case.d)
+        n_out = int(sum(n_kept))
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+        sc = torch.empty(k.shape[1], dtype=torch.float32, device="cuda")
+        kept = torch.empty(n_out, dtype=torch.int32, device="cuda")
+        k_out = torch.empty((case.hkv, n_out, case.d), dtype=k.dtype, device="cuda")
+        v_out = torch.empty_like(k_out)
+        h_out = torch.empty((n_out, hid.shape[1]), dtype=hid.dtype, device="cuda")
+        p_out = torch.empty((3, n_out), dtype=torch.int32, device="cuda")
+
+        def run():
+            A.apack_prune_layer(q, k, case.seqs, scores=sc, kept_rows=kept, workspace=ws)
+            A.apack_compact_kv(kept, k.shape[1], [k], [v], [k_out], [v_out], hid, h_out, pos, p_out)
+        return run, n_out, hid.shape[1]
+
+    def scorer(dyn):
+        xv, xa, xq = dev(dyn.xv), dev(dyn.xa), dev(dyn.xq)
+        n_kv, wsb = A.apack_score_dynamics_query(dyn.seqs, dyn.dim, dyn.params)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+        nk = int(sum(n_kv))
+        emb = torch.empty((nk, xv.shape[1]), dtype=xv.dtype, device="cuda")
+        bytes_ = 2 * (xv.numel() + xa.numel() + xq.numel()) + 2 * 2 * nk * xv.shape[1]
+
+        def run():
+            out = A.apack_score_dynamics(xv, xa, xq, dyn.seqs, dyn.params, workspace=ws)
+            A.apack_compact_kv(out["kept"], xv.shape[0], hidden_in=xv, hidden_out=emb)
+        return run, bytes_
+
+    def entry(t, cand, nbytes, what):
+        return {"what": what, "candidates": cand, "algorithmic_bytes": int(nbytes),
+                "ms_cold": round(t["cold"], 4), "ms_warm": round(t["warm"], 4),
+                "candidate_tokens_per_s_cold": round(cand / (t["cold"] / 1e3), 1),
+                "achieved_gbs_cold": round(nbytes / (t["cold"] / 1e3) / 1e9, 1)}
+
+    t0 = time.time()
+    case = W.prune_cfg2()
+    cache = W.cfg_cache(2, case)
+    run, n_out, hd = prune_compact(case, cache)
+    cand, nb = _prune_bytes(case, n_out, 1, hd)
+    res["cfg2_3b_layer"] = entry(_time_calls(torch, run, flush), cand, nb,
+                                 "prune + compaction of one layer's K/V, hidden states and positions")
+    log(f"config 2 done ({time.time() - t0:.1f}s)")
+
+    dyn = W.dynamics_cfg3("offset")
+    case = W.prune_cfg3()
+    cache = W.cfg_cache(3, case)
+    s_run, s_bytes = scorer(dyn)
+    p_run, n_out, hd = prune_compact(case, cache)
+    cand, nb = _prune_bytes(case, n_out, 1, hd)
+    ts = _time_calls(torch, s_run, flush)
+    tp = _time_calls(torch, p_run, flush)
+    res["cfg3_7b_scorer_gate_on"] = entry(ts, int(dyn.xv.shape[0]), s_bytes,
+                                          "pre-LLM scorer of a 60 s clip (gate fired) + gather of the kept "
+                                          "visual embeddings")
+    res["cfg3_7b_prune"] = entry(tp, cand, nb, "in-LLM prune + one-layer compaction of the 9454-row sequence")
+    log(f"config 3 done ({time.time() - t0:.1f}s)")
+
+    if with_ragged:
+        rb = W.ragged_batch()
+        log(f"ragged batch generated ({time.time() - t0:.1f}s)")
+        s_run, s_bytes = scorer(rb.dynamics)
+        p_run, n_out, hd = prune_compact(rb.prune, rb.cache)
+        cand, nb = _prune_bytes(rb.prune, n_out, 1, hd)
+
+        def both():
+            s_run()
+            p_run()
+        t = _time_calls(torch, both, flush)
+        res["cfg5_ragged_8_clips"] = entry(t, cand, nb + s_bytes,
+                                           f"scorer + embedding gather + prune + compaction of 8 clips of "
+                                           f"{rb.seconds} s, one launch sequence")
+        log(f"config 5 done ({time.time() - t0:.1f}s)")
+    return res
+
+
+def cpu_baseline(case, repeats=3):
+    """The fp64 oracle on one whole step of the same workload (three prune
+    steps, each with the gather of all 28 layers' K/V, the hidden states and
+    the positions), best of `repeats` runs."""
     from threadpoolctl import threadpool_info
+    import workloads as W
     from oracle import prune as OP, widen
 
-    s = st["seq"]
-    t0 = time.perf_counter()
-    q = widen(case.queries[0], "bf16")
-    k = widen(case.cache.k_layers[st["layer"]], "bf16")
-    r = OP.prune_sequence(q, k, s.tags(), s.keep, s.keep_basis)
-    kept = r["kept"]
-    for x in case.cache.k_layers + case.cache.v_layers:
-        OP.compact_rows(x, kept, axis=1)
-    OP.compact_rows(case.cache.hidden, kept, axis=0)
-    OP.compact_rows(case.cache.pos, kept, axis=1)
-    dt = time.perf_counter() - t0
+    times = []
+    cand = 0
+    for _ in range(repeats):
+        t0 = time.perf_counter()
+        cand = 0
+        k_layers, v_layers, hidden, pos = case.cache.k_layers, case.cache.v_layers, case.cache.hidden, case.cache.pos
+        seq = case.seq()
+        n_a, n_v = case.n_audio, case.n_visual
+        spans, n = list(seq.spans), seq.n_tokens
+        for i, (layer, keep) in enumerate(zip(case.prune_layers, case.keeps)):
+            s = W.PruneSeq(0, n, spans, 0, case.q_len, (keep, keep), (n_a, n_v))
+            q = widen(case.queries[i], "bf16")
+            k = widen(k_layers[layer], "bf16")
+            r = OP.prune_sequence(q, k, s.tags(), s.keep, s.keep_basis)
+            kept = r["kept"]
+            cand += int((s.tags() != 0).sum())
+            k_layers = [OP.compact_rows(x, kept, axis=1) for x in k_layers]
+            v_layers = [OP.compact_rows(x, kept, axis=1) for x in v_layers]
+            hidden = OP.compact_rows(hidden, kept, axis=0)
+            pos = OP.compact_rows(pos, kept, axis=1)
+            ka, kv = r["k"]["audio"], r["k"]["visual"]
+            spans, n = [(0, ka, W.AUDIO), (ka, kv, W.VISUAL)], len(kept)
+        times.append(time.perf_counter() - t0)
+    dt = min(times)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
-    log(f"cpu oracle step 1: {dt:.1f}s")
+    log(f"cpu oracle: {', '.join(f'{t:.1f}' for t in times)} s per step")
     return {
-        "value": round(st["cand"] / dt, 1),
+        "value": round(cand / dt, 1),
         "unit": "candidate tokens/s",
         "cores": threads,
         "kind": "oracle",
-        "sample": f"prune step 1 of 3 ({st['cand']} candidates): fp64 scores, top-k and the gather of all "
-                  f"28 layers' K/V, hidden states and positions; {dt:.1f} s on {os.cpu_count()} host CPUs",
+        "sample": f"one whole step ({cand} candidates over the three prune steps): fp64 scores, top-k and the "
+                  f"gather of all 28 layers' K/V, hidden states and positions; best of {repeats} runs "
+                  f"({', '.join(f'{t:.1f}' for t in times)} s) with {threads} BLAS threads on "
+                  f"{os.cpu_count()} host CPUs",
     }
 
 

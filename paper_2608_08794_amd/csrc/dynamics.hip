@@ -737,6 +737,41 @@ __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
   }
 }
 
+// Density of token i for DA-FPS: the mean of its dafps_k largest cosines to
+// the other tokens of the frame, and how many of those cosines reach the
+// coverage threshold.  The running top list lives in registers (static
+// indices only): each new value is carried down past the larger ones.  S is
+// exactly symmetric (entries (i, j) and (j, i) are the same products summed
+// in the same order), so lane i reads column i and the wave's loads for one
+// j are contiguous.
+template <int KM>
+__device__ __forceinline__ double dafps_density(const double* S, int P, int i, int k, double cover) {
+  double top[KM];
+#pragma unroll
+  for (int q = 0; q < KM; ++q) top[q] = -INFINITY;
+  int cov = 0;
+  for (int j = 0; j < P; ++j) {
+    if (j == i) continue;
+    double v = S[(int64_t)j * P + i];
+    if (v >= cover) ++cov;
+#pragma unroll
+    for (int q = 0; q < KM; ++q) {
+      if (q < k) {
+        const double hi = fmax(top[q], v);
+        v = fmin(top[q], v);
+        top[q] = hi;
+      }
+    }
+  }
+  const int nt = min(k, P - 1);
+  double knn = 0.0;
+#pragma unroll
+  for (int q = 0; q < KM; ++q)
+    if (q < nt) knn += top[q];
+  knn = nt > 0 ? knn / nt : 0.0;
+  return fmax(knn, 0.0) * (1.0 + cov);
+}
+
 // ---------------------------------------------------------------------------
 // DA-FPS on an anchor frame (one wave; up to 4 tokens per lane).
 // ---------------------------------------------------------------------------
@@ -762,34 +797,9 @@ __global__ __launch_bounds__(64) void k_dafps(const ClipDev* __restrict__ clips,
     smax[t] = 0.0;
     taken[t] = i >= P;
     if (i >= P) continue;
-    // Mean of the dafps_k largest cosines to other tokens; coverage count.
-    double top[32];
-    int nt = 0, cov = 0;
-    for (int j = 0; j < P; ++j) {
-      if (j == i) continue;
-      const double s = S[(int64_t)i * P + j];
-      if (s >= prm.cover) ++cov;
-      // insert into the descending top list (length <= dafps_k)
-      if (nt < prm.dafps_k) {
-        int pos = nt++;
-        while (pos > 0 && top[pos - 1] < s) {
-          top[pos] = top[pos - 1];
-          --pos;
-        }
-        top[pos] = s;
-      } else if (s > top[nt - 1]) {
-        int pos = nt - 1;
-        while (pos > 0 && top[pos - 1] < s) {
-          top[pos] = top[pos - 1];
-          --pos;
-        }
-        top[pos] = s;
-      }
-    }
-    double knn = 0.0;
-    for (int q = 0; q < nt; ++q) knn += top[q];
-    knn = nt ? knn / nt : 0.0;
-    rho[t] = fmax(knn, 0.0) * (1.0 + cov);
+    rho[t] = prm.dafps_k <= 8    ? dafps_density<8>(S, P, i, prm.dafps_k, prm.cover)
+             : prm.dafps_k <= 16 ? dafps_density<16>(S, P, i, prm.dafps_k, prm.cover)
+                                 : dafps_density<32>(S, P, i, prm.dafps_k, prm.cover);
     wgt[t] = pow(rho[t], prm.power);
   }
   // First pick: the densest token.

@@ -14,7 +14,8 @@
 //                continuity smoothing and cuts, Eq. 3 segment scores, frame
 //                scores, Eq. 4 segment budgets and frame budgets (capped
 //                largest remainder), anchors and output offsets
-//   k_gram       fp64 cosine Gram of the tokens of every anchor frame
+//   k_gram       fp64 cosine Gram of the tokens of every anchor frame (fp64
+//                MFMA)
 //   k_dafps      one wave per anchor frame: density-aware farthest-point
 //                sampling
 //   k_dedup      one workgroup per non-anchor frame: keep the positions least
@@ -667,60 +668,70 @@ __global__ __launch_bounds__(kBlk) void k_plan(ClipDev* __restrict__ clips, DynP
 }
 
 // ---------------------------------------------------------------------------
-// Cosine Gram of an anchor frame's tokens: rows i0 .. i0+7 against all P.
+// Cosine Gram of an anchor frame's P tokens in fp64 on the matrix cores
+// (v_mfma_f64_16x16x4f64).  One wave per 16 x 16 tile of the upper triangle;
+// each tile is written twice, (i, j) and (j, i), so S is exactly symmetric.
+// MFMA operands: lane l supplies A[l % 16][k = l / 16] and B[k = l / 16][l % 16];
+// accumulator element e of lane l is D[4e + l / 16][l % 16].  Each lane
+// loads 8 consecutive elements of its row and feeds them to 8 MFMAs, lane
+// group g = l / 16 covering elements [k0 + 8g, k0 + 8g + 8) of a 32-element
+// step; A and B use the same assignment, so every product enters once.
 // ---------------------------------------------------------------------------
-constexpr int kGramRows = 8;
+typedef double f64x4 __attribute__((ext_vector_type(4)));
+constexpr int kGramTile = 16;
+constexpr int kGramWaves = 4;  // tiles per workgroup
 
 template <class T>
-__global__ __launch_bounds__(kBlk) void k_gram(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
-                                               const FramePlanDev* __restrict__ plan, int dim, int rows_per_block,
-                                               const T* __restrict__ xv, const double* __restrict__ nv,
-                                               double* __restrict__ gram) {
-  extern __shared__ __attribute__((aligned(16))) char smem[];
+__global__ __launch_bounds__(kGramWaves * 64) void k_gram(const ClipDev* __restrict__ clips,
+                                                          const FrameDev* __restrict__ frames,
+                                                          const FramePlanDev* __restrict__ plan, int dim,
+                                                          const T* __restrict__ xv, const double* __restrict__ nv,
+                                                          double* __restrict__ gram) {
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
   const int64_t frame = c.frame_off + fr.f;
   const FramePlanDev fp = plan[frame];
   if (!fp.is_anchor || fp.budget == 0) return;
   const int P = c.per_frame;
-  const int i0 = blockIdx.y * rows_per_block;
-  if (i0 >= P) return;
-  const int ni = min(rows_per_block, P - i0);
-  const int64_t row0 = c.vis_off + (int64_t)fr.f * P;
-  T* rows = reinterpret_cast<T*>(smem);
-  for (int u = threadIdx.x * 8; u < ni * dim; u += kBlk * 8) {
-    const int r = u / dim, col = u % dim;
-    const T* src = xv + (row0 + i0 + r) * dim + col;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) rows[r * dim + col + e] = src[e];
+  const int nt = (P + kGramTile - 1) / kGramTile;
+  int t = blockIdx.y * kGramWaves + (threadIdx.x >> 6);
+  if (t >= nt * (nt + 1) / 2) return;
+  int ti = 0;
+  while (t >= nt - ti) {  // row-major upper triangle: tile (ti, tj), tj >= ti
+    t -= nt - ti;
+    ++ti;
   }
-  __syncthreads();
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  double* g = gram + c.gram_off + (int64_t)fr.f * P * P;
-  for (int j = wave; j < P; j += kBlk / 64) {
-    double acc[kGramRows], o[8];
+  const int tj = ti + t;
+  const int lane = threadIdx.x & 63, g = lane >> 4, r16 = lane & 15;
+  const int64_t row0 = c.vis_off + (int64_t)fr.f * P;
+  const int ra = min(ti * kGramTile + r16, P - 1), rb = min(tj * kGramTile + r16, P - 1);
+  const T* xa = xv + (row0 + ra) * dim;
+  const T* xb = xv + (row0 + rb) * dim;
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+  for (int k0 = 0; k0 < dim; k0 += 32) {
+    const int kk = k0 + 8 * g;
+    double a[8], b[8];
+    if (kk < dim) {
+      load8(xa + kk, a);
+      load8(xb + kk, b);
+    } else {
 #pragma unroll
-    for (int r = 0; r < kGramRows; ++r) acc[r] = 0.0;
-    const T* xj = xv + (row0 + j) * dim;
-    for (int d = lane * 8; d < dim; d += 64 * 8) {
-      load8(xj + d, o);
-#pragma unroll
-      for (int r = 0; r < kGramRows; ++r) {
-        if (r < ni) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) acc[r] += widen(rows[r * dim + d + e]) * o[e];
-        }
-      }
+      for (int e = 0; e < 8; ++e) a[e] = b[e] = 0.0;
     }
-    const double nj = sqrt(nv[row0 + j]);
 #pragma unroll
-    for (int r = 0; r < kGramRows; ++r) {
-      const double s = wave_sum(acc[r]);
-      if (lane == 0 && r < ni) {
-        const double ni_ = sqrt(nv[row0 + i0 + r]);
-        g[(int64_t)(i0 + r) * P + j] = (ni_ == 0.0 || nj == 0.0) ? 0.0 : s / (ni_ * nj);
-      }
-    }
+    for (int e = 0; e < 8; ++e) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a[e], b[e], acc, 0, 0, 0);
+  }
+  double* G = gram + c.gram_off + (int64_t)fr.f * P * P;
+  const int col = tj * kGramTile + r16;
+  const double nc = col < P ? sqrt(nv[row0 + col]) : 0.0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int row = ti * kGramTile + 4 * e + g;
+    if (row >= P || col >= P) continue;
+    const double nr = sqrt(nv[row0 + row]);
+    const double v = (nr == 0.0 || nc == 0.0) ? 0.0 : acc[e] / (nr * nc);
+    G[(int64_t)row * P + col] = v;
+    G[(int64_t)col * P + row] = v;
   }
 }
 
@@ -742,24 +753,31 @@ __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
 // coverage threshold.  The running top list lives in registers (static
 // indices only): each new value is carried down past the larger ones.  S is
 // exactly symmetric (entries (i, j) and (j, i) are the same products summed
-// in the same order), so lane i reads column i and the wave's loads for one
-// j are contiguous.
+// in the same order), so thread i reads column i and a wave's loads for one
+// j are contiguous; loads are issued eight at a time.
 template <int KM>
 __device__ __forceinline__ double dafps_density(const double* S, int P, int i, int k, double cover) {
   double top[KM];
 #pragma unroll
   for (int q = 0; q < KM; ++q) top[q] = -INFINITY;
   int cov = 0;
-  for (int j = 0; j < P; ++j) {
-    if (j == i) continue;
-    double v = S[(int64_t)j * P + i];
-    if (v >= cover) ++cov;
+  for (int j0 = 0; j0 < P; j0 += 8) {
+    double vals[8];
 #pragma unroll
-    for (int q = 0; q < KM; ++q) {
-      if (q < k) {
-        const double hi = fmax(top[q], v);
-        v = fmin(top[q], v);
-        top[q] = hi;
+    for (int u = 0; u < 8; ++u) vals[u] = j0 + u < P ? S[(int64_t)(j0 + u) * P + i] : 0.0;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + u;
+      if (j >= P || j == i) continue;
+      double v = vals[u];
+      if (v >= cover) ++cov;
+#pragma unroll
+      for (int q = 0; q < KM; ++q) {
+        if (q < k) {
+          const double hi = fmax(top[q], v);
+          v = fmin(top[q], v);
+          top[q] = hi;
+        }
       }
     }
   }
@@ -772,80 +790,74 @@ __device__ __forceinline__ double dafps_density(const double* S, int P, int i, i
   return fmax(knn, 0.0) * (1.0 + cov);
 }
 
+// Block-wide lexicographic (value desc, index asc) argmax; every thread
+// gets the winning index.
+__device__ __forceinline__ int block_argmax(double v, int idx, double* sv, int* si) {
+  wave_argmax(v, idx);
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  if (lane == 0) {
+    sv[wave] = v;
+    si[wave] = idx;
+  }
+  __syncthreads();
+  double bv = sv[0];
+  int bi = si[0];
+#pragma unroll
+  for (int w = 1; w < kMaxPerFrame / 64; ++w)
+    if (sv[w] > bv || (sv[w] == bv && si[w] < bi)) {
+      bv = sv[w];
+      bi = si[w];
+    }
+  __syncthreads();
+  return bi;
+}
+
 // ---------------------------------------------------------------------------
-// DA-FPS on an anchor frame (one wave; up to 4 tokens per lane).
+// DA-FPS on an anchor frame: one workgroup, thread i owns token i.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(64) void k_dafps(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
-                                              const FramePlanDev* __restrict__ plan, DynParamsDev prm,
-                                              const double* __restrict__ gram, int32_t* __restrict__ kept) {
+__global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restrict__ clips,
+                                                        const FrameDev* __restrict__ frames,
+                                                        const FramePlanDev* __restrict__ plan, DynParamsDev prm,
+                                                        const double* __restrict__ gram, int32_t* __restrict__ kept) {
+  __shared__ double sv[kMaxPerFrame / 64];
+  __shared__ int si[kMaxPerFrame / 64];
+  __shared__ int wcount[kMaxPerFrame / 64];
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
   const int64_t frame = c.frame_off + fr.f;
   const FramePlanDev fp = plan[frame];
   if (!fp.is_anchor || fp.budget == 0) return;
-  const int P = c.per_frame, lane = threadIdx.x;
+  const int P = c.per_frame, i = threadIdx.x;
   const int k = min(fp.budget, P);
   const double* S = gram + c.gram_off + (int64_t)fr.f * P * P;
-  constexpr int kT = kMaxPerFrame / 64;
-  double rho[kT], wgt[kT], smax[kT];
-  bool taken[kT];
-#pragma unroll
-  for (int t = 0; t < kT; ++t) {
-    const int i = lane + 64 * t;
-    rho[t] = -INFINITY;
-    wgt[t] = 0.0;
-    smax[t] = 0.0;
-    taken[t] = i >= P;
-    if (i >= P) continue;
-    rho[t] = prm.dafps_k <= 8    ? dafps_density<8>(S, P, i, prm.dafps_k, prm.cover)
-             : prm.dafps_k <= 16 ? dafps_density<16>(S, P, i, prm.dafps_k, prm.cover)
-                                 : dafps_density<32>(S, P, i, prm.dafps_k, prm.cover);
-    wgt[t] = pow(rho[t], prm.power);
+  const bool mine = i < P;
+  double rho = -INFINITY, wgt = 0.0, smax = 0.0;
+  bool taken = !mine;
+  if (mine) {
+    rho = prm.dafps_k <= 8    ? dafps_density<8>(S, P, i, prm.dafps_k, prm.cover)
+          : prm.dafps_k <= 16 ? dafps_density<16>(S, P, i, prm.dafps_k, prm.cover)
+                              : dafps_density<32>(S, P, i, prm.dafps_k, prm.cover);
+    wgt = pow(rho, prm.power);
   }
-  // First pick: the densest token.
-  double bv = -INFINITY;
-  int bi = 0x7FFFFFFF;
-#pragma unroll
-  for (int t = 0; t < kT; ++t)
-    if (!taken[t] && (rho[t] > bv || (rho[t] == bv && lane + 64 * t < bi))) {
-      bv = rho[t];
-      bi = lane + 64 * t;
-    }
-  wave_argmax(bv, bi);
-  int pick = bi;
+  // First pick: the densest token; then the farthest from the picked set,
+  // weighted by density.
+  int pick = block_argmax(taken ? -INFINITY : rho, taken ? 0x7FFFFFFF : i, sv, si);
   for (int n = 0;; ++n) {
-#pragma unroll
-    for (int t = 0; t < kT; ++t) {
-      const int i = lane + 64 * t;
-      if (i == pick) taken[t] = true;
-      if (i < P) smax[t] = n == 0 ? S[(int64_t)pick * P + i] : fmax(smax[t], S[(int64_t)pick * P + i]);
-    }
+    if (i == pick) taken = true;
+    if (mine) smax = n == 0 ? S[(int64_t)pick * P + i] : fmax(smax, S[(int64_t)pick * P + i]);
     if (n + 1 >= k) break;
-    bv = -INFINITY;
-    bi = 0x7FFFFFFF;
-#pragma unroll
-    for (int t = 0; t < kT; ++t) {
-      if (taken[t]) continue;
-      const double val = (1.0 - smax[t]) * wgt[t];
-      const int i = lane + 64 * t;
-      if (val > bv || (val == bv && i < bi)) {
-        bv = val;
-        bi = i;
-      }
-    }
-    wave_argmax(bv, bi);
-    pick = bi;
+    const double val = (1.0 - smax) * wgt;
+    pick = block_argmax(taken ? -INFINITY : val, taken ? 0x7FFFFFFF : i, sv, si);
   }
   // Ascending output of the picked positions.
+  const bool kp = mine && taken;
+  const uint64_t bal = __ballot(kp);
+  const int lane = i & 63, wave = i >> 6;
+  if (lane == 0) wcount[wave] = __popcll(bal);
+  __syncthreads();
   int64_t pos = fp.out_off;
-#pragma unroll
-  for (int t = 0; t < kT; ++t) {
-    const int i = lane + 64 * t;
-    const bool kp = i < P && taken[t];
-    const uint64_t bal = __ballot(kp);
-    if (kp) kept[pos + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(c.vis_off + (int64_t)fr.f * P + i);
-    pos += __popcll(bal);
-  }
+  for (int w = 0; w < wave; ++w) pos += wcount[w];
+  if (kp) kept[pos + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(c.vis_off + (int64_t)fr.f * P + i);
 }
 
 // ---------------------------------------------------------------------------
@@ -945,13 +957,12 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
                      dp.maxkey, dp.plan, scr, frame_score, frame_budget, segment_id);
   if ((st = launch_status("k_plan")) != APACK_OK) return st;
   if (nf > 0) {
-    const int rpb = std::max(1, std::min(kGramRows, (int)(65536 / ((size_t)dim * sizeof(T)))));
-    const size_t smem = (size_t)rpb * dim * sizeof(T);
-    const unsigned gy = (unsigned)((pl.max_per_frame + rpb - 1) / rpb);
-    hipLaunchKernelGGL(k_gram<T>, dim3(nf, gy), dim3(kBlk), smem, s, dp.clips, dp.frames, dp.plan, dim, rpb, xv,
+    const int nt = (pl.max_per_frame + kGramTile - 1) / kGramTile;
+    const unsigned gy = (unsigned)((nt * (nt + 1) / 2 + kGramWaves - 1) / kGramWaves);
+    hipLaunchKernelGGL(k_gram<T>, dim3(nf, gy), dim3(kGramWaves * 64), 0, s, dp.clips, dp.frames, dp.plan, dim, xv,
                        dp.nv, dp.gram);
     if ((st = launch_status("k_gram")) != APACK_OK) return st;
-    hipLaunchKernelGGL(k_dafps, dim3(nf), dim3(64), 0, s, dp.clips, dp.frames, dp.plan, prm, dp.gram, kept);
+    hipLaunchKernelGGL(k_dafps, dim3(nf), dim3(kMaxPerFrame), 0, s, dp.clips, dp.frames, dp.plan, prm, dp.gram, kept);
     if ((st = launch_status("k_dafps")) != APACK_OK) return st;
     hipLaunchKernelGGL(k_dedup<T>, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dp.plan, dim, xv, dp.nv, kept);
     if ((st = launch_status("k_dedup")) != APACK_OK) return st;

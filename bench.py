@@ -345,6 +345,9 @@ def other_configs(torch, A, W, with_ragged):
     res["cfg3_7b_prune"] = entry(tp, cand, nb, "in-LLM prune + one-layer compaction of the 9454-row sequence")
     log(f"config 3 done ({time.time() - t0:.1f}s)")
 
+    res["paper_schedule_7b"] = paper_schedule(torch, A, W, flush, dev)
+    log(f"paper schedule done ({time.time() - t0:.1f}s)")
+
     if with_ragged:
         rb = W.ragged_batch()
         log(f"ragged batch generated ({time.time() - t0:.1f}s)")
@@ -361,6 +364,62 @@ def other_configs(torch, A, W, with_ragged):
                                            f"{rb.seconds} s, one launch sequence")
         log(f"config 5 done ({time.time() - t0:.1f}s)")
     return res
+
+
+def paper_schedule(torch, A, W, flush, dev):
+    """Eq. 6 as the paper writes it, on the 5-minute 7B clip: from layer 14
+    on, every layer keeps the top ceil(0.9 |S|) of the current candidates,
+    ranked jointly by the last query token, and compacts all 28 layers' K/V,
+    the hidden states and the positions.  Joint ranking ignores modality, so
+    each step's candidates are one span; no host synchronisation between
+    steps."""
+    pc = W.paper_schedule_case()
+    hkv, d, hid = pc.hkv, pc.d, pc.hidden_dim
+    n_layers = len(pc.cache.k_layers)
+    k_in = [dev(x) for x in pc.cache.k_layers]
+    v_in = [dev(x) for x in pc.cache.v_layers]
+    h_in = dev(pc.cache.hidden)
+    p_in = torch.from_numpy(pc.cache.pos).cuda()
+    qs = [dev(x) for x in pc.queries]
+    n_text = pc.n_text
+    steps, n_cand = [], pc.n_audio + pc.n_visual
+    for keep in pc.keeps:
+        seq = W.PruneSeq(0, n_cand + n_text, [(0, n_cand, W.AUDIO)], 0, 1, (keep, 0.0), (0, 0), True)
+        n_kept, wsb = A.apack_prune_layer_query([seq], pc.hq, hkv, d)
+        steps.append(dict(seq=seq, n_in=n_cand + n_text, n_out=n_kept[0], cand=n_cand,
+                          ws=torch.empty(wsb, dtype=torch.uint8, device="cuda"),
+                          scores=torch.empty(n_cand + n_text, dtype=torch.float32, device="cuda"),
+                          kept=torch.empty(n_kept[0], dtype=torch.int32, device="cuda")))
+        n_cand = n_kept[0] - n_text
+    m = steps[0]["n_out"]
+    bufs = [dict(k=[torch.empty((hkv, m, d), dtype=torch.bfloat16, device="cuda") for _ in range(n_layers)],
+                 v=[torch.empty((hkv, m, d), dtype=torch.bfloat16, device="cuda") for _ in range(n_layers)],
+                 h=torch.empty((m, hid), dtype=torch.bfloat16, device="cuda"),
+                 p=torch.empty((3, m), dtype=torch.int32, device="cuda")) for _ in range(2)]
+
+    def run():
+        kk, vv, hh, pp = k_in, v_in, h_in, p_in
+        for i, (layer, st) in enumerate(zip(pc.prune_layers, steps)):
+            A.apack_prune_layer(qs[i], kk[layer], [st["seq"]], scores=st["scores"], kept_rows=st["kept"],
+                                workspace=st["ws"])
+            b, r = bufs[i % 2], st["n_out"]
+            ko = [x[:, :r] for x in b["k"]]
+            vo = [x[:, :r] for x in b["v"]]
+            A.apack_compact_kv(st["kept"], st["n_in"], kk, vv, ko, vo, hh, b["h"][:r], pp, b["p"][:, :r])
+            kk, vv, hh, pp = ko, vo, b["h"][:r], b["p"][:, :r]
+    t = _time_calls(torch, run, flush, reps=10, warmup=3)
+    e = 2
+    row = n_layers * 2 * hkv * d * e + hid * e + 3 * 4
+    cand = sum(st["cand"] for st in steps)
+    nbytes = sum(st["cand"] * hkv * d * e + pc.hq * d * e + 4 * st["n_in"] + 4 * st["n_out"]
+                 + st["n_out"] * (2 * row + 4) for st in steps)
+    return {"what": f"paper schedule: joint top-k, last query only, drop 10% at each of layers "
+                    f"{pc.prune_layers[0]}-{pc.prune_layers[-1]} of a 5-min 7B clip, each step compacting all "
+                    f"{n_layers} layers",
+            "candidates": cand, "algorithmic_bytes": int(nbytes),
+            "ms_cold": round(t["cold"], 3), "ms_warm": round(t["warm"], 3),
+            "candidate_tokens_per_s_cold": round(cand / (t["cold"] / 1e3), 1),
+            "achieved_gbs_cold": round(nbytes / (t["cold"] / 1e3) / 1e9, 1)}
 
 
 def cpu_baseline(case, repeats=3):

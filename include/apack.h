@@ -97,13 +97,18 @@ typedef struct apack_span {
   int32_t reserved;  /* must be 0 */
 } apack_span;
 
+/* apack_seq.flags: rank the audio and visual candidates together (Eq. 6 as
+ * written) instead of per modality.  keep[0] / keep_basis[0] then apply to
+ * the whole candidate set S, and keep[1] / keep_basis[1] must be 0. */
+#define APACK_RANK_JOINT 1
+
 /* One sequence of a (possibly ragged) packed batch at a prune layer. */
 typedef struct apack_seq {
   int64_t tok_off;          /* first row of the sequence in the packed K     */
   int64_t n_tokens;         /* rows of the sequence (N)                      */
   const apack_span* spans;  /* HOST; ascending, disjoint, inside [0, N)      */
   int32_t n_spans;
-  int32_t reserved;         /* must be 0                                     */
+  int32_t flags;            /* 0 (per-modality ranking) or APACK_RANK_JOINT  */
   int64_t q_off;            /* first query row of the sequence in packed Q   */
   int64_t q_len;            /* query rows (>= 1); 1 = the paper's last query */
   double keep[2];           /* keep ratio for [audio, visual], in [0, 1]     */
@@ -120,7 +125,8 @@ apack_status apack_prune_layer_query(int32_t n_seq, const apack_seq* seqs,
 /* Scores the candidate rows S (audio and visual rows) of every sequence by
  * the attention mass of its query rows (Eq. 5), averaged over all hq heads
  * and q_len query rows, and selects per modality the ceil(keep*n) highest
- * (Eq. 6 applied within each modality; ties go to the lower row).
+ * (Eq. 6 applied within each modality), or the ceil(keep[0]*n) highest of S
+ * with APACK_RANK_JOINT (Eq. 6 as written); ties go to the lower row.
  *
  *   q       [hq][q_rows][d] query projections of the query span (post-RoPE,
  *           as the decoder holds them); head h starts at q + h*q_head_stride

@@ -134,16 +134,20 @@ def boundary_gap(scores, rows, k):
     return float((s[k - 1] - s[k]) / s[k - 1])
 
 
-def prune_sequence(q, k, tags, keep, keep_basis=(0, 0)):
+def prune_sequence(q, k, tags, keep, keep_basis=(0, 0), joint=False):
     """One prune step of one sequence.
 
     q: [Hq, T, D] fp64; k: [Hkv, N, D] fp64; tags: [N] int (0 other,
     1 audio, 2 visual); keep: (keep_audio, keep_visual);
     keep_basis: n used in ceil(keep*n) per modality, 0 = current count.
+    joint: rank the audio and visual candidates together, as Eq. 6 is
+    written (S <- TopK of ceil((1-P)|S|) over the whole candidate set), with
+    keep[0] = 1 - P and keep_basis[0] its n; keep[1] and keep_basis[1] are
+    unused.
 
     Returns a dict with ``scores`` [N] fp64 (0 for non-candidates), ``kept``
-    (ascending sequence-local rows), ``k`` (per-modality counts) and
-    ``margin`` (the smallest relative boundary gap over both modalities).
+    (ascending sequence-local rows), ``k`` (per-modality counts, or the joint
+    count under "joint") and ``margin`` (the smallest relative boundary gap).
     """
     tags = np.asarray(tags)
     cand = (tags == AUDIO) | (tags == VISUAL)
@@ -151,6 +155,12 @@ def prune_sequence(q, k, tags, keep, keep_basis=(0, 0)):
     kept = [np.flatnonzero(~cand)]
     ks = {}
     margin = math.inf
+    if joint:
+        rows = np.flatnonzero(cand)
+        kj = keep_count(keep[0], int(keep_basis[0]) or rows.size)
+        kept.append(topk_rows(scores, rows, kj))
+        kept = np.sort(np.concatenate(kept))
+        return {"scores": scores, "kept": kept, "k": {"joint": kj}, "margin": boundary_gap(scores, rows, kj)}
     for m, name in ((AUDIO, "audio"), (VISUAL, "visual")):
         rows = np.flatnonzero(tags == m)
         basis = int(keep_basis[m - 1]) or rows.size
@@ -167,7 +177,7 @@ def prune_batch(q, k, seqs, q_off_key="q_off"):
 
     q: [Hq, sum T, D] fp64; k: [Hkv, sum N, D] fp64.
     seqs: list of dicts with tok_off, n_tokens, q_off, q_len, tags [n_tokens],
-    keep (pair) and optional keep_basis (pair).
+    keep (pair), optional keep_basis (pair) and optional joint (bool).
     Returns (scores [sum N], kept_rows: packed absolute rows, sequences in
     order, ascending within each; n_kept per sequence; margins).
     """
@@ -178,7 +188,7 @@ def prune_batch(q, k, seqs, q_off_key="q_off"):
         o, n = s["tok_off"], s["n_tokens"]
         qo, ql = s[q_off_key], s["q_len"]
         r = prune_sequence(q[:, qo:qo + ql], k[:, o:o + n], s["tags"], s["keep"],
-                           s.get("keep_basis", (0, 0)))
+                           s.get("keep_basis", (0, 0)), s.get("joint", False))
         scores[o:o + n] = r["scores"]
         kept_all.append(r["kept"] + o)
         n_kept.append(r["kept"].size)

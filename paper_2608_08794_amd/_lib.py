@@ -26,10 +26,13 @@ class Span(ctypes.Structure):
                 ("modality", ctypes.c_int32), ("reserved", ctypes.c_int32)]
 
 
+APACK_RANK_JOINT = 1
+
+
 class Seq(ctypes.Structure):
     _fields_ = [("tok_off", ctypes.c_int64), ("n_tokens", ctypes.c_int64),
                 ("spans", ctypes.POINTER(Span)), ("n_spans", ctypes.c_int32),
-                ("reserved", ctypes.c_int32), ("q_off", ctypes.c_int64),
+                ("flags", ctypes.c_int32), ("q_off", ctypes.c_int64),
                 ("q_len", ctypes.c_int64), ("keep", ctypes.c_double * 2),
                 ("keep_basis", ctypes.c_int64 * 2)]
 
@@ -177,7 +180,11 @@ def _seq_array(seqs):
             basis = g("keep_basis")
         except (KeyError, AttributeError):
             basis = (0, 0)
-        arr[i] = Seq(int(g("tok_off")), int(g("n_tokens")), sp, len(spans), 0,
+        try:
+            joint = bool(g("joint"))
+        except (KeyError, AttributeError):
+            joint = False
+        arr[i] = Seq(int(g("tok_off")), int(g("n_tokens")), sp, len(spans), APACK_RANK_JOINT if joint else 0,
                      int(g("q_off")), int(g("q_len")),
                      (ctypes.c_double * 2)(float(keep[0]), float(keep[1])),
                      (ctypes.c_int64 * 2)(int(basis[0]), int(basis[1])))

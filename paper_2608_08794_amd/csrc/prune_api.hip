@@ -31,7 +31,11 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     APACK_CHECK(a.n_tokens < (int64_t(1) << 31), APACK_E_UNSUPPORTED, "seq %d: n_tokens >= 2^31", s);
     APACK_CHECK(a.q_len >= 1 && a.q_len <= 65536 && a.q_off >= 0, APACK_E_SHAPE,
                 "seq %d: q_len must lie in [1, 65536] (got %lld)", s, (long long)a.q_len);
-    APACK_CHECK(a.reserved == 0, APACK_E_ARG, "seq %d: reserved field must be 0", s);
+    APACK_CHECK(a.flags == 0 || a.flags == APACK_RANK_JOINT, APACK_E_ARG, "seq %d: unknown flags %d", s,
+                (int)a.flags);
+    const bool joint = a.flags == APACK_RANK_JOINT;
+    APACK_CHECK(!joint || (a.keep[1] == 0.0 && a.keep_basis[1] == 0), APACK_E_ARG,
+                "seq %d: joint ranking takes keep[0] and keep_basis[0]; keep[1] and keep_basis[1] must be 0", s);
     APACK_CHECK(a.n_spans >= 0 && (a.n_spans == 0 || a.spans), APACK_E_ARG, "seq %d: spans is NULL", s);
     int64_t cnt[2] = {0, 0};
     int64_t prev_end = 0;
@@ -44,7 +48,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
                   "seq %d span %d: spans must be ascending, disjoint and inside [0, %lld)", s, i,
                   (long long)a.n_tokens);
       prev_end = sp.begin + sp.len;
-      if (sp.modality != APACK_OTHER) cnt[sp.modality - 1] += sp.len;
+      if (sp.modality != APACK_OTHER) cnt[joint ? 0 : sp.modality - 1] += sp.len;
     }
     SeqDev& sd = pl.seqs[s];
     std::memset(&sd, 0, sizeof sd);
@@ -236,11 +240,14 @@ apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype
     std::memcpy(h + pl.off_ftiles, pl.ftiles.data(), pl.ftiles.size() * sizeof(FTileDev));
   uint8_t* tags = reinterpret_cast<uint8_t*>(h + pl.off_tags);
   std::memset(tags, 0, pl.total_tok);
+  // Tag = selection slot + 1: the modality, or slot 1 for every candidate of
+  // a jointly ranked sequence.
   for (int s = 0; s < n_seq; ++s)
     for (int i = 0; i < seqs[s].n_spans; ++i) {
       const apack_span& sp = seqs[s].spans[i];
       if (sp.modality != APACK_OTHER)
-        std::memset(tags + pl.seqs[s].tag_off + sp.begin, sp.modality, (size_t)sp.len);
+        std::memset(tags + pl.seqs[s].tag_off + sp.begin, seqs[s].flags == APACK_RANK_JOINT ? 1 : sp.modality,
+                    (size_t)sp.len);
     }
   std::memset(h + pl.off_ctr, 0, pl.total_ctr * sizeof(uint32_t));
   hipStream_t hs = static_cast<hipStream_t>(stream);

@@ -68,9 +68,9 @@ def test_default_params_are_table_s1():
 FAKE = 1 << 40
 
 
-def _seq(spans, n, q_len=4, keep=(0.5, 0.5), basis=(0, 0), tok_off=0, q_off=0, reserved=0):
+def _seq(spans, n, q_len=4, keep=(0.5, 0.5), basis=(0, 0), tok_off=0, q_off=0, flags=0):
     sp = (L.Span * max(1, len(spans)))(*[L.Span(b, l, m, 0) for b, l, m in spans])
-    s = L.Seq(tok_off, n, sp, len(spans), reserved, q_off, q_len,
+    s = L.Seq(tok_off, n, sp, len(spans), flags, q_off, q_len,
               (ctypes.c_double * 2)(*keep), (ctypes.c_int64 * 2)(*basis))
     return s, sp
 
@@ -87,6 +87,15 @@ def _prune(seqs, hq=4, hkv=2, d=64, dtype=0, q=FAKE, k=FAKE + (1 << 34), scores=
     return st, A.library().apack_last_error().decode()
 
 
+def test_prune_query_joint_counts_over_both_modalities():
+    s, _sp = _seq([(0, 100, 1), (100, 300, 2)], 420, keep=(0.55, 0.0), flags=L.APACK_RANK_JOINT)
+    arr = (L.Seq * 1)(s)
+    nk = (ctypes.c_int64 * 1)()
+    ws = ctypes.c_size_t(0)
+    assert A.library().apack_prune_layer_query(1, arr, 8, 2, 128, nk, ctypes.byref(ws)) == 0
+    assert nk[0] == 20 + OP.keep_count(0.55, 400)
+
+
 def test_prune_query_reports_counts_and_workspace():
     s, _sp = _seq([(0, 100, 1), (100, 300, 2)], 420, keep=(0.55, 0.3))
     arr = (L.Seq * 1)(s)
@@ -101,7 +110,8 @@ def test_prune_query_reports_counts_and_workspace():
     ("hq_not_multiple", 2), ("bad_d", 7), ("bad_dtype", 3), ("span_outside", 2), ("span_unsorted", 2),
     ("bad_modality", 1), ("keep_range", 1), ("k_exceeds", 1), ("q_len0", 2), ("q_rows", 2),
     ("k_rows", 2), ("overlap_seqs", 2), ("small_ws", 4), ("misaligned_ws", 4), ("null_ws", 4),
-    ("small_capacity", 2), ("alias", 5), ("reserved", 1), ("misaligned_q", 1), ("null_k", 1),
+    ("small_capacity", 2), ("alias", 5), ("bad_flags", 1), ("misaligned_q", 1), ("null_k", 1),
+    ("joint_second_keep", 1), ("joint_second_basis", 1), ("joint_k_exceeds", 1),
 ])
 def test_prune_validation_errors(case, status):
     s, sp = _seq([(0, 10, 1), (10, 20, 2)], 40)
@@ -141,8 +151,14 @@ def test_prune_validation_errors(case, status):
         kw = dict(cap=5)
     elif case == "alias":
         kw = dict(scores=FAKE + (1 << 34) + 64)
-    elif case == "reserved":
-        seqs = [_seq([(0, 5, 1)], 40, reserved=1)[0]]
+    elif case == "bad_flags":
+        seqs = [_seq([(0, 5, 1)], 40, flags=2)[0]]
+    elif case == "joint_second_keep":
+        seqs = [_seq([(0, 5, 1)], 40, keep=(0.5, 0.5), flags=1)[0]]
+    elif case == "joint_second_basis":
+        seqs = [_seq([(0, 5, 1)], 40, keep=(0.5, 0.0), basis=(0, 3), flags=1)[0]]
+    elif case == "joint_k_exceeds":
+        seqs = [_seq([(0, 5, 1), (5, 5, 2)], 40, keep=(0.5, 0.0), basis=(30, 0), flags=1)[0]]
     elif case == "misaligned_q":
         kw = dict(q=FAKE + 4)
     elif case == "null_k":

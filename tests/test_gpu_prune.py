@@ -41,7 +41,7 @@ def _run_prune(case, seqs=None):
 def _oracle(case, seqs=None):
     seqs = seqs or case.seqs
     sd = [dict(tok_off=s.tok_off, n_tokens=s.n_tokens, q_off=s.q_off, q_len=s.q_len, tags=s.tags(),
-               keep=s.keep, keep_basis=s.keep_basis) for s in seqs]
+               keep=s.keep, keep_basis=s.keep_basis, joint=s.joint) for s in seqs]
     return OP.prune_batch(widen(case.q, case.dtype), widen(case.k, case.dtype), sd)
 
 
@@ -239,3 +239,70 @@ def test_long_sequence_beyond_register_resident_select():
     specs = [([(0, 20000, A_), (20000, 99000, V_)], 120000, 3, (0.4, 0.25))]
     case = _synthetic("bf16", 2, 1, 64, specs, seed=16)
     _parity(case)
+
+
+# -- Eq. 6 as written: one TopK over S, last query token only ----------------
+
+
+def test_joint_ranking_last_query_7b_layer():
+    _parity(W.prune_joint_layer())
+
+
+def test_joint_and_per_modality_sequences_in_one_batch():
+    # A jointly ranked sequence next to a per-modality one, interleaved spans.
+    specs = [([(0, 60, V_), (60, 40, A_), (100, 90, V_)], 230, 1, (0.85, 0.0)),
+             ([(0, 300, A_), (300, 500, V_)], 900, 3, (0.6, 0.25))]
+    case = _synthetic("bf16", 28, 4, 128, specs, seed=41, lift=False)
+    seqs = list(case.seqs)
+    seqs[0] = W.PruneSeq(seqs[0].tok_off, seqs[0].n_tokens, seqs[0].spans, seqs[0].q_off, seqs[0].q_len,
+                         (0.85, 0.0), (0, 0), True)
+    _parity(case, seqs, min_margin=0)
+
+
+def test_paper_schedule_every_layer_from_l_mid():
+    """Algorithm 1's loop: every layer from the first prune layer on keeps
+    the top ceil((1-P)|S|) jointly; each step compacts every layer's K/V, the
+    hidden states and the positions, and the next step scores the compacted
+    cache."""
+    import paper_2608_08794_amd as A
+    pc = W.paper_schedule_case(n_audio=1500, n_frames=120, n_text=64, n_layers=6, first_layer=2, drop=0.15,
+                               hidden_dim=512)
+    log(f"[schedule] layers {pc.prune_layers}, drop 0.15")
+    n = pc.seq().n_tokens
+    tags_all = pc.seq().tags()
+    kd = [to_dev(x, "bf16") for x in pc.cache.k_layers]
+    vd = [to_dev(x, "bf16") for x in pc.cache.v_layers]
+    hd = to_dev(pc.cache.hidden, "bf16")
+    pd = torch.from_numpy(pc.cache.pos).cuda()
+    rows = np.arange(n)
+    for i, layer in enumerate(pc.prune_layers):
+        tags = tags_all[rows]
+        spans, b = [], 0
+        while b < rows.size:   # maximal runs of one tag in the current order
+            e = b
+            while e < rows.size and tags[e] == tags[b]:
+                e += 1
+            if tags[b] != 0:
+                spans.append((b, e - b, int(tags[b])))
+            b = e
+        seq = W.PruneSeq(0, rows.size, spans, 0, 1, (pc.keeps[i], 0.0), (0, 0), True)
+        q = to_dev(pc.queries[i], "bf16")
+        scores, kept, n_kept = A.apack_prune_layer(q, kd[layer], [seq])
+        r = OP.prune_sequence(widen(pc.queries[i], "bf16"), widen(pc.cache.k_layers[layer], "bf16")[:, rows],
+                              tags, (pc.keeps[i], 0.0), joint=True)
+        assert r["margin"] >= 1e-2
+        np.testing.assert_array_equal(kept.cpu().numpy().astype(np.int64), r["kept"])
+        m = kept.numel()
+        ko = [torch.empty((x.shape[0], m, x.shape[2]), dtype=x.dtype, device="cuda") for x in kd]
+        vo = [torch.empty_like(x) for x in ko]
+        ho = torch.empty((m, hd.shape[1]), dtype=hd.dtype, device="cuda")
+        po = torch.empty((3, m), dtype=torch.int32, device="cuda")
+        A.apack_compact_kv(kept, rows.size, kd, vd, ko, vo, hd, ho, pd, po)
+        torch.cuda.synchronize()
+        rows = rows[r["kept"]]
+        for l in range(len(kd)):
+            np.testing.assert_array_equal(bits(ko[l]), raw_bits(pc.cache.k_layers[l], "bf16")[:, rows])
+        np.testing.assert_array_equal(bits(ho), raw_bits(pc.cache.hidden, "bf16")[rows])
+        np.testing.assert_array_equal(po.cpu().numpy(), pc.cache.pos[:, rows])
+        kd, vd, hd, pd = ko, vo, ho, po
+        log(f"  layer {layer}: {n_kept[0]} rows kept")

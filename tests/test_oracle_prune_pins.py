@@ -196,6 +196,54 @@ def test_kept_list_invariants():
     assert np.array_equal(OP.compact_rows(x, kept, axis=1), x[:, kept])
 
 
+# -- joint ranking (Eq. 6 as written: one TopK over S)
+
+
+def test_joint_ranking_brute_force():
+    rng = np.random.default_rng(17)
+    hq, hkv, t, d = 4, 2, 1, 3
+    tags = np.array([VISUAL, OTHER, AUDIO, AUDIO, VISUAL, OTHER, VISUAL, AUDIO, VISUAL, VISUAL])
+    q, k, tags = _rand_case(rng, hq, hkv, t, d, tags)
+    cands = [j for j in range(len(tags)) if tags[j] != OTHER]
+    mass = {j: 0.0 for j in cands}
+    for h in range(hq):
+        g = h // (hq // hkv)
+        lg = {j: sum(q[h, 0, x] * k[g, j, x] for x in range(d)) / math.sqrt(d) for j in cands}
+        z = sum(math.exp(v) for v in lg.values())
+        for j in cands:
+            mass[j] += math.exp(lg[j]) / z / hq
+    for keep in (0.0, 0.1, 0.5, 0.85, 0.9, 1.0):
+        kk = math.ceil(Fraction(str(keep)) * len(cands))
+        top = sorted(cands, key=lambda j: (-np.float32(mass[j]), j))[:kk]
+        want = sorted([j for j in range(len(tags)) if tags[j] == OTHER] + top)
+        r = OP.prune_sequence(q, k, tags, (keep, 0.0), joint=True)
+        assert r["kept"].tolist() == want, keep
+        assert r["k"] == {"joint": kk}
+
+
+def test_joint_equals_per_modality_with_one_modality():
+    rng = np.random.default_rng(18)
+    tags = np.array([AUDIO] * 9 + [OTHER] * 3)
+    q, k, tags = _rand_case(rng, 4, 2, 2, 5, tags)
+    for keep in (0.2, 0.5, 0.77):
+        a = OP.prune_sequence(q, k, tags, (keep, 0.3))
+        b = OP.prune_sequence(q, k, tags, (keep, 0.0), joint=True)
+        assert a["kept"].tolist() == b["kept"].tolist()
+
+
+def test_joint_schedule_counts_follow_the_drop_ratio():
+    # Repeated Eq. 6 with drop P keeps ceil((1-P)|S|) of the current set.
+    n = 1000
+    for p_drop in ("0.10", "0.15"):
+        keep = 1 - float(p_drop)
+        cur = n
+        for _ in range(14):
+            nxt = OP.keep_count(keep, cur)
+            assert nxt == math.ceil((1 - Fraction(p_drop)) * cur)
+            cur = nxt
+    assert OP.keep_count(0.9, 94028 - 128) == 84510
+
+
 def test_keep_basis_counts_against_original_length():
     q = np.ones((1, 1, 2))
     k = np.zeros((1, 10, 2))

@@ -77,8 +77,9 @@ class PruneSeq:
     spans: List[tuple]          # (begin, len, modality), sequence-local rows
     q_off: int
     q_len: int
-    keep: tuple                 # (audio, visual)
+    keep: tuple                 # (audio, visual); (joint, 0) with joint ranking
     keep_basis: tuple = (0, 0)  # n in ceil(keep * n); 0 = current count
+    joint: bool = False         # rank audio and visual together
 
     def tags(self):
         t = np.zeros(self.n_tokens, dtype=np.int8)
@@ -135,8 +136,10 @@ def _lift(kv, dirs, rows, amount):
 
 
 def _ceil_keep(keep, n):
-    # Generator-side count, used only to size the planted sets.
-    return int(math.ceil(float(keep) * float(n)))
+    # Generator-side count, used only to size the planted sets: the ceiling
+    # of keep * n for the decimal ratio written as `keep`.
+    from fractions import Fraction
+    return int(math.ceil(Fraction(repr(float(keep))) * n))
 
 
 def _single_seq(n_audio, n_visual, n_text, q_len, keep, basis=(0, 0)):
@@ -224,6 +227,27 @@ def prune_cfg3(seed=2):
     seq = _single_seq(1500, 7890, 64, 64, (0.5, 0.3))
     q, k, top = _bf16_step(rng, hq, hkv, d, seq, high_frac=0.05)
     return PruneCase("cfg3", "bf16", hq, hkv, d, q, k, [seq], {0: top})
+
+
+def prune_joint_layer(seed=5, keep=0.85):
+    """Eq. 6 as the paper writes it: the last query token only (q_len = 1)
+    and one TopK over all audio and visual candidates.  7B shape after the
+    pre-LLM stage (1500 audio + 7890 visual + 64 text); the planted top set
+    of size ceil(keep * |S|) is drawn from both modalities together."""
+    rng = np.random.default_rng(seed)
+    hq, hkv, d = 28, 4, 128
+    n_a, n_v, n_t = 1500, 7890, 64
+    spans = [(0, n_a, AUDIO), (n_a, n_v, VISUAL)]
+    seq = PruneSeq(0, n_a + n_v + n_t, spans, 0, 1, (keep, 0.0), (0, 0), True)
+    scale = np.float32(1.0 / math.sqrt(d))
+    qf = rng.standard_normal((hq, 1, d), dtype=np.float32) * scale
+    q = to_bf16_bits(qf)
+    kf = rng.standard_normal((hkv, seq.n_tokens, d), dtype=np.float32) * scale
+    dirs = _group_unit_dirs(bf16_bits_to_f32(q), hkv)
+    cand = np.flatnonzero(seq.tags() != OTHER)
+    top = np.sort(rng.choice(cand, size=_ceil_keep(keep, cand.size), replace=False))
+    _lift(kf, dirs, top, LIFT_BF16_BOUNDARY)
+    return PruneCase("joint", "bf16", hq, hkv, d, q, to_bf16_bits(kf), [seq], {0: {"joint": top}})
 
 
 def cache_payload(rng, dtype, n_layers, hkv, d, n, hidden_dim, with_pos=True):
@@ -323,6 +347,41 @@ def progressive_case(seed=3, n_audio=7500, n_frames=600, n_text=128, q_len=128,
         prev = top
     return ProgressiveCase("bf16", hq, hkv, d, hidden_dim, n_audio, n_visual, n_text,
                            q_len, tuple(prune_layers), tuple(keeps), queries, cache, planted)
+
+
+def paper_schedule_case(seed=6, n_audio=7500, n_frames=600, n_text=128, n_layers=CFG4_LAYERS,
+                        first_layer=14, drop=0.10, hq=28, hkv=4, d=128, hidden_dim=3584, payload=True):
+    """The paper's inner-LLM schedule (Algorithm 1; Section 3.2; Section 4.1
+    implementation details): from `first_layer` on, every layer keeps the
+    top ceil((1 - drop) |S|) of the current candidates, ranked jointly by the
+    last query token's attention.  The planted sets are nested over all
+    candidates, each lifted only at its own layer."""
+    rng = np.random.default_rng(seed)
+    n_visual = n_frames * TOKENS_PER_FRAME
+    n = n_audio + n_visual + n_text
+    seq = _single_seq(n_audio, n_visual, n_text, 1, (0, 0))
+    tags = seq.tags()
+    scale = np.float32(1.0 / math.sqrt(d))
+    if payload:
+        cache = cache_payload(rng, "bf16", n_layers, hkv, d, n, hidden_dim)
+    else:
+        cache = CacheCase("bf16", hkv, d, hidden_dim, [None] * n_layers, [None] * n_layers, None, None)
+    layers = tuple(range(first_layer, n_layers))
+    keep = 1.0 - drop
+    prev = np.flatnonzero(tags != OTHER)
+    queries, planted = [], []
+    for layer in layers:
+        qb = to_bf16_bits(rng.standard_normal((hq, 1, d), dtype=np.float32) * scale)
+        dirs = _group_unit_dirs(bf16_bits_to_f32(qb), hkv)
+        kf = rng.standard_normal((hkv, n, d), dtype=np.float32) * scale
+        top = np.sort(rng.choice(prev, size=_ceil_keep(keep, prev.size), replace=False))
+        _lift(kf, dirs, top, LIFT_BF16_BOUNDARY)
+        cache.k_layers[layer] = to_bf16_bits(kf)
+        queries.append(qb)
+        planted.append({"joint": top})
+        prev = top
+    return ProgressiveCase("bf16", hq, hkv, d, hidden_dim, n_audio, n_visual, n_text, 1, layers,
+                           tuple([keep] * len(layers)), queries, cache, planted)
 
 
 # --------------------------------------------------------------------------

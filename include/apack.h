@@ -11,6 +11,8 @@
  *   apack_compact_kv      gather of the kept rows of the K/V cache, hidden
  *                         states and position ids (Section 3.2, last
  *                         sentence; Algorithm 1, "slice their KV-cache entries")
+ *   apack_compact_kv_inplace  the same slicing done in place, for callers
+ *                         that cannot hold the cache twice
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -178,6 +180,38 @@ apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows, int64_t n_
                               const int32_t* pos_in, int32_t* pos_out, int32_t pos_rows,
                               int64_t pos_stride_in, int64_t pos_stride_out,
                               void* stream);
+
+/* Workspace bytes apack_compact_kv_inplace needs for n_out kept rows
+ * (0 for a negative n_out).  About 64 bytes per 64 kept rows. */
+size_t apack_compact_kv_inplace_workspace(int64_t n_out);
+
+/* In-place form of apack_compact_kv (Section 3.2, last sentence; Algorithm 1,
+ * "slice their KV-cache entries"): x[i] = x[src_rows[i]] for i < n_out in
+ * every plane, on raw bits, without a second copy of the cache.
+ *   - k[l] (and v[l]): [hkv][rows][d] tensors, head stride head_stride
+ *     elements; k and v are HOST arrays of n_layers device pointers, v may
+ *     be NULL (only the K planes move);
+ *   - hidden: [rows][hidden_dim] (nullable; hidden_dim 0 when absent);
+ *   - pos: [pos_rows][rows] int32 with row stride pos_stride (nullable;
+ *     pos_rows <= 16).
+ * src_rows is a DEVICE int32 array of n_out <= n_in indices that must be
+ * strictly increasing and lie in [0, n_in), as apack_prune_layer's
+ * kept_rows are; then rows [0, n_out) of every plane end up exactly as
+ * apack_compact_kv would write them and rows [n_out, n_in) keep their old
+ * contents.  For any other src_rows the call still ends and stays inside
+ * the planes, but the contents of rows [0, n_out) are unspecified.
+ * Planes may not overlap each other, src_rows or the workspace
+ * (APACK_E_ALIAS).  The workspace (DEVICE, 256-byte aligned, size from
+ * apack_compact_kv_inplace_workspace) holds per-call counters: calls that
+ * share a workspace must not run concurrently.
+ */
+apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* src_rows, int64_t n_in,
+                                      int32_t n_layers, void* const* k, void* const* v,
+                                      int32_t hkv, int32_t d, apack_dtype dtype,
+                                      int64_t head_stride,
+                                      void* hidden, int32_t hidden_dim,
+                                      int32_t* pos, int32_t pos_rows, int64_t pos_stride,
+                                      void* workspace, size_t workspace_bytes, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Pre-LLM local audio-visual dynamics scorer (Section 3.1)                 */

@@ -17,6 +17,8 @@ from ._lib import (  # noqa: F401
     ApackError,
     DynParams,
     apack_compact_kv,
+    apack_compact_kv_inplace,
+    apack_compact_kv_inplace_workspace,
     apack_dyn_params_default,
     apack_keep_count,
     apack_prune_layer,

@@ -70,6 +70,10 @@ _SIGS = {
     "apack_compact_kv": (ctypes.c_int, [_I64, _P, _I64, _I32, ctypes.POINTER(_P), ctypes.POINTER(_P),
                                         ctypes.POINTER(_P), ctypes.POINTER(_P), _I32, _I32, ctypes.c_int,
                                         _I64, _I64, _P, _P, _I32, _P, _P, _I32, _I64, _I64, _P]),
+    "apack_compact_kv_inplace_workspace": (_SZ, [_I64]),
+    "apack_compact_kv_inplace": (ctypes.c_int, [_I64, _P, _I64, _I32, ctypes.POINTER(_P), ctypes.POINTER(_P),
+                                                _I32, _I32, ctypes.c_int, _I64, _P, _I32, _P, _I32, _I64,
+                                                _P, _SZ, _P]),
     "apack_score_dynamics_query": (ctypes.c_int, [_I32, ctypes.POINTER(AVSeq), _I32,
                                                   ctypes.POINTER(DynParams), ctypes.POINTER(_I64),
                                                   ctypes.POINTER(_SZ)]),
@@ -276,6 +280,51 @@ def apack_compact_kv(src_rows, n_in, k_in=(), v_in=(), k_out=(), v_out=(), hidde
         None if k_only else tabs[3],
         hkv, d, code, hs_in, hs_out, _ptr(hidden_in), _ptr(hidden_out), hid,
         _ptr(pos_in), _ptr(pos_out), prow, ps_in, ps_out, _stream(stream)))
+
+
+def apack_compact_kv_inplace_workspace(n_out):
+    return int(library().apack_compact_kv_inplace_workspace(int(n_out)))
+
+
+def apack_compact_kv_inplace(src_rows, n_in, k=(), v=(), hidden=None, pos=None, workspace=None, stream=None):
+    """x[i] = x[src_rows[i]] in place for every K/V layer tensor [Hkv, rows, D]
+    (v may be empty: K planes only), the hidden states [rows, H] and the
+    position ids [P, rows]; src_rows must be strictly increasing.  Rows
+    [0, n_out) hold the result, later rows keep their contents."""
+    n_out = int(src_rows.numel())
+    n_layers = len(k)
+    if len(v) not in (0, n_layers):
+        raise ApackError(1, "v needs one tensor per layer of k, or none")
+    tk = (ctypes.c_void_p * max(1, n_layers))()
+    tv = (ctypes.c_void_p * max(1, n_layers))() if len(v) else None
+    hkv = d = hs = 0
+    code = APACK_BF16
+    for l in range(n_layers):
+        tk[l] = k[l].data_ptr()
+        hkv, _, d = k[l].shape
+        hs = _heads_rows(k[l], "k")
+        if tv is not None:
+            tv[l] = v[l].data_ptr()
+            if _heads_rows(v[l], "v") != hs or tuple(v[l].shape) != tuple(k[l].shape):
+                raise ApackError(2, "v tensors must match the k tensors' shape and head stride")
+        code = _dtype_code(k[l])
+    hid = 0
+    if hidden is not None:
+        hid = hidden.shape[1]
+        code = _dtype_code(hidden) if n_layers == 0 else code
+        if hidden.stride(1) != 1 or hidden.stride(0) != hid:
+            raise ApackError(2, "hidden states must be contiguous [rows, H]")
+    prow = ps = 0
+    if pos is not None:
+        prow, ps = pos.shape[0], pos.stride(0)
+        if pos.stride(1) != 1:
+            raise ApackError(2, "position ids must have unit column stride")
+    need = apack_compact_kv_inplace_workspace(n_out)
+    if workspace is None:
+        workspace = _workspace(need, src_rows.device)
+    _check(library().apack_compact_kv_inplace(
+        n_out, _ptr(src_rows), int(n_in), n_layers, tk, tv, hkv, d, code, hs,
+        _ptr(hidden), hid, _ptr(pos), prow, ps, workspace.data_ptr(), workspace.numel(), _stream(stream)))
 
 
 def apack_dyn_params_default():

@@ -1,0 +1,378 @@
+// In-place stable compaction of the kept rows (Section 3.2: the pruned
+// tokens' key and value entries are removed; Algorithm 1: slice their
+// KV-cache entries), for callers that cannot hold the cache twice.
+//
+// For every plane x (each K/V head plane, the hidden states, each position
+// row):  x[i] = x[src[i]] for i < n_out, with src strictly increasing, so
+// src[i] >= i and a row only ever moves towards the front.  The hazard is a
+// store into row r that lands before an earlier output row j (src[j] = r,
+// j < r) has read row r.
+//
+// Output rows are cut into stripes of kStripe rows.  The readers of the rows
+// of stripe s are output rows j <= r, so they sit in stripes <= s, and since
+// src is increasing they form one run [first_reader[s], first_reader[s+1]).
+// Work items are (stripe, slice of one plane) in stripe-major order and are
+// claimed through a ticket counter in that order, kGroup items at a time.
+// An item loads its source rows into registers, waits until every earlier
+// stripe holding readers of its destination rows has been read completely
+// (per-stripe counters of items read), then stores.  Readers inside the
+// item's own stripe and plane are the item itself: a workgroup barrier
+// separates its loads from its stores.
+//
+// Why it drains: an item counts itself as read before it waits, and it only
+// waits on strictly earlier stripes, whose items hold smaller tickets and so
+// were claimed by running workgroups.  By induction over stripes every
+// counter fills.  This holds for any src; only the row contents need src to
+// be strictly increasing.
+#include <algorithm>
+#include <cstring>
+#include <vector>
+
+#include "common.hpp"
+#include "sync.hpp"
+
+namespace apack {
+namespace {
+
+typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
+
+constexpr int kMaxTensors = 128;           // 64 layers x {K, V}
+constexpr int kThreads = 256;
+constexpr int kPerThread = 4;
+constexpr int kStripe = 64;                // output rows per stripe
+constexpr int kSlice = kThreads * kPerThread / kStripe;  // units per row slice (16)
+constexpr int kGroup = 8;                  // items per ticket
+constexpr int kCounterPad = 16;            // one 64-byte line per stripe counter
+constexpr int kMaxPosRows = kThreads * kPerThread / kStripe;
+constexpr uint32_t kSpinCap = 1u << 22;    // defensive bound on one wait (seconds)
+
+struct InplaceArgs {
+  const int32_t* src;
+  int64_t n_out, n_in;
+  int64_t n_stripes, n_items;
+  int32_t items_per_stripe;
+  // K/V planes: tensor t, head h at planes[t] + h * hs; rows of kv_row_units.
+  int32_t kv_planes, heads, kv_slices;
+  int64_t kv_row_units, hs;
+  // Hidden states [rows][h_row_units units], cut into h_slices slices.
+  void* hid;
+  int32_t h_slices;
+  int64_t h_row_units;
+  // Position ids [p_rows][p_stride] int32 (one item per stripe).
+  int32_t* pos;
+  int32_t p_rows;
+  int64_t p_stride;
+  // Workspace.
+  uint32_t* ticket;
+  uint32_t* err;
+  uint32_t* done;          // [n_stripes][kCounterPad]
+  const int32_t* first_reader;  // [n_stripes + 1]
+  void* planes[kMaxTensors];
+};
+
+__device__ __forceinline__ int64_t floor_div(int64_t a, int64_t b) { return a >= 0 ? a / b : -((-a + b - 1) / b); }
+
+// Zeroes the ticket and the stripe counters and fills first_reader[s], the
+// first output row j with src[j] >= s * kStripe (n_out when there is none).
+__global__ __launch_bounds__(kThreads) void k_inplace_prep(const InplaceArgs a) {
+  const int64_t g = (int64_t)blockIdx.x * kThreads + threadIdx.x;
+  int32_t* fr = const_cast<int32_t*>(a.first_reader);
+  if (g == 0) {
+    *a.ticket = 0u;
+    *a.err = 0u;
+  }
+  if (g < a.n_stripes) a.done[g * kCounterPad] = 0u;
+  if (g >= a.n_out) return;
+  const int64_t prev = g == 0 ? -1 : (int64_t)a.src[g - 1];
+  const int64_t cur = a.src[g];
+  // Stripes s with src[g-1] < s * kStripe <= src[g] take g.
+  const int64_t lo = std::max<int64_t>(floor_div(prev, kStripe) + 1, 0);
+  const int64_t hi = std::min<int64_t>(floor_div(cur, kStripe), a.n_stripes);
+  for (int64_t s = lo; s <= hi; ++s) fr[s] = (int32_t)g;
+  if (g == a.n_out - 1)
+    for (int64_t s = std::max<int64_t>(floor_div(cur, kStripe) + 1, 0); s <= a.n_stripes; ++s) fr[s] = (int32_t)a.n_out;
+}
+
+// Blocks until every stripe in [lo, hi] has all of its items read.
+__device__ void wait_stripes(const InplaceArgs& a, int64_t lo, int64_t hi) {
+  for (int64_t st = lo; st <= hi; ++st) {
+    const uint32_t* c = a.done + st * kCounterPad;
+    uint32_t spins = 0;
+    while (ld_agent(c) < (uint32_t)a.items_per_stripe) {
+      if (++spins > kSpinCap) {
+        __hip_atomic_fetch_or(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        break;
+      }
+      __builtin_amdgcn_s_sleep(2);
+    }
+  }
+}
+
+template <class U>
+__global__ __launch_bounds__(kThreads) void k_compact_inplace(const InplaceArgs a) {
+  __shared__ uint32_t sh_ticket;
+  const int tid = threadIdx.x;
+  int64_t waited = -1;  // stripe whose readers this workgroup has seen complete (thread 0)
+  for (;;) {
+    if (tid == 0) sh_ticket = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    __syncthreads();
+    const int64_t first = (int64_t)sh_ticket * kGroup;
+    if (first >= a.n_items) break;
+    const int64_t end = std::min<int64_t>(first + kGroup, a.n_items);
+    for (int64_t item = first; item < end; ++item) {
+      const int64_t s = item / a.items_per_stripe;
+      const int k = (int)(item % a.items_per_stripe);
+      const int64_t r0 = s * kStripe;
+      const int kv_items = a.kv_planes * a.kv_slices;
+      const bool is_pos = k >= kv_items + a.h_slices;
+      // Geometry of this item's slice (units of U).
+      U* base = nullptr;
+      int64_t stride = 0;
+      int c0 = 0, w = 0;
+      if (k < kv_items) {
+        const int plane = k / a.kv_slices, sl = k % a.kv_slices;
+        base = static_cast<U*>(a.planes[plane / a.heads]) + (plane % a.heads) * a.hs;
+        stride = a.kv_row_units;
+        c0 = sl * kSlice;
+        w = (int)std::min<int64_t>(kSlice, a.kv_row_units - c0);
+      } else if (!is_pos) {
+        base = static_cast<U*>(a.hid);
+        stride = a.h_row_units;
+        c0 = (k - kv_items) * kSlice;
+        w = (int)std::min<int64_t>(kSlice, a.h_row_units - c0);
+      }
+      U v[kPerThread];
+      int32_t pv[kPerThread];
+      int64_t dst[kPerThread];
+#pragma unroll
+      for (int i = 0; i < kPerThread; ++i) {
+        const int u = tid + i * kThreads;
+        dst[i] = -1;
+        if (!is_pos) {
+          const int64_t r = r0 + u / kSlice;
+          const int c = u % kSlice;
+          if (c < w && r < a.n_out) {
+            const int64_t sr = a.src[r];
+            if (sr >= 0 && sr < a.n_in && sr != r) {
+              v[i] = __builtin_nontemporal_load(base + sr * stride + c0 + c);
+              dst[i] = r * stride + c0 + c;
+            }
+          }
+        } else {
+          const int prow = u / kStripe;
+          const int64_t r = r0 + u % kStripe;
+          if (prow < a.p_rows && r < a.n_out) {
+            const int64_t sr = a.src[r];
+            if (sr >= 0 && sr < a.n_in && sr != r) {
+              pv[i] = __builtin_nontemporal_load(a.pos + prow * a.p_stride + sr);
+              dst[i] = prow * a.p_stride + r;
+            }
+          }
+        }
+      }
+      if (tid == 0 && s != waited) {
+        // Readers of rows [r0, r0 + kStripe) outside this stripe.
+        const int64_t lo = std::clamp<int64_t>(a.first_reader[s], 0, a.n_out);
+        const int64_t hi = std::clamp<int64_t>(a.first_reader[s + 1], lo, a.n_out);
+        if (hi > lo) wait_stripes(a, lo / kStripe, std::min<int64_t>((hi - 1) / kStripe, s - 1));
+        waited = s;
+      }
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+      __syncthreads();
+      if (tid == 0 && (item + 1 == end || (item + 1) / a.items_per_stripe != s)) {
+        const int64_t from = std::max<int64_t>(first, s * a.items_per_stripe);
+        __hip_atomic_fetch_add(a.done + s * kCounterPad, (uint32_t)(item - from + 1), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      }
+#pragma unroll
+      for (int i = 0; i < kPerThread; ++i) {
+        if (dst[i] < 0) continue;
+        if (!is_pos)
+          __builtin_nontemporal_store(v[i], base + dst[i]);
+        else
+          __builtin_nontemporal_store(pv[i], a.pos + dst[i]);
+      }
+    }
+  }
+}
+
+struct InplaceLayout {
+  size_t off_ticket, off_done, off_fr, bytes;
+};
+
+InplaceLayout inplace_layout(int64_t n_out) {
+  const int64_t n_stripes = (n_out + kStripe - 1) / kStripe;
+  Carver c(nullptr);
+  InplaceLayout l;
+  l.off_ticket = c.used;
+  c.take<uint32_t>(2);
+  l.off_done = c.used;
+  c.take<uint32_t>((size_t)n_stripes * kCounterPad);
+  l.off_fr = c.used;
+  c.take<int32_t>((size_t)n_stripes + 1);
+  l.bytes = c.used;
+  return l;
+}
+
+int resident_groups() {
+  static int n = 0;
+  if (n == 0) {
+    int dev = 0, cus = 0, per_cu = 0;
+    if (hipGetDevice(&dev) != hipSuccess ||
+        hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess)
+      cus = 256;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, k_compact_inplace<u32x4>, kThreads, 0) != hipSuccess ||
+        per_cu <= 0)
+      per_cu = 4;
+    n = std::max(1, cus * per_cu);
+  }
+  return n;
+}
+
+}  // namespace
+}  // namespace apack
+
+using namespace apack;
+
+extern "C" size_t apack_compact_kv_inplace_workspace(int64_t n_out) {
+  return n_out < 0 ? 0 : inplace_layout(n_out).bytes;
+}
+
+extern "C" apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* src_rows, int64_t n_in,
+                                                 int32_t n_layers, void* const* k, void* const* v, int32_t hkv,
+                                                 int32_t d, apack_dtype dtype, int64_t head_stride, void* hidden,
+                                                 int32_t hidden_dim, int32_t* pos, int32_t pos_rows,
+                                                 int64_t pos_stride, void* workspace, size_t workspace_bytes,
+                                                 void* stream) {
+  clear_error();
+  APACK_CHECK(dtype_ok(dtype), APACK_E_DTYPE, "unknown dtype %d", (int)dtype);
+  APACK_CHECK(n_out >= 0 && n_in >= 0, APACK_E_SHAPE, "negative row count");
+  APACK_CHECK(n_out <= n_in, APACK_E_SHAPE, "n_out (%lld) exceeds n_in (%lld)", (long long)n_out,
+              (long long)n_in);
+  APACK_CHECK(n_in < (int64_t(1) << 31), APACK_E_UNSUPPORTED, "row counts must be < 2^31");
+  APACK_CHECK(n_layers >= 0 && n_layers <= kMaxTensors / 2, APACK_E_ARG, "n_layers must lie in [0, %d]",
+              kMaxTensors / 2);
+  APACK_CHECK(hidden_dim >= 0 && pos_rows >= 0, APACK_E_ARG, "negative hidden_dim or pos_rows");
+  APACK_CHECK(pos_rows <= kMaxPosRows, APACK_E_UNSUPPORTED, "at most %d position rows", kMaxPosRows);
+  APACK_CHECK(n_out == 0 || src_rows, APACK_E_ARG, "src_rows is NULL");
+  const size_t es = dtype_size(dtype);
+  const bool has_v = v != nullptr;
+  if (n_layers > 0) {
+    APACK_CHECK(k != nullptr, APACK_E_ARG, "K pointer table must be non-NULL");
+    APACK_CHECK(hkv > 0 && d > 0, APACK_E_SHAPE, "hkv and d must be positive");
+    APACK_CHECK(head_stride >= n_in * d, APACK_E_SHAPE, "head stride must be >= rows * d");
+  }
+  const bool has_h = hidden_dim > 0;
+  const bool has_p = pos_rows > 0;
+  if (has_h) APACK_CHECK(hidden, APACK_E_ARG, "hidden must be non-NULL");
+  if (has_p) {
+    APACK_CHECK(pos, APACK_E_ARG, "pos must be non-NULL");
+    APACK_CHECK(pos_stride >= n_in, APACK_E_SHAPE, "position row stride must be >= rows");
+  }
+  // Every plane is distinct; src_rows and the workspace touch none of them.
+  std::vector<std::pair<const void*, size_t>> bufs;
+  const size_t kv_bytes = n_layers ? (size_t)((hkv - 1) * head_stride + n_in * d) * es : 0;
+  for (int l = 0; l < n_layers; ++l) {
+    APACK_CHECK(k[l] && (!has_v || v[l]), APACK_E_ARG, "layer %d: NULL K/V pointer", l);
+    bufs.emplace_back(k[l], kv_bytes);
+    if (has_v) bufs.emplace_back(v[l], kv_bytes);
+  }
+  if (has_h) bufs.emplace_back(hidden, (size_t)n_in * hidden_dim * es);
+  if (has_p) bufs.emplace_back(pos, (size_t)((pos_rows - 1) * pos_stride + n_in) * 4);
+  for (size_t i = 0; i < bufs.size(); ++i)
+    for (size_t j = i + 1; j < bufs.size(); ++j)
+      APACK_CHECK(!overlaps(bufs[i].first, bufs[i].second, bufs[j].first, bufs[j].second), APACK_E_ALIAS,
+                  "two compacted tensors overlap");
+  const InplaceLayout lay = inplace_layout(n_out);
+  if (n_out > 0) {
+    APACK_CHECK(workspace && ((uintptr_t)workspace % kAlign) == 0, APACK_E_WORKSPACE,
+                "workspace must be non-NULL and %zu-byte aligned", kAlign);
+    APACK_CHECK(workspace_bytes >= lay.bytes, APACK_E_WORKSPACE, "workspace of %zu bytes < %zu needed",
+                workspace_bytes, lay.bytes);
+    for (auto& b : bufs) {
+      APACK_CHECK(!overlaps(b.first, b.second, src_rows, (size_t)n_out * 4), APACK_E_ALIAS,
+                  "src_rows overlaps a compacted tensor");
+      APACK_CHECK(!overlaps(b.first, b.second, workspace, lay.bytes), APACK_E_ALIAS,
+                  "the workspace overlaps a compacted tensor");
+    }
+    APACK_CHECK(!overlaps(src_rows, (size_t)n_out * 4, workspace, lay.bytes), APACK_E_ALIAS,
+                "the workspace overlaps src_rows");
+  }
+  if (n_out == 0) return APACK_OK;
+
+  // 16-byte units when every row, stride and base allows it, else 4 bytes.
+  const int64_t kv_row_bytes = (int64_t)d * (int64_t)es;
+  auto al = [](const void* p, uintptr_t b) { return ((uintptr_t)p % b) == 0; };
+  bool wide = true;
+  if (n_layers) {
+    wide &= kv_row_bytes % 16 == 0 && (head_stride * (int64_t)es) % 16 == 0;
+    for (int l = 0; l < n_layers; ++l) wide &= al(k[l], 16) && (!has_v || al(v[l], 16));
+  }
+  if (has_h) wide &= ((int64_t)hidden_dim * (int64_t)es) % 16 == 0 && al(hidden, 16);
+  if (!wide) {
+    APACK_CHECK(kv_row_bytes % 4 == 0 && ((int64_t)hidden_dim * (int64_t)es) % 4 == 0, APACK_E_UNSUPPORTED,
+                "row sizes must be multiples of 4 bytes");
+    for (int l = 0; l < n_layers; ++l)
+      APACK_CHECK(al(k[l], 4) && (!has_v || al(v[l], 4)), APACK_E_ARG, "K/V pointers must be 4-byte aligned");
+    if (has_h) APACK_CHECK(al(hidden, 4), APACK_E_ARG, "hidden must be 4-byte aligned");
+  }
+  if (has_p) APACK_CHECK(al(pos, 4), APACK_E_ARG, "pos must be 4-byte aligned");
+  const int64_t ub = wide ? 16 : 4;
+
+  InplaceArgs a;
+  std::memset(&a, 0, sizeof a);
+  a.src = src_rows;
+  a.n_out = n_out;
+  a.n_in = n_in;
+  a.n_stripes = (n_out + kStripe - 1) / kStripe;
+  a.heads = n_layers ? hkv : 1;
+  if (n_layers) {
+    const int n_tensors = (has_v ? 2 : 1) * n_layers;
+    a.kv_planes = n_tensors * hkv;
+    a.kv_row_units = kv_row_bytes / ub;
+    a.kv_slices = (int32_t)((a.kv_row_units + kSlice - 1) / kSlice);
+    a.hs = head_stride * (int64_t)es / ub;
+    for (int l = 0; l < n_layers; ++l) {
+      if (has_v) {
+        a.planes[2 * l] = k[l];
+        a.planes[2 * l + 1] = v[l];
+      } else {
+        a.planes[l] = k[l];
+      }
+    }
+  }
+  if (has_h) {
+    a.hid = hidden;
+    a.h_row_units = (int64_t)hidden_dim * (int64_t)es / ub;
+    a.h_slices = (int32_t)((a.h_row_units + kSlice - 1) / kSlice);
+  }
+  if (has_p) {
+    a.pos = pos;
+    a.p_rows = pos_rows;
+    a.p_stride = pos_stride;
+  }
+  const int64_t ips = (int64_t)a.kv_planes * a.kv_slices + a.h_slices + (has_p ? 1 : 0);
+  if (ips == 0) return APACK_OK;
+  APACK_CHECK(ips * a.n_stripes < (int64_t(1) << 31) * kGroup, APACK_E_UNSUPPORTED, "too many work items");
+  a.items_per_stripe = (int32_t)ips;
+  a.n_items = ips * a.n_stripes;
+  char* ws = static_cast<char*>(workspace);
+  a.ticket = reinterpret_cast<uint32_t*>(ws + lay.off_ticket);
+  a.err = a.ticket + 1;
+  a.done = reinterpret_cast<uint32_t*>(ws + lay.off_done);
+  a.first_reader = reinterpret_cast<const int32_t*>(ws + lay.off_fr);
+
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  const int64_t prep_threads = std::max<int64_t>(n_out, a.n_stripes + 1);
+  hipLaunchKernelGGL(k_inplace_prep, dim3((unsigned)((prep_threads + kThreads - 1) / kThreads)), dim3(kThreads), 0,
+                     hs, a);
+  apack_status st = launch_status("k_inplace_prep");
+  if (st != APACK_OK) return st;
+  const int64_t tickets = (a.n_items + kGroup - 1) / kGroup;
+  const unsigned grid = (unsigned)std::min<int64_t>(tickets, resident_groups());
+  if (wide)
+    hipLaunchKernelGGL(k_compact_inplace<u32x4>, dim3(grid), dim3(kThreads), 0, hs, a);
+  else
+    hipLaunchKernelGGL(k_compact_inplace<uint32_t>, dim3(grid), dim3(kThreads), 0, hs, a);
+  return launch_status("k_compact_inplace");
+}

@@ -15,35 +15,13 @@
 #include <cstdint>
 
 #include "prune_plan.hpp"
+#include "sync.hpp"
 
 namespace apack {
 
 constexpr int kRadixBins = 2048;
 
 __device__ __forceinline__ uint32_t clamp_bits(float s) { return min(__float_as_uint(s), 0x7F800000u); }
-
-// Loads and stores at agent scope bypass the per-XCD L2 caches, which are
-// not coherent with each other: values passed between workgroups of one
-// launch go through them (see arrive_last).
-__device__ __forceinline__ uint32_t ld_agent(const uint32_t* p) {
-  return __hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ float ld_agent(const float* p) {
-  return __uint_as_float(ld_agent(reinterpret_cast<const uint32_t*>(p)));
-}
-__device__ __forceinline__ float2 ld_agent(const float2* p) {
-  const uint64_t v =
-      __hip_atomic_load(reinterpret_cast<const uint64_t*>(p), __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  return make_float2(__uint_as_float((uint32_t)v), __uint_as_float((uint32_t)(v >> 32)));
-}
-__device__ __forceinline__ void st_agent(float* p, float v) {
-  __hip_atomic_store(reinterpret_cast<uint32_t*>(p), __float_as_uint(v), __ATOMIC_RELAXED,
-                     __HIP_MEMORY_SCOPE_AGENT);
-}
-__device__ __forceinline__ void st_agent(float2* p, float2 v) {
-  const uint64_t b = (uint64_t)__float_as_uint(v.x) | ((uint64_t)__float_as_uint(v.y) << 32);
-  __hip_atomic_store(reinterpret_cast<uint64_t*>(p), b, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
 
 // Inclusive scan over a block of NT threads; sh holds NT/64 words.
 template <int NT>
@@ -136,24 +114,6 @@ __device__ __forceinline__ void merge_hist(const uint32_t* lh, uint32_t* hist) {
     const uint32_t v = lh[b];
     if (v) atomicAdd(&hist[b], v);
   }
-}
-
-// Arrival at a counter of `expected` workgroups; true in the last one to
-// arrive (all threads of the workgroup get the same answer).  Every thread
-// first waits until its own vector memory operations have completed, so the
-// results the workgroup wrote with agent-scope stores or device atomics are
-// visible before its arrival counts; the last workgroup reads them with
-// agent-scope loads.  A full device fence here would also write back the
-// XCD's L2, which costs far more on this chip.
-template <int NT>
-__device__ __forceinline__ bool arrive_last(uint32_t* counter, uint32_t expected) {
-  __shared__ bool last;
-  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-  __syncthreads();
-  if (threadIdx.x == 0)
-    last = __hip_atomic_fetch_add(counter, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) == expected - 1;
-  __syncthreads();
-  return last;
 }
 
 }  // namespace apack

@@ -231,6 +231,80 @@ def test_compact_with_nothing_to_copy_is_ok_without_device():
     assert st == 0, msg
 
 
+def _inplace(n_out=10, n_in=20, layers=1, src=FAKE, k=None, v=True, hid=(0, 0), pos=(0, 0, 0), hkv=2, d=64,
+             dtype=0, hs=None, ws=FAKE + (40 << 34), ws_bytes=None):
+    P = ctypes.c_void_p * max(1, layers)
+    base = FAKE + (1 << 34)
+    k = k or [base + l * (1 << 30) for l in range(layers)]
+    vt = P(*[base + (1 << 33) + l * (1 << 30) for l in range(layers)]) if v else None
+    hs = n_in * d if hs is None else hs
+    need = A.apack_compact_kv_inplace_workspace(n_out)
+    st = A.library().apack_compact_kv_inplace(n_out, src, n_in, layers, P(*k), vt, hkv, d, dtype, hs, hid[0],
+                                              hid[1], pos[0], pos[1], pos[2], ws,
+                                              need if ws_bytes is None else ws_bytes, None)
+    return st, A.library().apack_last_error().decode()
+
+
+def test_inplace_workspace_size_grows_with_stripes():
+    f = A.apack_compact_kv_inplace_workspace
+    assert f(-1) == 0
+    assert 0 < f(0) <= f(1) == f(64) <= f(65) < f(10**6)
+    assert f(10**6) % 256 == 0
+    # A 64-byte counter line and a 4-byte reader index per 64 kept rows.
+    stripes = -(-10**6 // 64)
+    assert stripes * 68 <= f(10**6) <= stripes * 68 + 1024
+
+
+@pytest.mark.parametrize("case,status", [
+    ("more_out_than_in", 2), ("negative", 2), ("null_src", 1), ("bad_dtype", 3), ("stride", 2),
+    ("too_many_pos_rows", 7), ("planes_overlap", 5), ("hidden_overlaps_kv", 5), ("src_in_plane", 5),
+    ("ws_in_plane", 5), ("ws_over_src", 5), ("small_ws", 4), ("misaligned_ws", 4), ("null_ws", 4),
+    ("null_pos", 1), ("too_many_layers", 1),
+])
+def test_inplace_validation_errors(case, status):
+    kw = {}
+    if case == "more_out_than_in":
+        kw = dict(n_out=21)
+    elif case == "negative":
+        kw = dict(n_in=-1)
+    elif case == "null_src":
+        kw = dict(src=None)
+    elif case == "bad_dtype":
+        kw = dict(dtype=9)
+    elif case == "stride":
+        kw = dict(hs=64)
+    elif case == "too_many_pos_rows":
+        kw = dict(pos=(FAKE + (30 << 34), 17, 20))
+    elif case == "planes_overlap":
+        kw = dict(layers=2, k=[FAKE + (1 << 34), FAKE + (1 << 34) + 1024])
+    elif case == "hidden_overlaps_kv":
+        kw = dict(hid=(FAKE + (1 << 34) + 4096, 512))
+    elif case == "src_in_plane":
+        kw = dict(src=FAKE + (1 << 34) + 64)
+    elif case == "ws_in_plane":
+        kw = dict(ws=FAKE + (1 << 34) + 1024)
+    elif case == "ws_over_src":
+        kw = dict(src=FAKE + (40 << 34) + 256)
+    elif case == "small_ws":
+        kw = dict(ws_bytes=16)
+    elif case == "misaligned_ws":
+        kw = dict(ws=FAKE + (40 << 34) + 4)
+    elif case == "null_ws":
+        kw = dict(ws=None)
+    elif case == "null_pos":
+        kw = dict(pos=(None, 3, 20))
+    elif case == "too_many_layers":
+        kw = dict(layers=65)
+    st, msg = _inplace(**kw)
+    assert st == status, msg
+    assert msg
+
+
+def test_inplace_with_nothing_to_move_is_ok_without_device():
+    assert _inplace(n_out=0, ws=None)[0] == 0
+    assert _inplace(n_out=0, layers=0, v=False, ws=None)[0] == 0
+
+
 # -- scorer validation (fake device addresses, never dereferenced) ----------
 
 def _av(n_frames=8, per_frame=16, n_audio=100, n_query=4, vis_off=0, aud_off=0, qry_off=0):

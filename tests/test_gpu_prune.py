@@ -7,6 +7,7 @@ top-k boundary; each case first certifies that gap with the oracle.
 """
 
 import math
+import zlib
 
 import numpy as np
 import pytest
@@ -124,6 +125,95 @@ def test_compact_k_only_planes():
     torch.cuda.synchronize()
     np.testing.assert_array_equal(bits(outs[0]), raw_bits(cache.k_layers[0], "bf16")[:, kept])
     np.testing.assert_array_equal(bits(outs[1]), raw_bits(cache.v_layers[0], "bf16")[:, kept])
+
+
+def _src_rows(kind, n_in, rng):
+    """Strictly increasing kept rows of several shapes."""
+    if kind == "all":
+        return np.arange(n_in)
+    if kind == "none":
+        return np.zeros(0, np.int64)
+    if kind == "one_last":
+        return np.array([n_in - 1])
+    if kind == "prefix_then_sparse":   # an untouched prefix, then rows far behind their readers
+        p = n_in // 3
+        return np.concatenate([np.arange(p), np.sort(rng.choice(np.arange(p, n_in), (n_in - p) // 4, replace=False))])
+    if kind == "drop_first":
+        return np.arange(1, n_in)
+    return np.sort(rng.choice(n_in, max(1, int(n_in * float(kind))), replace=False))
+
+
+@pytest.mark.parametrize("dtype,d,hid,prows,layers,n_in,kind,strided,k_only", [
+    ("bf16", 128, 512, 3, 2, 1000, "0.5", False, False),
+    ("bf16", 128, 3584, 3, 1, 5000, "prefix_then_sparse", False, False),
+    ("bf16", 128, 256, 3, 1, 777, "all", False, False),
+    ("bf16", 128, 256, 3, 1, 64, "drop_first", False, False),
+    ("bf16", 128, 256, 3, 1, 65, "one_last", False, False),
+    ("bf16", 128, 256, 3, 1, 1, "all", False, False),
+    ("bf16", 128, 256, 3, 1, 300, "none", False, False),
+    ("bf16", 256, 0, 0, 2, 2000, "0.3", True, False),      # two slices per row, strided heads
+    ("bf16", 8, 24, 16, 1, 3000, "0.9", False, False),     # one-unit rows, 16 position rows
+    ("f32", 3, 5, 1, 1, 1500, "0.7", False, False),        # 4-byte units
+    ("f32", 64, 100, 2, 3, 2500, "0.1", True, True),       # K planes only
+])
+def test_inplace_compaction_matches_gather(dtype, d, hid, prows, layers, n_in, kind, strided, k_only):
+    """Rows [0, n_out) equal the oracle's gather of the original rows, rows
+    [n_out, n_in) keep their contents, bit for bit; the second call reuses
+    the workspace on the compacted cache."""
+    import paper_2608_08794_amd as A
+    rng = np.random.default_rng(zlib.crc32(repr((dtype, d, n_in, kind)).encode()))
+    hkv = 3
+    pad = 17 if strided else 0
+    cpu = dict(k=[W.payload_bits(rng, (hkv, n_in + pad, d), dtype) for _ in range(layers)],
+               v=[] if k_only else [W.payload_bits(rng, (hkv, n_in + pad, d), dtype) for _ in range(layers)],
+               h=W.payload_bits(rng, (n_in, hid), dtype) if hid else None,
+               p=rng.integers(-2**31, 2**31, size=(prows, n_in + pad), dtype=np.int64).astype(np.int32)
+               if prows else None)
+    dev = dict(k=[to_dev(x, dtype)[:, :n_in] for x in cpu["k"]], v=[to_dev(x, dtype)[:, :n_in] for x in cpu["v"]],
+               h=to_dev(cpu["h"], dtype) if hid else None,
+               p=torch.from_numpy(cpu["p"]).cuda()[:, :n_in] if prows else None)
+    want = {key: ([x[..., :n_in, :] for x in val] if key in "kv" else val) for key, val in cpu.items()}
+    if prows:
+        want["p"] = cpu["p"][:, :n_in]
+    ws = None
+    n = n_in
+    for step in range(2):
+        src = _src_rows(kind if step == 0 else "0.6", n, rng) if n else np.zeros(0, np.int64)
+        log(f"[inplace] {dtype} d={d} hid={hid} pos={prows} layers={layers} step {step}: {n} -> {src.size} ({kind})")
+        if ws is None:
+            ws = torch.empty(max(256, A.apack_compact_kv_inplace_workspace(src.size)), dtype=torch.uint8,
+                             device="cuda")
+        A.apack_compact_kv_inplace(torch.from_numpy(src.astype(np.int32)).cuda(), n,
+                                   [x[:, :n] for x in dev["k"]], [x[:, :n] for x in dev["v"]],
+                                   dev["h"][:n] if hid else None, dev["p"][:, :n] if prows else None, workspace=ws)
+        torch.cuda.synchronize()
+        m = src.size
+
+        def moved(x, axis):
+            y = x.copy()
+            idx = [slice(None)] * x.ndim
+            idx[axis] = slice(0, m)
+            y[tuple(idx)] = OP.compact_rows(x, src, axis=axis)
+            return y
+
+        want = dict(k=[moved(x, 1) for x in want["k"]], v=[moved(x, 1) for x in want["v"]],
+                    h=moved(want["h"], 0) if hid else None, p=moved(want["p"], 1) if prows else None)
+        for l in range(layers):
+            np.testing.assert_array_equal(bits(dev["k"][l]), raw_bits(want["k"][l], dtype))
+            if not k_only:
+                np.testing.assert_array_equal(bits(dev["v"][l]), raw_bits(want["v"][l], dtype))
+        if strided:   # the padding rows past n_in stay untouched
+            for l in range(layers):
+                t = dev["k"][l]
+                tail = t.as_strided((hkv, pad, d), t.stride(), t.storage_offset() + n_in * d)
+                np.testing.assert_array_equal(bits(tail), raw_bits(cpu["k"][l], dtype)[:, n_in:])
+        if hid:
+            np.testing.assert_array_equal(bits(dev["h"]), raw_bits(want["h"], dtype))
+        if prows:
+            np.testing.assert_array_equal(dev["p"].cpu().numpy(), want["p"])
+        n = m
+        if n == 0:
+            break
 
 
 # -- edge cases ---------------------------------------------------------------

@@ -232,6 +232,8 @@ def main():
     }
 
     if not args.no_other_configs:
+        result["in_place_compaction"] = in_place_compaction(torch, A, steps, k_in, v_in, h_in, p_in, row_bytes,
+                                                            g_ms)
         del k_in, v_in, h_in, p_in, queries, steps
         torch.cuda.empty_cache()
         result["other_configs"] = other_configs(torch, A, W, args.ragged)
@@ -260,6 +262,33 @@ def _time_calls(torch, fn, flush, reps=20, warmup=5):
             torch.cuda.synchronize()
             ms.append(a.elapsed_time(b))
         out[mode] = float(np.median(ms))
+    return out
+
+
+def in_place_compaction(torch, A, steps, k_in, v_in, h_in, p_in, row_bytes, gather_ms):
+    """The step's three compactions done in place on one cache with the kept
+    lists of the timed run: per launch, the median time (cold and warm, 10
+    repetitions after 2 warm-ups) against the out-of-place gather.  Repeating
+    a compaction in place shuffles the cache's contents but not the work.
+    Rows whose index does not change (the kept prefix) are not moved, so the
+    algorithmic bytes count only the rows that move."""
+    flush = torch.empty(512 << 20, dtype=torch.uint8, device="cuda")
+    ws = torch.empty(A.apack_compact_kv_inplace_workspace(steps[0]["n_out"]), dtype=torch.uint8, device="cuda")
+    out = []
+    for i, st in enumerate(steps):
+        n = st["n_in"]
+        view = ([x[:, :n] for x in k_in], [x[:, :n] for x in v_in], h_in[:n], p_in[:, :n])
+        kept = st["kept"].cpu().numpy()
+        moved = int(np.count_nonzero(kept != np.arange(kept.size)))
+        nbytes = moved * 2 * row_bytes + 4 * kept.size
+        t = _time_calls(torch, lambda: A.apack_compact_kv_inplace(st["kept"], n, *view, workspace=ws), flush,
+                        reps=10, warmup=2)
+        out.append({"rows_in": n, "rows_out": int(kept.size), "rows_moved": moved, "algorithmic_bytes": nbytes,
+                    "ms_cold": round(t["cold"], 4), "ms_warm": round(t["warm"], 4),
+                    "achieved_gbs_cold": round(nbytes / (t["cold"] / 1e3) / 1e9, 1),
+                    "out_of_place_gather_ms": round(gather_ms[i], 4)})
+    log("in-place compaction: " + ", ".join(f"{o['ms_cold']:.3f} ms ({o['achieved_gbs_cold']:.0f} GB/s)"
+                                            for o in out))
     return out
 
 

@@ -182,7 +182,7 @@ apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows, int64_t n_
                               void* stream);
 
 /* Workspace bytes apack_compact_kv_inplace needs for n_out kept rows
- * (0 for a negative n_out).  About 64 bytes per 64 kept rows. */
+ * (0 for a negative n_out): 68 bytes per 128 kept rows and a few hundred more. */
 size_t apack_compact_kv_inplace_workspace(int64_t n_out);
 
 /* In-place form of apack_compact_kv (Section 3.2, last sentence; Algorithm 1,

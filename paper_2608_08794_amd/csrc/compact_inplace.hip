@@ -13,9 +13,9 @@
 // src is increasing they form one run [first_reader[s], first_reader[s+1]).
 // Work items are (stripe, slice of one plane) in stripe-major order and are
 // claimed through a ticket counter in that order, kGroup items at a time.
-// An item loads its source rows into registers, waits until every earlier
-// stripe holding readers of its destination rows has been read completely
-// (per-stripe counters of items read), then stores.  Readers inside the
+// An item loads its source rows into registers, counts itself as read in its
+// stripe's counter, waits until every earlier stripe holding readers of its
+// destination rows has been read completely, then stores.  Readers inside the
 // item's own stripe and plane are the item itself: a workgroup barrier
 // separates its loads from its stores.
 //
@@ -37,11 +37,11 @@ namespace {
 typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kMaxTensors = 128;           // 64 layers x {K, V}
-constexpr int kThreads = 256;
+constexpr int kThreads = 512;
 constexpr int kPerThread = 4;
-constexpr int kStripe = 64;                // output rows per stripe
-constexpr int kSlice = kThreads * kPerThread / kStripe;  // units per row slice (16)
-constexpr int kGroup = 8;                  // items per ticket
+constexpr int kSlice = 16;                 // units per row slice (256 bytes at 16-byte units)
+constexpr int kStripe = kThreads * kPerThread / kSlice;  // output rows per stripe
+constexpr int kGroup = 2;                  // items per ticket, loaded together
 constexpr int kCounterPad = 16;            // one 64-byte line per stripe counter
 constexpr int kMaxPosRows = kThreads * kPerThread / kStripe;
 constexpr uint32_t kSpinCap = 1u << 22;    // defensive bound on one wait (seconds)
@@ -108,91 +108,182 @@ __device__ void wait_stripes(const InplaceArgs& a, int64_t lo, int64_t hi) {
   }
 }
 
+// Position ids move as 4-byte words inside a unit of either width.
+__device__ __forceinline__ void put_word(uint32_t& u, uint32_t x) { u = x; }
+__device__ __forceinline__ void put_word(u32x4& u, uint32_t x) { u.x = x; }
+__device__ __forceinline__ uint32_t get_word(uint32_t u) { return u; }
+__device__ __forceinline__ uint32_t get_word(const u32x4& u) { return u.x; }
+
+// One item's share of one thread: up to kPerThread units loaded from the
+// source rows, with a bit per unit that has somewhere to go.
+template <class U>
+struct ItemRegs {
+  U v[kPerThread];
+  uint32_t live;
+};
+
+// Geometry of item k of a stripe: base, row stride and slice of a K/V plane
+// or of the hidden states (units of U); positions use their own path.
+template <class U>
+struct Slice {
+  U* base;
+  int64_t stride;
+  int c0, w;
+  bool pos;
+};
+
+template <class U>
+__device__ __forceinline__ Slice<U> slice_of(const InplaceArgs& a, int k) {
+  Slice<U> g{nullptr, 0, 0, 0, false};
+  const int kv_items = a.kv_planes * a.kv_slices;
+  if (k < kv_items) {
+    const int plane = k / a.kv_slices, sl = k % a.kv_slices;
+    g.base = static_cast<U*>(a.planes[plane / a.heads]) + (plane % a.heads) * a.hs;
+    g.stride = a.kv_row_units;
+    g.c0 = sl * kSlice;
+    g.w = (int)std::min<int64_t>(kSlice, a.kv_row_units - g.c0);
+  } else if (k < kv_items + a.h_slices) {
+    g.base = static_cast<U*>(a.hid);
+    g.stride = a.h_row_units;
+    g.c0 = (k - kv_items) * kSlice;
+    g.w = (int)std::min<int64_t>(kSlice, a.h_row_units - g.c0);
+  } else {
+    g.pos = true;
+  }
+  return g;
+}
+
+// Unit i of this thread in an item of stripe s: destination row r and
+// column c (position items: position row c), or false if there is none.
+template <class U>
+__device__ __forceinline__ bool unit_of(const InplaceArgs& a, const Slice<U>& g, int64_t s, int i, int64_t& r,
+                                        int& c) {
+  const int u = threadIdx.x + i * kThreads;
+  if (!g.pos) {
+    r = s * kStripe + u / kSlice;
+    c = u % kSlice;
+    return c < g.w && r < a.n_out;
+  }
+  r = s * kStripe + u % kStripe;
+  c = u / kStripe;
+  return c < a.p_rows && r < a.n_out;
+}
+
+template <class U>
+__device__ __forceinline__ void load_item(const InplaceArgs& a, int64_t item, ItemRegs<U>& q) {
+  const int64_t s = item / a.items_per_stripe;
+  const Slice<U> g = slice_of<U>(a, (int)(item % a.items_per_stripe));
+  q.live = 0;
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    int64_t r;
+    int c;
+    if (!unit_of(a, g, s, i, r, c)) continue;
+    const int64_t sr = a.src[r];
+    if (sr < 0 || sr >= a.n_in || sr == r) continue;   // nothing to move
+    if (!g.pos) {
+      q.v[i] = __builtin_nontemporal_load(g.base + sr * g.stride + g.c0 + c);
+    } else {
+      put_word(q.v[i], __builtin_nontemporal_load(reinterpret_cast<const uint32_t*>(a.pos) + c * a.p_stride + sr));
+    }
+    q.live |= 1u << i;
+  }
+}
+
+template <class U>
+__device__ __forceinline__ void store_item(const InplaceArgs& a, int64_t item, const ItemRegs<U>& q) {
+  const int64_t s = item / a.items_per_stripe;
+  const Slice<U> g = slice_of<U>(a, (int)(item % a.items_per_stripe));
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i) {
+    if (!(q.live >> i & 1u)) continue;
+    int64_t r;
+    int c;
+    unit_of(a, g, s, i, r, c);
+    if (!g.pos)
+      __builtin_nontemporal_store(q.v[i], g.base + r * g.stride + g.c0 + c);
+    else
+      __builtin_nontemporal_store(get_word(q.v[i]), reinterpret_cast<uint32_t*>(a.pos) + c * a.p_stride + r);
+  }
+}
+
+// Stripes in [lo, hi] whose items are not all read yet: true if any.
+__device__ __forceinline__ bool stripes_pending(const InplaceArgs& a, int64_t lo, int64_t hi) {
+  bool pending = false;
+  for (int64_t st = lo; st <= hi; ++st) pending |= ld_agent(a.done + st * kCounterPad) < (uint32_t)a.items_per_stripe;
+  return pending;
+}
+
+// Earlier stripes holding readers of the rows of stripe t, as [lo, hi]
+// (empty when lo > hi), from first_reader[t] and first_reader[t + 1].
+__device__ __forceinline__ void reader_stripes(const InplaceArgs& a, int64_t t, int32_t f0, int32_t f1, int64_t& lo,
+                                               int64_t& hi) {
+  const int64_t j0 = std::clamp<int64_t>(f0, 0, a.n_out);
+  const int64_t j1 = std::clamp<int64_t>(f1, j0, a.n_out);
+  lo = j0 / kStripe;
+  hi = j1 > j0 ? std::min<int64_t>((j1 - 1) / kStripe, t - 1) : -1;
+}
+
+// A workgroup claims kGroup items with one ticket, loads them all, counts
+// them read in their stripes' counters, then waits for the readers of their
+// destination rows, then stores, and only then claims its next ticket.  So
+// a workgroup never waits while it holds a claimed item it has not counted:
+// a count waits on nothing but its own loads, and no chain of waits forms
+// between stripes.  Thread 0 reads the reader ranges before the data loads
+// and looks at the counters once while those loads are in flight; it blocks
+// after counting only if some reader stripe was incomplete then.
 template <class U>
 __global__ __launch_bounds__(kThreads) void k_compact_inplace(const InplaceArgs a) {
   __shared__ uint32_t sh_ticket;
   const int tid = threadIdx.x;
-  int64_t waited = -1;  // stripe whose readers this workgroup has seen complete (thread 0)
+  int64_t waited = -1;  // latest stripe whose readers thread 0 has seen complete
   for (;;) {
     if (tid == 0) sh_ticket = __hip_atomic_fetch_add(a.ticket, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     __syncthreads();
-    const int64_t first = (int64_t)sh_ticket * kGroup;
-    if (first >= a.n_items) break;
-    const int64_t end = std::min<int64_t>(first + kGroup, a.n_items);
-    for (int64_t item = first; item < end; ++item) {
-      const int64_t s = item / a.items_per_stripe;
-      const int k = (int)(item % a.items_per_stripe);
-      const int64_t r0 = s * kStripe;
-      const int kv_items = a.kv_planes * a.kv_slices;
-      const bool is_pos = k >= kv_items + a.h_slices;
-      // Geometry of this item's slice (units of U).
-      U* base = nullptr;
-      int64_t stride = 0;
-      int c0 = 0, w = 0;
-      if (k < kv_items) {
-        const int plane = k / a.kv_slices, sl = k % a.kv_slices;
-        base = static_cast<U*>(a.planes[plane / a.heads]) + (plane % a.heads) * a.hs;
-        stride = a.kv_row_units;
-        c0 = sl * kSlice;
-        w = (int)std::min<int64_t>(kSlice, a.kv_row_units - c0);
-      } else if (!is_pos) {
-        base = static_cast<U*>(a.hid);
-        stride = a.h_row_units;
-        c0 = (k - kv_items) * kSlice;
-        w = (int)std::min<int64_t>(kSlice, a.h_row_units - c0);
-      }
-      U v[kPerThread];
-      int32_t pv[kPerThread];
-      int64_t dst[kPerThread];
+    const int64_t i0 = (int64_t)sh_ticket * kGroup;
+    if (i0 >= a.n_items) break;
+    const int64_t i1 = std::min<int64_t>(i0 + kGroup, a.n_items);
+    const int64_t sb = (i1 - 1) / a.items_per_stripe;
+    // Thread 0: reader ranges of the ticket's stripes not yet seen complete.
+    int32_t fr[kGroup + 1];
+    const int64_t t0 = std::max(waited + 1, i0 / a.items_per_stripe);
+    if (tid == 0)
 #pragma unroll
-      for (int i = 0; i < kPerThread; ++i) {
-        const int u = tid + i * kThreads;
-        dst[i] = -1;
-        if (!is_pos) {
-          const int64_t r = r0 + u / kSlice;
-          const int c = u % kSlice;
-          if (c < w && r < a.n_out) {
-            const int64_t sr = a.src[r];
-            if (sr >= 0 && sr < a.n_in && sr != r) {
-              v[i] = __builtin_nontemporal_load(base + sr * stride + c0 + c);
-              dst[i] = r * stride + c0 + c;
-            }
-          }
-        } else {
-          const int prow = u / kStripe;
-          const int64_t r = r0 + u % kStripe;
-          if (prow < a.p_rows && r < a.n_out) {
-            const int64_t sr = a.src[r];
-            if (sr >= 0 && sr < a.n_in && sr != r) {
-              pv[i] = __builtin_nontemporal_load(a.pos + prow * a.p_stride + sr);
-              dst[i] = prow * a.p_stride + r;
-            }
-          }
-        }
-      }
-      if (tid == 0 && s != waited) {
-        // Readers of rows [r0, r0 + kStripe) outside this stripe.
-        const int64_t lo = std::clamp<int64_t>(a.first_reader[s], 0, a.n_out);
-        const int64_t hi = std::clamp<int64_t>(a.first_reader[s + 1], lo, a.n_out);
-        if (hi > lo) wait_stripes(a, lo / kStripe, std::min<int64_t>((hi - 1) / kStripe, s - 1));
-        waited = s;
-      }
-      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
-      __syncthreads();
-      if (tid == 0 && (item + 1 == end || (item + 1) / a.items_per_stripe != s)) {
-        const int64_t from = std::max<int64_t>(first, s * a.items_per_stripe);
-        __hip_atomic_fetch_add(a.done + s * kCounterPad, (uint32_t)(item - from + 1), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-      }
+      for (int j = 0; j <= kGroup; ++j) fr[j] = t0 + j <= sb + 1 ? a.first_reader[t0 + j] : 0;
+    ItemRegs<U> q[kGroup];
 #pragma unroll
-      for (int i = 0; i < kPerThread; ++i) {
-        if (dst[i] < 0) continue;
-        if (!is_pos)
-          __builtin_nontemporal_store(v[i], base + dst[i]);
-        else
-          __builtin_nontemporal_store(pv[i], a.pos + dst[i]);
-      }
+    for (int p = 0; p < kGroup; ++p) {
+      q[p].live = 0;
+      if (i0 + p < i1) load_item<U>(a, i0 + p, q[p]);
     }
+    bool pending = false;
+    if (tid == 0)
+#pragma unroll
+      for (int j = 0; j < kGroup; ++j)
+        if (t0 + j <= sb) {
+          int64_t lo, hi;
+          reader_stripes(a, t0 + j, fr[j], fr[j + 1], lo, hi);
+          pending |= stripes_pending(a, lo, hi);
+        }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (tid == 0) {
+      for (int64_t i = i0; i < i1; ++i)
+        __hip_atomic_fetch_add(a.done + i / a.items_per_stripe * kCounterPad, 1u, __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+      if (pending)
+        for (int j = 0; j < kGroup; ++j)
+          if (t0 + j <= sb) {
+            int64_t lo, hi;
+            reader_stripes(a, t0 + j, fr[j], fr[j + 1], lo, hi);
+            wait_stripes(a, lo, hi);
+          }
+      waited = std::max(waited, sb);
+    }
+    __syncthreads();
+#pragma unroll
+    for (int p = 0; p < kGroup; ++p)
+      if (q[p].live) store_item<U>(a, i0 + p, q[p]);
   }
 }
 

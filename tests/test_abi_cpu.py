@@ -250,8 +250,8 @@ def test_inplace_workspace_size_grows_with_stripes():
     assert f(-1) == 0
     assert 0 < f(0) <= f(1) == f(64) <= f(65) < f(10**6)
     assert f(10**6) % 256 == 0
-    # A 64-byte counter line and a 4-byte reader index per 64 kept rows.
-    stripes = -(-10**6 // 64)
+    # A 64-byte counter line and a 4-byte reader index per 128 kept rows.
+    stripes = -(-10**6 // 128)
     assert stripes * 68 <= f(10**6) <= stripes * 68 + 1024
 
 

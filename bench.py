@@ -228,6 +228,7 @@ def main():
             "algorithmic_bytes_per_launch": round(sum(gather_bytes) / len(gather_bytes)),
         },
         "per_prune_step_ms": {"score_select": [round(x, 4) for x in p_ms], "compact": [round(x, 4) for x in g_ms]},
+        "prefill_flops": prefill_flops(A, n_layers, n0, case.prune_layers, [st["n_out"] for st in steps]),
         "algorithmic_bytes_per_step": step_bytes,
     }
 
@@ -263,6 +264,17 @@ def _time_calls(torch, fn, flush, reps=20, warmup=5):
             ms.append(a.elapsed_time(b))
         out[mode] = float(np.median(ms))
     return out
+
+
+def prefill_flops(A, n_layers, n0, prune_layers, n_after, d_model=3584, d_ffn=18944):
+    """Analytic prefill FLOPs (Appendix G) of the schedule the run produced:
+    each prune takes effect from the layer after it, at the kept counts the
+    prune calls returned; 7B thinker constants."""
+    lengths = A.apack_schedule_lengths(n_layers, n0, prune_layers, n_after)
+    f_pre, ratio = A.apack_prefill_flops(lengths, n0, d_model, d_ffn)
+    return {"f_pre_tflops": round(f_pre / 1e12, 3),
+            "full_tflops": round(n_layers * A.apack_layer_flops(n0, d_model, d_ffn) / 1e12, 3),
+            "ratio": round(ratio, 4), "final_retention": round(lengths[-1] / n0, 4)}
 
 
 def in_place_compaction(torch, A, steps, k_in, v_in, h_in, p_in, row_bytes, gather_ms):
@@ -448,7 +460,9 @@ def paper_schedule(torch, A, W, flush, dev):
             "candidates": cand, "algorithmic_bytes": int(nbytes),
             "ms_cold": round(t["cold"], 3), "ms_warm": round(t["warm"], 3),
             "candidate_tokens_per_s_cold": round(cand / (t["cold"] / 1e3), 1),
-            "achieved_gbs_cold": round(nbytes / (t["cold"] / 1e3) / 1e9, 1)}
+            "achieved_gbs_cold": round(nbytes / (t["cold"] / 1e3) / 1e9, 1),
+            "prefill_flops": prefill_flops(A, n_layers, pc.seq().n_tokens, list(pc.prune_layers),
+                                           [st["n_out"] for st in steps])}
 
 
 def cpu_baseline(case, repeats=3):
@@ -485,6 +499,7 @@ def cpu_baseline(case, repeats=3):
     dt = min(times)
     threads = max([i.get("num_threads", 1) for i in threadpool_info()] + [1])
     log(f"cpu oracle: {', '.join(f'{t:.1f}' for t in times)} s per step")
+    single = single_thread_configs(OP, widen, W)
     return {
         "value": round(cand / dt, 1),
         "unit": "candidate tokens/s",
@@ -494,7 +509,36 @@ def cpu_baseline(case, repeats=3):
                   f"gather of all 28 layers' K/V, hidden states and positions; best of {repeats} runs "
                   f"({', '.join(f'{t:.1f}' for t in times)} s) with {threads} BLAS threads on "
                   f"{os.cpu_count()} host CPUs",
+        "host_cpus": os.cpu_count(),
+        "blas_threads": threads,
+        "single_thread_configs_1_3": single,
     }
+
+
+def single_thread_configs(OP, widen, W, repeats=3):
+    """The oracle's prune + compaction of configs 1-3 with one BLAS thread,
+    best of `repeats` (inputs widened from their bits inside the timing)."""
+    from threadpoolctl import threadpool_limits
+    out = {}
+    with threadpool_limits(limits=1):
+        for cfg, fn in ((1, W.prune_cfg1), (2, W.prune_cfg2), (3, W.prune_cfg3)):
+            case = fn()
+            cache = W.cfg_cache(cfg, case)
+            sd = [dict(tok_off=s.tok_off, n_tokens=s.n_tokens, q_off=s.q_off, q_len=s.q_len, tags=s.tags(),
+                       keep=s.keep, keep_basis=s.keep_basis) for s in case.seqs]
+            cand = sum(int((s.tags() != 0).sum()) for s in case.seqs)
+            best = float("inf")
+            for _ in range(repeats):
+                t0 = time.perf_counter()
+                _, kept, _, _ = OP.prune_batch(widen(case.q, case.dtype), widen(case.k, case.dtype), sd)
+                for x in cache.k_layers + cache.v_layers:
+                    OP.compact_rows(x, kept, axis=1)
+                OP.compact_rows(cache.hidden, kept, axis=0)
+                OP.compact_rows(cache.pos, kept, axis=1)
+                best = min(best, time.perf_counter() - t0)
+            out[f"cfg{cfg}"] = {"seconds": round(best, 4), "candidate_tokens_per_s": round(cand / best, 1)}
+    log("cpu oracle, one thread: " + ", ".join(f"{k} {v['seconds']:.3f} s" for k, v in out.items()))
+    return out
 
 
 if __name__ == "__main__":

@@ -13,6 +13,8 @@
  *                         sentence; Algorithm 1, "slice their KV-cache entries")
  *   apack_compact_kv_inplace  the same slicing done in place, for callers
  *                         that cannot hold the cache twice
+ *   apack_prefill_flops   analytic prefill FLOPs of a token-length schedule
+ *                         (Appendix G)
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -212,6 +214,34 @@ apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* src_rows, in
                                       void* hidden, int32_t hidden_dim,
                                       int32_t* pos, int32_t pos_rows, int64_t pos_stride,
                                       void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Prefill-FLOPs accounting (Appendix G)                                    */
+/* ------------------------------------------------------------------------ */
+
+/* Prefill cost of one decoder layer at sequence length n: 4 n d^2 for the
+ * Q, K, V and O projections, 2 n^2 d for the attention and 2 n d m for the
+ * feed-forward block, with d = d_model and m = d_ffn (Appendix G, per-layer
+ * equation; Qwen2.5-Omni-7B: d 3584, m 18944, 28 layers; 3B: 2048, 11008,
+ * 36).  Host only; -1 for a negative argument. */
+double apack_layer_flops(int64_t n, int64_t d_model, int64_t d_ffn);
+
+/* F_pre = sum over layers of apack_layer_flops(lengths[i]) and its ratio to
+ * n_layers layers at the full length n0 (Appendix G, prefill and ratio
+ * equations).  lengths is a HOST array of n_layers lengths entering each
+ * layer; f_pre and ratio are HOST outputs (either may be NULL). */
+apack_status apack_prefill_flops(int32_t n_layers, const int64_t* lengths, int64_t n0,
+                                 int64_t d_model, int64_t d_ffn, double* f_pre, double* ratio);
+
+/* The lengths entering each of n_layers layers (numbered from 0) when the
+ * sequence starts at n_start and the prune at layer prune_layers[j] leaves
+ * n_after[j] tokens: a prune scores with its layer's attention and takes
+ * effect from the next layer (Algorithm 1, loop over layers from L_mid).
+ * prune_layers (strictly increasing, in [0, n_layers)), n_after and lengths
+ * are HOST arrays; n_after[j] is usually apack_prune_layer's n_kept. */
+apack_status apack_schedule_lengths(int32_t n_layers, int64_t n_start, int32_t n_prunes,
+                                    const int32_t* prune_layers, const int64_t* n_after,
+                                    int64_t* lengths);
 
 /* ------------------------------------------------------------------------ */
 /* Pre-LLM local audio-visual dynamics scorer (Section 3.1)                 */

@@ -21,8 +21,11 @@ from ._lib import (  # noqa: F401
     apack_compact_kv_inplace_workspace,
     apack_dyn_params_default,
     apack_keep_count,
+    apack_layer_flops,
+    apack_prefill_flops,
     apack_prune_layer,
     apack_prune_layer_query,
+    apack_schedule_lengths,
     apack_score_dynamics,
     apack_score_dynamics_query,
     apack_visual_budget,

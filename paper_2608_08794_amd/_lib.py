@@ -71,6 +71,11 @@ _SIGS = {
                                         ctypes.POINTER(_P), ctypes.POINTER(_P), _I32, _I32, ctypes.c_int,
                                         _I64, _I64, _P, _P, _I32, _P, _P, _I32, _I64, _I64, _P]),
     "apack_compact_kv_inplace_workspace": (_SZ, [_I64]),
+    "apack_layer_flops": (ctypes.c_double, [_I64, _I64, _I64]),
+    "apack_prefill_flops": (ctypes.c_int, [_I32, ctypes.POINTER(_I64), _I64, _I64, _I64,
+                                           ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
+    "apack_schedule_lengths": (ctypes.c_int, [_I32, _I64, _I32, ctypes.POINTER(_I32), ctypes.POINTER(_I64),
+                                              ctypes.POINTER(_I64)]),
     "apack_compact_kv_inplace": (ctypes.c_int, [_I64, _P, _I64, _I32, ctypes.POINTER(_P), ctypes.POINTER(_P),
                                                 _I32, _I32, ctypes.c_int, _I64, _P, _I32, _P, _I32, _I64,
                                                 _P, _SZ, _P]),
@@ -325,6 +330,30 @@ def apack_compact_kv_inplace(src_rows, n_in, k=(), v=(), hidden=None, pos=None, 
     _check(library().apack_compact_kv_inplace(
         n_out, _ptr(src_rows), int(n_in), n_layers, tk, tv, hkv, d, code, hs,
         _ptr(hidden), hid, _ptr(pos), prow, ps, workspace.data_ptr(), workspace.numel(), _stream(stream)))
+
+
+def apack_layer_flops(n, d_model, d_ffn):
+    return float(library().apack_layer_flops(int(n), int(d_model), int(d_ffn)))
+
+
+def apack_prefill_flops(lengths, n0, d_model, d_ffn):
+    """(F_pre, ratio) of a per-layer length schedule."""
+    arr = (_I64 * max(1, len(lengths)))(*[int(x) for x in lengths])
+    f, r = ctypes.c_double(0), ctypes.c_double(0)
+    _check(library().apack_prefill_flops(len(lengths), arr, int(n0), int(d_model), int(d_ffn),
+                                         ctypes.byref(f), ctypes.byref(r)))
+    return f.value, r.value
+
+
+def apack_schedule_lengths(n_layers, n_start, prune_layers, n_after):
+    """Lengths entering each layer; a prune at layer l takes effect from l + 1."""
+    pl = (_I32 * max(1, len(prune_layers)))(*[int(x) for x in prune_layers])
+    na = (_I64 * max(1, len(n_after)))(*[int(x) for x in n_after])
+    out = (_I64 * max(1, int(n_layers)))()
+    if len(prune_layers) != len(n_after):
+        raise ApackError(1, "prune_layers and n_after differ in length")
+    _check(library().apack_schedule_lengths(int(n_layers), int(n_start), len(prune_layers), pl, na, out))
+    return [int(out[i]) for i in range(int(n_layers))]
 
 
 def apack_dyn_params_default():

@@ -365,6 +365,7 @@ def test_paper_schedule_every_layer_from_l_mid():
     hd = to_dev(pc.cache.hidden, "bf16")
     pd = torch.from_numpy(pc.cache.pos).cuda()
     rows = np.arange(n)
+    gpu_kept, oracle_kept = [], []
     for i, layer in enumerate(pc.prune_layers):
         tags = tags_all[rows]
         spans, b = [], 0
@@ -395,4 +396,14 @@ def test_paper_schedule_every_layer_from_l_mid():
         np.testing.assert_array_equal(bits(ho), raw_bits(pc.cache.hidden, "bf16")[rows])
         np.testing.assert_array_equal(po.cpu().numpy(), pc.cache.pos[:, rows])
         kd, vd, hd, pd = ko, vo, ho, po
+        gpu_kept.append(n_kept[0])
+        oracle_kept.append(r["kept"].size)
         log(f"  layer {layer}: {n_kept[0]} rows kept")
+    # Appendix G accounting of the schedule the path produced: the library's
+    # ratio from the GPU's kept counts equals the oracle's from its own.
+    from oracle import flops as OF
+    T, d, m = len(pc.cache.k_layers), 3584, 18944
+    lengths = A.apack_schedule_lengths(T, n, list(pc.prune_layers), gpu_kept)
+    assert lengths == OF.step_schedule(T, n, list(pc.prune_layers), oracle_kept)
+    _, ratio = A.apack_prefill_flops(lengths, n, d, m)
+    assert ratio == pytest.approx(float(OF.flops_ratio(lengths, n, d, m)), rel=1e-13)

@@ -384,6 +384,7 @@ def other_configs(torch, A, W, with_ragged):
                                           "pre-LLM scorer of a 60 s clip (gate fired) + gather of the kept "
                                           "visual embeddings")
     res["cfg3_7b_prune"] = entry(tp, cand, nb, "in-LLM prune + one-layer compaction of the 9454-row sequence")
+    res["cfg3_7b_scorer_alignments"] = alignment_ablation(torch, A, dyn, flush, dev)
     log(f"config 3 done ({time.time() - t0:.1f}s)")
 
     res["paper_schedule_7b"] = paper_schedule(torch, A, W, flush, dev)
@@ -405,6 +406,29 @@ def other_configs(torch, A, W, with_ragged):
                                            f"{rb.seconds} s, one launch sequence")
         log(f"config 5 done ({time.time() - t0:.1f}s)")
     return res
+
+
+def alignment_ablation(torch, A, dyn, flush, dev):
+    """The alternative frame-alignment scorers on the 60 s 7B clip whose
+    window CKA is low (the gate fires): scorer time, and how many kept
+    visual tokens each shares with the paper's gated CKA."""
+    xv, xa, xq = dev(dyn.xv), dev(dyn.xa), dev(dyn.xq)
+    kept, out = {}, {}
+    for name in ("gated_cka", "cka", "av_cosine", "spatial_cka"):
+        params = dict(dyn.params, alignment=name)
+        n_kv, wsb = A.apack_score_dynamics_query(dyn.seqs, dyn.dim, params)
+        ws = torch.empty(wsb, dtype=torch.uint8, device="cuda")
+        t = _time_calls(torch, lambda: A.apack_score_dynamics(xv, xa, xq, dyn.seqs, params, workspace=ws), flush,
+                        reps=10, warmup=2)
+        r = A.apack_score_dynamics(xv, xa, xq, dyn.seqs, params, workspace=ws)
+        torch.cuda.synchronize()
+        kept[name] = set(r["kept"].cpu().numpy().tolist())
+        out[name] = {"ms_cold": round(t["cold"], 4), "gate_fired": bool(r["gate"].cpu().numpy()[0]),
+                     "kept": len(kept[name])}
+    for name in out:
+        out[name]["kept_shared_with_gated_cka"] = round(len(kept[name] & kept["gated_cka"]) / max(1, len(kept[name])),
+                                                        4)
+    return out
 
 
 def paper_schedule(torch, A, W, flush, dev):

@@ -260,7 +260,28 @@ typedef struct apack_dyn_params {
   double cover_thresh;  /* DA-FPS coverage cosine threshold (0.8)             */
   double dafps_power;   /* power on the DA-FPS density (0.5)                  */
   double r_pre;         /* pre-LLM joint retention R_pre (0.50)               */
+  int32_t alignment;    /* frame alignment scorer, APACK_ALIGN_* (gated CKA)  */
 } apack_dyn_params;
+
+/* Frame alignment scorers (the supplement's comparison of alignment-scoring
+ * rules and its window sweep); the rest of the scorer is unchanged.
+ *   GATED_CKA    Eq. 1 over the window and the gate of Eq. 2 (the paper's).
+ *   CKA          Eq. 1 alone: alpha_f = c_f for every clip, never gated.
+ *   AV_COSINE    alpha_f = 1 - d_hat_f for every clip: each visual token's
+ *                strongest cosine to any audio token of the clip, averaged
+ *                over the frame and min-max normalised -- a token-wise match
+ *                that ignores time (the "static" similarity).
+ *   SPATIAL_CKA  the w = 1 variant: within frame f, linear CKA between the
+ *                covariance of its visual tokens and that of the audio
+ *                tokens of its adaptive-pool bin, each set centred by its
+ *                own mean: c_f = ||A~ V~^T||^2 / (||A~ A~^T|| ||V~ V~^T||)
+ *                (0 for a bin of one token); c_f then enters Eq. 2's gate.
+ * frame_cka reports the c_f the mode uses (the window CKA for the first
+ * three). */
+#define APACK_ALIGN_GATED_CKA 0
+#define APACK_ALIGN_CKA 1
+#define APACK_ALIGN_AV_COSINE 2
+#define APACK_ALIGN_SPATIAL_CKA 3
 
 void apack_dyn_params_default(apack_dyn_params* p);
 

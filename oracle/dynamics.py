@@ -37,6 +37,22 @@ step:
 * non-anchor frames keep exactly their budget of least-anchor-similar
   positions; ties go to the lower index everywhere.
 
+Alternative alignment scorers (the supplement's comparison of alignment-
+scoring rules and the window sweep), selected by ``alignment``, with the
+rest of the compressor unchanged:
+
+* ``"gated_cka"`` (default): Eq. 1 and the gate of Eq. 2;
+* ``"cka"``: local-window CKA alone, alpha_f = c_f, never gated;
+* ``"av_cosine"``: alpha_f = 1 - d_hat_f for every clip, the token-wise
+  match of each visual token to its strongest audio token over the whole
+  clip (the "static" similarity that ignores time);
+* ``"spatial_cka"``: the w = 1 variant that compares, within each frame,
+  the covariance of the visual patches with that of the co-timed audio
+  tokens (the frame's adaptive-pool bin):
+  c_f = ||A~ V~^T||_F^2 / (||A~ A~^T||_F ||V~ V~^T||_F), each token set
+  centred by its own mean (so a bin of one audio token gives 0); this c_f
+  then enters the gate of Eq. 2 in place of the window CKA.
+
 Every helper also reports the margins of its discrete decisions so tests can
 certify that the seeded inputs sit away from every decision boundary.
 """
@@ -60,7 +76,11 @@ DEFAULTS = {
     "cover_thresh": 0.8,
     "dafps_power": 0.5,
     "r_pre": 0.50,
+    # Alignment scorer (see the module docstring); the paper's is gated CKA.
+    "alignment": "gated_cka",
 }
+
+ALIGNMENTS = ("gated_cka", "cka", "av_cosine", "spatial_cka")
 
 
 # --------------------------------------------------------------------------
@@ -125,6 +145,26 @@ def frame_cka(a, v, w):
 # --------------------------------------------------------------------------
 # Gated fine pass (Eq. 2)
 # --------------------------------------------------------------------------
+
+def spatial_cka(xv, xa, n_frames, per_frame):
+    """Per-frame spatial CKA at w = 1 (reading above): linear CKA between the
+    feature covariances of the frame's P visual tokens and of the audio
+    tokens of its adaptive-pool bin, each centred by its own mean."""
+    lo_hi = audio_bins(xa.shape[0], n_frames)
+    out = np.zeros(n_frames)
+    for f in range(n_frames):
+        v = xv[f * per_frame:(f + 1) * per_frame]
+        lo, hi = lo_hi[f]
+        a = xa[lo:hi]
+        if a.shape[0] == 0 or v.shape[0] == 0:
+            continue
+        vc = v - v.mean(axis=0)
+        ac = a - a.mean(axis=0)
+        num = float(np.sum((ac @ vc.T) ** 2))
+        den = float(np.linalg.norm(ac @ ac.T)) * float(np.linalg.norm(vc @ vc.T))
+        out[f] = num / den if den != 0.0 else 0.0
+    return out
+
 
 def cosine(x, y):
     nx = math.sqrt(float(x @ x))
@@ -428,15 +468,23 @@ def score_sequence(xv, xa, xq, n_frames, per_frame, params=None):
     a = resample_audio(xa, F)
     qbar = xq.mean(axis=0)
 
-    # Local-window CKA and the gate (Eq. 1, Eq. 2).
-    c = frame_cka(a, v, p["window"])
+    # Local-window CKA and the gate (Eq. 1, Eq. 2), or an alternative scorer.
+    mode = p["alignment"]
+    if mode not in ALIGNMENTS:
+        raise ValueError(f"unknown alignment {mode!r}")
+    c = spatial_cka(xv, xa, F, P) if mode == "spatial_cka" else frame_cka(a, v, p["window"])
     cbar = float(c.mean()) if F else 0.0
-    fired = bool(F > 0 and cbar < p["tau_gate"])
-    margins["gate"] = abs(cbar - p["tau_gate"]) if F else math.inf
+    if mode in ("gated_cka", "spatial_cka"):
+        fired = bool(F > 0 and cbar < p["tau_gate"])
+        margins["gate"] = abs(cbar - p["tau_gate"]) if F else math.inf
+    else:
+        fired = bool(F > 0 and mode == "av_cosine")
+        margins["gate"] = math.inf
+    beta = 1.0 if mode == "av_cosine" else p["beta"]
     if fired:
         d, _ = direct_distance(xv, xa, F, P)
         dhat = minmax(d)
-        alpha = (1.0 - p["beta"]) * c + p["beta"] * (1.0 - dhat)
+        alpha = (1.0 - beta) * c + beta * (1.0 - dhat)
     else:
         d = np.zeros(F)
         dhat = np.zeros(F)

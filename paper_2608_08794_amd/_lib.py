@@ -27,6 +27,7 @@ class Span(ctypes.Structure):
 
 
 APACK_RANK_JOINT = 1
+ALIGNMENTS = {"gated_cka": 0, "cka": 1, "av_cosine": 2, "spatial_cka": 3}
 
 
 class Seq(ctypes.Structure):
@@ -43,7 +44,7 @@ class DynParams(ctypes.Structure):
                 ("gamma", ctypes.c_double), ("tau_sim", ctypes.c_double),
                 ("sigma", ctypes.c_double), ("lambda_seg", ctypes.c_double),
                 ("cover_thresh", ctypes.c_double), ("dafps_power", ctypes.c_double),
-                ("r_pre", ctypes.c_double)]
+                ("r_pre", ctypes.c_double), ("alignment", ctypes.c_int32)]
 
 
 class AVSeq(ctypes.Structure):
@@ -363,8 +364,12 @@ def apack_dyn_params_default():
 
 
 def _params(params):
+    """apack_dyn_params from the defaults and a dict of overrides; the
+    alignment scorer may be given by name (see ALIGNMENTS)."""
     p = apack_dyn_params_default()
     for key, val in (params or {}).items():
+        if key == "alignment" and isinstance(val, str):
+            val = ALIGNMENTS[val]
         setattr(p, key, val)
     return p
 

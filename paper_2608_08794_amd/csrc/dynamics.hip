@@ -207,7 +207,7 @@ __device__ __forceinline__ double band_at(const double* band, int64_t f0, int i,
 // ---------------------------------------------------------------------------
 // Eq. 1 per frame over its clamped window, the clip mean and the gate.
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w, double tau,
+__global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w, double tau, int alignment,
                                               const double* __restrict__ band_v, const double* __restrict__ band_a,
                                               double* __restrict__ cka, float* __restrict__ frame_cka,
                                               uint8_t* __restrict__ gate_out) {
@@ -218,6 +218,12 @@ __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w
   const int ww = F <= w ? F : w;
   double sum = 0.0;
   for (int f = threadIdx.x; f < F; f += kBlk) {
+    if (alignment == APACK_ALIGN_SPATIAL_CKA) {  // c_f already written by k_spatial_reduce
+      const double cf = cka[f0 + f];
+      if (frame_cka) frame_cka[f0 + f] = (float)cf;
+      sum += cf;
+      continue;
+    }
     int lo = 0;
     if (F > w) lo = min(max(f - w / 2, 0), F - w);
     // Centred Grams K = H G H of the window rows lo .. lo+ww-1.
@@ -255,7 +261,11 @@ __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w
   }
   sum = block_sum(sum, sh);
   if (threadIdx.x == 0) {
-    const int fired = (F > 0 && sum / F < tau) ? 1 : 0;
+    // The window (or spatial) CKA gate of Eq. 2; CKA alone never fires it,
+    // AV cosine always does.
+    int fired = (F > 0 && sum / F < tau) ? 1 : 0;
+    if (alignment == APACK_ALIGN_CKA) fired = 0;
+    if (alignment == APACK_ALIGN_AV_COSINE) fired = F > 0 ? 1 : 0;
     c->gate = fired;
     if (gate_out) gate_out[blockIdx.x] = (uint8_t)fired;
   }
@@ -735,6 +745,123 @@ __global__ __launch_bounds__(kGramWaves * 64) void k_gram(const ClipDev* __restr
   }
 }
 
+// ---------------------------------------------------------------------------
+// Spatial CKA at w = 1 (alternative alignment scorer): for frame f, the rows
+// R = [A~; V~] stack the audio tokens of its adaptive-pool bin and its P
+// visual tokens, each centred in fp64 by its own mean (a_f and v_f of
+// k_pool).  One wave per 16 x 16 tile of the upper triangle of R R^T (fp64
+// MFMA, operand layout as in k_gram) adds the squared entries of its tile
+// to the audio-audio, audio-visual and visual-visual sums; off-diagonal
+// tiles of the symmetric blocks count twice, and the cross block counts
+// once, in its audio-row orientation.  The per-tile sums go to
+// part[frame][tile][3] and k_spatial_reduce adds them in tile order.
+// ---------------------------------------------------------------------------
+template <class T>
+__device__ __forceinline__ void load8_centred(const T* x, const double* mu, double (&o)[8]) {
+  load8(x, o);
+#pragma unroll
+  for (int e = 0; e < 8; ++e) o[e] -= mu[e];
+}
+
+template <class T>
+__global__ __launch_bounds__(kGramWaves * 64) void k_spatial_gram(const ClipDev* __restrict__ clips,
+                                                                  const FrameDev* __restrict__ frames, int dim,
+                                                                  const T* __restrict__ xv, const T* __restrict__ xa,
+                                                                  const double* __restrict__ vmean,
+                                                                  const double* __restrict__ amean, int tiles,
+                                                                  double* __restrict__ part) {
+  const FrameDev fr = frames[blockIdx.x];
+  const ClipDev c = clips[fr.clip];
+  const int64_t frame = c.frame_off + fr.f;
+  const int P = c.per_frame;
+  const int64_t lo = ((int64_t)fr.f * c.n_audio) / c.n_frames;
+  const int64_t hi = (((int64_t)fr.f + 1) * c.n_audio + c.n_frames - 1) / c.n_frames;
+  const int na = (int)(hi - lo), m = na + P;
+  const int nt = (m + kGramTile - 1) / kGramTile;
+  const int t0 = blockIdx.y * kGramWaves + (threadIdx.x >> 6);
+  if (t0 >= tiles) return;
+  const int lane = threadIdx.x & 63, g = lane >> 4, r16 = lane & 15;
+  double* out = part + (frame * tiles + t0) * 3;
+  if (t0 >= nt * (nt + 1) / 2) {  // past this frame's triangle: contributes nothing
+    if (lane < 3) out[lane] = 0.0;
+    return;
+  }
+  int t = t0, ti = 0;
+  while (t >= nt - ti) {
+    t -= nt - ti;
+    ++ti;
+  }
+  const int tj = ti + t;
+  // Row r of R: audio row lo + r (centred by a_f) or visual token r - na (by v_f).
+  auto row_ptr = [&](int r, const T*& x, const double*& mu) {
+    r = min(r, m - 1);
+    if (r < na) {
+      x = xa + (c.aud_off + lo + r) * dim;
+      mu = amean + frame * dim;
+    } else {
+      x = xv + (c.vis_off + (int64_t)fr.f * P + (r - na)) * dim;
+      mu = vmean + frame * dim;
+    }
+  };
+  const T *pa, *pb;
+  const double *ma, *mb;
+  row_ptr(ti * kGramTile + r16, pa, ma);
+  row_ptr(tj * kGramTile + r16, pb, mb);
+  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+  for (int k0 = 0; k0 < dim; k0 += 32) {
+    const int kk = k0 + 8 * g;
+    double a[8], b[8];
+    if (kk < dim) {
+      load8_centred(pa + kk, ma + kk, a);
+      load8_centred(pb + kk, mb + kk, b);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) a[e] = b[e] = 0.0;
+    }
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a[e], b[e], acc, 0, 0, 0);
+  }
+  double s_aa = 0.0, s_av = 0.0, s_vv = 0.0;
+  const int col = tj * kGramTile + r16;
+  const double twice = ti == tj ? 1.0 : 2.0;
+#pragma unroll
+  for (int e = 0; e < 4; ++e) {
+    const int row = ti * kGramTile + 4 * e + g;
+    if (row >= m || col >= m) continue;
+    const double x2 = acc[e] * acc[e];
+    if (row < na && col < na)
+      s_aa += twice * x2;
+    else if (row >= na && col >= na)
+      s_vv += twice * x2;
+    else if (row < na)  // audio row, visual column; its transpose is not counted
+      s_av += x2;
+  }
+  s_aa = wave_sum(s_aa);
+  s_av = wave_sum(s_av);
+  s_vv = wave_sum(s_vv);
+  if (lane == 0) {
+    out[0] = s_aa;
+    out[1] = s_av;
+    out[2] = s_vv;
+  }
+}
+
+// c_f = S_av / (sqrt(S_aa) sqrt(S_vv)) from the tile sums, in tile order.
+__global__ __launch_bounds__(kBlk) void k_spatial_reduce(int64_t n_frames, int tiles, const double* __restrict__ part,
+                                                         double* __restrict__ cka) {
+  const int64_t f = (int64_t)blockIdx.x * kBlk + threadIdx.x;
+  if (f >= n_frames) return;
+  double s_aa = 0.0, s_av = 0.0, s_vv = 0.0;
+  for (int t = 0; t < tiles; ++t) {
+    const double* q = part + (f * tiles + t) * 3;
+    s_aa += q[0];
+    s_av += q[1];
+    s_vv += q[2];
+  }
+  const double den = sqrt(s_aa) * sqrt(s_vv);
+  cka[f] = den == 0.0 ? 0.0 : s_av / den;
+}
+
 // Lexicographic (value desc, index asc) argmax across a wave.
 __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
 #pragma unroll
@@ -928,8 +1055,17 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
                        dp.band_v, dp.band_a, dp.vq, dp.qq);
     if ((st = launch_status("k_band")) != APACK_OK) return st;
   }
-  hipLaunchKernelGGL(k_cka, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm.window, prm.tau_gate, dp.band_v, dp.band_a,
-                     dp.cka, frame_cka, gate_fired);
+  if (prm.alignment == APACK_ALIGN_SPATIAL_CKA && nf > 0) {
+    const unsigned gy = (unsigned)((pl.spatial_tiles + kGramWaves - 1) / kGramWaves);
+    hipLaunchKernelGGL(k_spatial_gram<T>, dim3(nf, gy), dim3(kGramWaves * 64), 0, s, dp.clips, dp.frames, dim, xv,
+                       xa, dp.v, dp.a, pl.spatial_tiles, dp.spatial);
+    if ((st = launch_status("k_spatial_gram")) != APACK_OK) return st;
+    hipLaunchKernelGGL(k_spatial_reduce, dim3((unsigned)((nf + kBlk - 1) / kBlk)), dim3(kBlk), 0, s, (int64_t)nf,
+                       pl.spatial_tiles, dp.spatial, dp.cka);
+    if ((st = launch_status("k_spatial_reduce")) != APACK_OK) return st;
+  }
+  hipLaunchKernelGGL(k_cka, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm.window, prm.tau_gate, prm.alignment,
+                     dp.band_v, dp.band_a, dp.cka, frame_cka, gate_fired);
   if ((st = launch_status("k_cka")) != APACK_OK) return st;
   const int64_t rows = visual_rows + audio_rows;
   if (rows > 0) {

@@ -21,6 +21,8 @@ static apack_status check_params(const apack_dyn_params* p) {
   APACK_CHECK(p->cover_thresh >= -1.0 && p->cover_thresh <= 1.0, APACK_E_ARG, "cover_thresh must lie in [-1, 1]");
   APACK_CHECK(p->dafps_power >= 0.0 && std::isfinite(p->dafps_power), APACK_E_ARG, "dafps_power must be >= 0");
   APACK_CHECK(p->r_pre >= 0.0 && p->r_pre <= 1.0, APACK_E_ARG, "r_pre must lie in [0, 1]");
+  APACK_CHECK(p->alignment >= APACK_ALIGN_GATED_CKA && p->alignment <= APACK_ALIGN_SPATIAL_CKA, APACK_E_ARG,
+              "alignment must be one of APACK_ALIGN_*");
   return APACK_OK;
 }
 
@@ -64,6 +66,18 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
     aud_end = std::max(aud_end, a.aud_off + a.n_audio);
     pl.max_per_frame = std::max(pl.max_per_frame, a.tokens_per_frame);
     pl.clips.push_back(c);
+  }
+  // Spatial CKA: one 16 x 16 tile per upper-triangle block of the stacked
+  // [co-timed audio; visual] rows of a frame, sized for the largest frame.
+  if (p->alignment == APACK_ALIGN_SPATIAL_CKA) {
+    int64_t m = 0;
+    for (int s = 0; s < n_seq; ++s) {
+      const apack_av_seq& a = seqs[s];
+      if (a.n_frames == 0) continue;
+      m = std::max<int64_t>(m, (a.n_audio + a.n_frames - 1) / a.n_frames + 1 + a.tokens_per_frame);
+    }
+    const int64_t nt = (m + 15) / 16;
+    pl.spatial_tiles = (int32_t)(nt * (nt + 1) / 2);
   }
   pl.total_frames = frames;
   pl.total_tokens = vis_end;
@@ -120,6 +134,8 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
   c.take<double>(gram);
   pl.off_scratch = c.used;
   c.take<double>(16 * (frames + nc + 1));
+  pl.off_spatial = c.used;
+  c.take<double>((size_t)frames * pl.spatial_tiles * 3);
   pl.ws_bytes = std::max<size_t>(c.used, kAlign);
   pl.gemm = std::move(tiles);
   return APACK_OK;
@@ -223,6 +239,7 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   dp.plan = reinterpret_cast<FramePlanDev*>(ws + pl.off_plan);
   dp.gram = reinterpret_cast<double*>(ws + pl.off_gram);
   dp.scratch = reinterpret_cast<double*>(ws + pl.off_scratch);
+  dp.spatial = reinterpret_cast<double*>(ws + pl.off_spatial);
   DynParamsDev prm;
   prm.tau_gate = p->tau_gate;
   prm.beta = p->beta;
@@ -234,6 +251,9 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   prm.power = p->dafps_power;
   prm.window = p->window;
   prm.dafps_k = p->dafps_k;
+  prm.alignment = p->alignment;
+  // AV cosine is the fine-pass term alone: the Eq. 2 blend with beta = 1.
+  if (p->alignment == APACK_ALIGN_AV_COSINE) prm.beta = 1.0;
   return launch_dynamics(pl, dp, prm, dtype, dim, visual, audio, query, pl.total_tokens, pl.total_audio, frame_cka,
                          frame_score, frame_budget, segment_id, gate_fired, kept_visual, hs);
 }

@@ -27,7 +27,7 @@ struct ClipDev {
 
 struct DynParamsDev {
   double tau_gate, beta, gamma, tau_sim, sigma, lambda_seg, cover, power;
-  int32_t window, dafps_k;
+  int32_t window, dafps_k, alignment;
 };
 
 // Per-frame work item: clip and frame index within it.
@@ -46,11 +46,13 @@ struct DynPlan {
   int64_t total_frames = 0, total_tokens = 0, total_audio = 0, total_kept = 0, total_gram = 0;
   int max_per_frame = 1;
   int64_t gemm_tiles = 0;            // gate GEMM workgroups over all clips
+  int32_t spatial_tiles = 0;         // spatial CKA Gram tiles per frame (0 unless selected)
   std::vector<GemmTileDev> gemm;
   // Workspace layout (byte offsets).
   size_t off_clips = 0, off_frames = 0, off_gemm = 0, blob_bytes = 0;
   size_t off_v = 0, off_a = 0, off_q = 0, off_band_v = 0, off_band_a = 0, off_vq = 0, off_qq = 0;
   size_t off_cka = 0, off_nv = 0, off_na = 0, off_maxkey = 0, off_plan = 0, off_gram = 0, off_scratch = 0;
+  size_t off_spatial = 0;
   size_t ws_bytes = 0;
 };
 
@@ -73,7 +75,7 @@ struct DynPtrs {
   ClipDev* clips;
   FrameDev* frames;
   GemmTileDev* gemm;
-  double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *na, *gram, *scratch;
+  double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *na, *gram, *scratch, *spatial;
   uint32_t* maxkey;
   FramePlanDev* plan;
 };

@@ -171,6 +171,7 @@ void apack_dyn_params_default(apack_dyn_params* p) {
   p->cover_thresh = 0.8;
   p->dafps_power = 0.5;
   p->r_pre = 0.50;
+  p->alignment = APACK_ALIGN_GATED_CKA;
 }
 
 }  // extern "C"

@@ -60,7 +60,11 @@ def test_default_params_are_table_s1():
     p = A.apack_dyn_params_default()
     got = {f: getattr(p, f) for f, _ in A.DynParams._fields_}
     for key, val in OD.DEFAULTS.items():
+        if key == "alignment":   # the library numbers the scorers, the oracle names them
+            assert got[key] == L.ALIGNMENTS[val] == 0
+            continue
         assert got[key] == val, key
+    assert sorted(L.ALIGNMENTS, key=L.ALIGNMENTS.get) == list(OD.ALIGNMENTS)
 
 
 # -- validation paths (fake, never dereferenced device addresses) ------------
@@ -346,7 +350,7 @@ def test_score_empty_batch_is_ok_without_device():
     ("power", 1), ("tau_nan", 1), ("dim_odd", 2), ("dim_big", 2), ("per_frame", 2), ("no_audio", 2),
     ("no_query", 2), ("neg_off", 2), ("vis_rows", 2), ("aud_rows", 2), ("qry_rows", 2), ("capacity", 2),
     ("null_visual", 1), ("misaligned", 1), ("null_kept", 1), ("out_in", 5), ("out_out", 5), ("small_ws", 4),
-    ("misaligned_ws", 4), ("null_ws", 4), ("dtype", 3),
+    ("misaligned_ws", 4), ("null_ws", 4), ("dtype", 3), ("alignment", 1), ("alignment_neg", 1),
 ])
 def test_score_validation_errors(case, status):
     kw = {}
@@ -354,6 +358,7 @@ def test_score_validation_errors(case, status):
     base = FAKE + (8 << 34)
     outs = [base + i * (1 << 30) for i in range(6)]
     params = {"window0": {"window": 0}, "window17": {"window": 17}, "dafps_k": {"dafps_k": 33},
+              "alignment": {"alignment": 4}, "alignment_neg": {"alignment": -1},
               "sigma": {"sigma": 0.0}, "beta": {"beta": 1.5}, "r_pre": {"r_pre": 1.01},
               "cover": {"cover_thresh": 1.5}, "power": {"dafps_power": -1.0},
               "tau_nan": {"tau_gate": float("nan")}}
@@ -403,3 +408,19 @@ def test_score_validation_errors(case, status):
     st, msg, nk = _score(seqs, **kw)
     assert st == status, (msg, case)
     assert msg
+
+
+def test_spatial_alignment_sizes_its_tile_sums():
+    # The spatial scorer needs per-frame tile sums; the other scorers do not.
+    seqs = [_av(n_frames=30, per_frame=144, n_audio=375)]
+    arr = (L.AVSeq * 1)(*seqs)
+    sizes = {}
+    for name, code in L.ALIGNMENTS.items():
+        p = A.apack_dyn_params_default()
+        p.alignment = code
+        ws = ctypes.c_size_t(0)
+        assert A.library().apack_score_dynamics_query(1, arr, 3584, ctypes.byref(p), None, ctypes.byref(ws)) == 0
+        sizes[name] = ws.value
+    assert sizes["gated_cka"] == sizes["cka"] == sizes["av_cosine"]
+    # 13 or 14 audio rows + 144 visual rows -> 10 tiles a side, 55 tiles, 3 sums each, per frame.
+    assert sizes["spatial_cka"] - sizes["gated_cka"] >= 30 * 55 * 3 * 8

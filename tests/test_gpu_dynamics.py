@@ -139,3 +139,46 @@ def test_budget_extremes(r_pre):
     want = _oracle(case)
     _certify(want)
     _compare(case, _run(case), want)
+
+
+# -- alternative alignment scorers (the supplement's scorer comparison) -------
+
+@pytest.mark.parametrize("alignment", ["gated_cka", "cka", "av_cosine", "spatial_cka"])
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_alignment_scorers_small_clips(structure, alignment):
+    case = W.dynamics_small(structure, seed=8)
+    case.params = dict(case.params, alignment=alignment)
+    log(f"[dynamics] small {structure}, {alignment}")
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+@pytest.mark.parametrize("alignment", ["cka", "av_cosine", "spatial_cka"])
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_alignment_scorers_7b_shape_60s_clip(structure, alignment):
+    case = W.dynamics_cfg3(structure)
+    case.params = dict(case.params, alignment=alignment)
+    log(f"[dynamics] 60 s clip, 3584-d, {structure}, {alignment}")
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+def test_spatial_cka_ragged_batch_with_edge_shapes():
+    # Bins of one audio token (N_A = F), a frame with more audio rows than a
+    # tile, P not a multiple of the 16-row tile, and the largest P.
+    parts = [
+        W.dynamics_small("offset", seed=21, frames=30, per_frame=16, audio=375),
+        W.dynamics_small("shared", seed=26, frames=10, per_frame=9, audio=10),     # one audio row per bin
+        W.dynamics_small("shared", seed=23, frames=1, per_frame=5, audio=40),      # 40 audio rows, one frame
+        W.dynamics_small("offset", seed=24, frames=20, per_frame=70, audio=250),
+        W.dynamics_small("shared", seed=25, frames=12, per_frame=256, audio=150),
+    ]
+    case = _packed(parts, {"window": 3, "r_pre": 0.5, "alignment": "spatial_cka"})
+    want = _oracle(case)
+    _certify(want)
+    got = _run(case)
+    _compare(case, got, want)
+    f0 = sum(p.seqs[0].n_frames for p in parts[:1])
+    assert np.all(got["cka"][f0:f0 + 10] == 0.0)   # one-token bins have no audio covariance

@@ -350,3 +350,77 @@ def test_scorer_recovers_planted_scenes_and_budgets(structure):
     np.testing.assert_array_equal(per_frame, r["frame_budget"])
     for key, m in r["margins"].items():
         assert m > 1e-9, key
+
+
+# -- alternative alignment scorers -------------------------------------------
+
+def _spatial_by_covariance(xv, xa, F, P):
+    """Spatial CKA the long way: explicit d x d feature covariances of each
+    frame's centred patches and centred co-timed audio tokens, compared by
+    their Frobenius cosine."""
+    out = []
+    for f, (lo, hi) in enumerate(OD.audio_bins(xa.shape[0], F)):
+        v = xv[f * P:(f + 1) * P]
+        a = xa[lo:hi]
+        cv = (v - v.mean(0)).T @ (v - v.mean(0))
+        ca = (a - a.mean(0)).T @ (a - a.mean(0))
+        den = np.linalg.norm(cv) * np.linalg.norm(ca)
+        out.append(float(np.sum(cv * ca) / den) if den else 0.0)
+    return np.array(out)
+
+
+def test_spatial_cka_equals_feature_covariance_alignment():
+    rng = np.random.default_rng(41)
+    for F, P, NA, d in ((5, 7, 23, 6), (3, 16, 9, 11), (8, 4, 40, 3)):
+        xv = rng.standard_normal((F * P, d))
+        xa = rng.standard_normal((NA, d))
+        np.testing.assert_allclose(OD.spatial_cka(xv, xa, F, P), _spatial_by_covariance(xv, xa, F, P),
+                                   rtol=1e-12, atol=1e-15)
+
+
+def test_spatial_cka_rank_one_is_squared_cosine():
+    # Patches varying along w only and audio along u only: c = cos^2(u, w).
+    rng = np.random.default_rng(42)
+    d, P = 9, 12
+    u, w = rng.standard_normal(d), rng.standard_normal(d)
+    base_v, base_a = rng.standard_normal(d), rng.standard_normal(d)
+    xv = base_v + np.outer(rng.standard_normal(P), w)
+    xa = base_a + np.outer(rng.standard_normal(6), u)     # one frame, bin of all 6 audio rows
+    want = (u @ w) ** 2 / ((u @ u) * (w @ w))
+    assert OD.spatial_cka(xv, xa, 1, P)[0] == pytest.approx(want, rel=1e-12)
+
+
+def test_spatial_cka_invariances_and_degenerate_bins():
+    rng = np.random.default_rng(43)
+    F, P, NA, d = 4, 10, 30, 7
+    xv = rng.standard_normal((F * P, d))
+    xa = rng.standard_normal((NA, d))
+    c = OD.spatial_cka(xv, xa, F, P)
+    q, _ = np.linalg.qr(rng.standard_normal((d, d)))
+    np.testing.assert_allclose(OD.spatial_cka(xv @ q, xa @ q, F, P), c, rtol=1e-11)       # shared rotation
+    np.testing.assert_allclose(OD.spatial_cka(3.5 * xv, 0.2 * xa, F, P), c, rtol=1e-12)   # scales
+    shift = np.repeat(rng.standard_normal((F, d)), P, axis=0)
+    np.testing.assert_allclose(OD.spatial_cka(xv + shift, xa + 5.0, F, P), c, rtol=1e-9)  # per-frame shifts
+    perm = np.concatenate([f * P + rng.permutation(P) for f in range(F)])
+    np.testing.assert_allclose(OD.spatial_cka(xv[perm], xa, F, P), c, rtol=1e-12)         # patch order
+    assert np.all((c >= 0.0) & (c <= 1.0 + 1e-12))
+    # A bin of one audio token has no covariance: c = 0.
+    assert np.all(OD.spatial_cka(xv, xa[:F], F, P) == 0.0)
+
+
+def test_alignment_modes_select_their_frame_scores():
+    case = W.dynamics_small("offset", seed=44)
+    s = case.seqs[0]
+    xv, xa, xq = (widen(x, "bf16") for x in (case.xv, case.xa, case.xq))
+    base = OD.score_sequence(xv, xa, xq, s.n_frames, s.per_frame, case.params)
+    cka = OD.score_sequence(xv, xa, xq, s.n_frames, s.per_frame, dict(case.params, alignment="cka"))
+    assert base["gate"] and not cka["gate"]
+    np.testing.assert_array_equal(cka["alpha"], cka["cka"])
+    av = OD.score_sequence(xv, xa, xq, s.n_frames, s.per_frame, dict(case.params, alignment="av_cosine"))
+    assert av["gate"]
+    np.testing.assert_array_equal(av["alpha"], 1.0 - av["dhat"])
+    np.testing.assert_array_equal(av["dhat"], base["dhat"])
+    sp = OD.score_sequence(xv, xa, xq, s.n_frames, s.per_frame, dict(case.params, alignment="spatial_cka"))
+    np.testing.assert_array_equal(sp["cka"], OD.spatial_cka(xv, xa, s.n_frames, s.per_frame))
+    with pytest.raises(ValueError):
+        OD.score_sequence(xv, xa, xq, s.n_frames, s.per_frame, dict(case.params, alignment="ot"))

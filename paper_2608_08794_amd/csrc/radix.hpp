@@ -80,16 +80,18 @@ __device__ void pick_bins(SeqDev* sq, uint32_t* hist, int pass) {
       c[j] = b >= 0 ? ld_agent(h + b) : 0u;
       sum += c[j];
     }
+    // Read the rank and prefix before the scan: its barrier keeps every
+    // thread's read ahead of the one thread that overwrites them below.
+    const uint32_t kk = sq->kk[m], prefix0 = sq->prefix[m];
     uint32_t total;
     const uint32_t incl = block_scan<NT>(sum, sh, total);
     uint32_t before = incl - sum;
-    const uint32_t kk = sq->kk[m];
     if (before < kk && incl >= kk) {
 #pragma unroll
       for (int j = 0; j < B; ++j) {
         if (before < kk && before + c[j] >= kk) {
           const uint32_t b = (uint32_t)(nb - 1 - (tid * B + j));
-          const uint32_t prefix = pass == 0 ? b : (sq->prefix[m] << (pass == 1 ? 11 : 9)) | b;
+          const uint32_t prefix = pass == 0 ? b : (prefix0 << (pass == 1 ? 11 : 9)) | b;
           sq->prefix[m] = prefix;
           sq->kk[m] = kk - before;
           if (pass == 2) {

@@ -198,6 +198,133 @@ __global__ __launch_bounds__(kT) void k_keep_write(const SeqDev* __restrict__ se
     }
 }
 
+// ---------------------------------------------------------------------------
+// Short sequences (up to kSmallRows rows): one workgroup per sequence holds
+// every row's tag and score in registers and runs the last two digits with
+// LDS histograms, the threshold, and the ordered kept list, in one launch
+// instead of four.  Same rules as above: rows above the threshold, then the
+// first `need` rows equal to it in row order.
+// ---------------------------------------------------------------------------
+constexpr int kST = 1024;                 // threads
+constexpr int kSPer = 16;                 // contiguous rows per thread
+constexpr int kSmallRows = kST * kSPer;
+
+__global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__ seqs,
+                                                      const uint8_t* __restrict__ tags,
+                                                      float* __restrict__ scores, int32_t* __restrict__ kept) {
+  __shared__ uint32_t lh[2 * kBins1];
+  __shared__ uint32_t sh[kST / 64];
+  __shared__ uint32_t s_prefix[2], s_kk[2], s_thr[2], s_need[2];
+  const SeqDev& sq = seqs[blockIdx.x];
+  const int n = (int)sq.n_tokens;
+  if (n == 0) return;
+  const int tid = threadIdx.x;
+  const uint8_t* tg = tags + sq.tag_off;
+  uint32_t bits[kSPer];
+  uint8_t mt[kSPer];
+#pragma unroll
+  for (int u = 0; u < kSPer; ++u) {
+    const int i = tid * kSPer + u;
+    mt[u] = i < n ? tg[i] : 0xFF;
+    bits[u] = 0;
+    if (mt[u] == 1 || mt[u] == 2) bits[u] = clamp_bits(scores[sq.tok_off + i]);
+    // Scores of sequences with candidates are written by the score kernels;
+    // a sequence without any has no score workgroups.
+    if (mt[u] == 0 && sq.n_cand == 0) scores[sq.tok_off + i] = 0.f;
+  }
+  if (tid < 2) {
+    s_prefix[tid] = sq.prefix[tid];
+    s_kk[tid] = sq.kk[tid];
+    s_thr[tid] = sq.thr[tid];
+    s_need[tid] = (uint32_t)sq.need[tid];
+  }
+  __syncthreads();
+  const bool act0 = sq.select[0] != 0, act1 = sq.select[1] != 0;
+  for (int pass = 1; pass <= 2 && (act0 || act1); ++pass) {
+    for (int b = tid; b < 2 * kBins1; b += kST) lh[b] = 0;
+    __syncthreads();
+    const uint32_t pre0 = s_prefix[0], pre1 = s_prefix[1];
+#pragma unroll
+    for (int u = 0; u < kSPer; ++u) {
+      const bool a = mt[u] == 1 && act0, v = mt[u] == 2 && act1;
+      if (!a && !v) continue;
+      uint32_t d;
+      if (digit_of(bits[u], pass, a ? pre0 : pre1, d)) atomicAdd(&lh[(a ? 0 : kBins1) + d], 1u);
+    }
+    __syncthreads();
+    // Bin holding the kk-th largest value: thread t covers bins
+    // nb-1-2t and nb-2-2t (descending), a block scan finds it.
+    const int nb = pass == 2 ? 512 : kRadixBins;
+    for (int m = 0; m < 2; ++m) {
+      if (!(m == 0 ? act0 : act1)) continue;
+      uint32_t c[2], sum = 0;
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int b = nb - 1 - (tid * 2 + j);
+        c[j] = b >= 0 ? lh[m * kBins1 + b] : 0u;
+        sum += c[j];
+      }
+      // Rank and prefix are read before the scan, whose barrier keeps every
+      // read ahead of the single write below.
+      const uint32_t kk = s_kk[m], prefix0 = s_prefix[m];
+      uint32_t total;
+      const uint32_t incl = block_scan<kST>(sum, sh, total);
+      uint32_t before = incl - sum;
+      if (before < kk && incl >= kk) {
+#pragma unroll
+        for (int j = 0; j < 2; ++j) {
+          if (before < kk && before + c[j] >= kk) {
+            const uint32_t b = (uint32_t)(nb - 1 - (tid * 2 + j));
+            const uint32_t prefix = (prefix0 << (pass == 1 ? 11 : 9)) | b;
+            s_prefix[m] = prefix;
+            s_kk[m] = kk - before;
+            if (pass == 2) {
+              s_thr[m] = prefix;
+              s_need[m] = kk - before;
+            }
+          }
+          before += c[j];
+        }
+      }
+      __syncthreads();
+    }
+  }
+  // Kept list: ties ranked in row order, then positions by a block scan.
+  const uint32_t thr0 = s_thr[0], thr1 = s_thr[1], need0 = s_need[0], need1 = s_need[1];
+  uint32_t ea = 0, ev = 0;
+#pragma unroll
+  for (int u = 0; u < kSPer; ++u) {
+    ea += mt[u] == 1 && bits[u] == thr0;
+    ev += mt[u] == 2 && bits[u] == thr1;
+  }
+  uint32_t tot;
+  const uint32_t packed = ea | (ev << 16);
+  const uint32_t ex = block_scan<kST>(packed, sh, tot) - packed;
+  // keep(u) with the tie ranks running from (ra, rv); the ranks advance.
+  auto keep_row = [&](int u, uint32_t& ra, uint32_t& rv) {
+    const uint8_t m = mt[u];
+    if (m == 0) return true;
+    if (m == 1) return bits[u] > thr0 || (bits[u] == thr0 && ra++ < need0);
+    if (m == 2) return bits[u] > thr1 || (bits[u] == thr1 && rv++ < need1);
+    return false;
+  };
+  uint32_t nk = 0;
+  {
+    uint32_t ra = ex & 0xFFFFu, rv = ex >> 16;
+#pragma unroll
+    for (int u = 0; u < kSPer; ++u) nk += keep_row(u, ra, rv);
+  }
+  uint32_t pos = block_scan<kST>(nk, sh, tot) - nk;
+  int32_t* out = kept + sq.out_off;
+  uint32_t ra = ex & 0xFFFFu, rv = ex >> 16;
+#pragma unroll
+  for (int u = 0; u < kSPer; ++u)
+    if (keep_row(u, ra, rv)) {
+      if (pos < (uint32_t)sq.n_kept) out[pos] = (int32_t)(sq.tok_off + tid * kSPer + u);
+      ++pos;
+    }
+}
+
 }  // namespace
 
 int64_t select_hist_words(int64_t n_seq) { return n_seq * 2 * kRadixBins; }
@@ -208,6 +335,11 @@ apack_status launch_select(const PrunePlan& pl, const DevPtrs& dp, float* scores
   if (nf == 0) return APACK_OK;
   apack_status st;
   // The scores and the first digit come from k_colsum, earlier on this stream.
+  if (pl.max_tokens <= kSmallRows) {
+    hipLaunchKernelGGL(k_select_small, dim3((unsigned)pl.seqs.size()), dim3(kST), 0, stream, dp.seqs, dp.tags,
+                       scores, kept);
+    return launch_status("k_select_small");
+  }
   if (pl.any_select) {
     for (int pass = 1; pass <= 2; ++pass) {
       hipLaunchKernelGGL(k_select_pass, dim3(nf), dim3(kT), 0, stream, dp.seqs, dp.ftiles, dp.tags, scores,

@@ -331,6 +331,24 @@ def test_long_sequence_beyond_register_resident_select():
     _parity(case)
 
 
+@pytest.mark.parametrize("n", [16384, 16385])
+@pytest.mark.parametrize("ties", [False, True])
+def test_select_paths_meet_at_16384_rows(n, ties):
+    # Sequences of up to 16384 rows are selected by one workgroup each;
+    # longer ones by the tiled kernels.  Both must keep the same rows, with
+    # all-equal scores (every key zero) ranked by row.
+    specs = [([(0, 3000, A_), (3000, n - 3100, V_)], n, 5, (0.45, 0.3))]
+    case = _synthetic("bf16", 4, 1, 64, specs, seed=17, zero_keys=ties)
+    if not ties:
+        _parity(case)
+        return
+    w_scores, w_kept, _, _ = _oracle(case)
+    g_scores, g_kept, _ = _run_prune(case)
+    np.testing.assert_array_equal(g_kept, w_kept)
+    k_a, k_v = OP.keep_count(0.45, 3000), OP.keep_count(0.3, n - 3100)
+    assert w_kept.tolist() == list(range(k_a)) + list(range(3000, 3000 + k_v)) + list(range(n - 100, n))
+
+
 # -- Eq. 6 as written: one TopK over S, last query token only ----------------
 
 

@@ -26,6 +26,7 @@
 #include <algorithm>
 #include <cfloat>
 #include <cmath>
+#include <type_traits>
 
 #include "common.hpp"
 #include "dynamics_plan.hpp"
@@ -298,14 +299,6 @@ __global__ __launch_bounds__(kBlk) void k_norms(int64_t n_vis, int64_t n_aud, in
       na[row - n_vis] = acc;
     }
   }
-}
-
-__device__ __forceinline__ uint32_t order_key(float x) {
-  const uint32_t u = __float_as_uint(x);
-  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
-}
-__device__ __forceinline__ float key_value(uint32_t k) {
-  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
 }
 
 // ---------------------------------------------------------------------------
@@ -1074,9 +1067,18 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
     if ((st = launch_status("k_norms")) != APACK_OK) return st;
   }
   if (pl.gemm_tiles > 0) {
-    hipLaunchKernelGGL(k_gate_gemm<T>, dim3((unsigned)pl.gemm_tiles), dim3(kBlk), 0, s, dp.clips, dp.gemm, dim, xv,
-                       xa, dp.na, dp.maxkey);
-    if ((st = launch_status("k_gate_gemm")) != APACK_OK) return st;
+    if constexpr (std::is_same<T, bf16_t>::value) {
+      if (pl.use256) {
+        if ((st = launch_gate_gemm256(dp.clips, dp.gemm, pl.gemm_tiles, dim, xv, xa, dp.na, dp.maxkey, s)) !=
+            APACK_OK)
+          return st;
+      }
+    }
+    if (!pl.use256) {
+      hipLaunchKernelGGL(k_gate_gemm<T>, dim3((unsigned)pl.gemm_tiles), dim3(kBlk), 0, s, dp.clips, dp.gemm, dim,
+                         xv, xa, dp.na, dp.maxkey);
+      if ((st = launch_status("k_gate_gemm")) != APACK_OK) return st;
+    }
   }
   PlanScratch scr;
   {

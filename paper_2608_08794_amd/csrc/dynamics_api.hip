@@ -96,7 +96,9 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
         for (int n = g0; n < std::min(g0 + 8, nb); ++n) tiles.push_back({s, m * 128, n * 128, 0});
   }
   pl.gemm_tiles = (int64_t)tiles.size();
-  const size_t n_tiles = tiles.size();
+  if (dim % kGemm256K == 0) pl.gemm256 = gate_gemm256_tiles(pl.clips);
+  // The blob holds whichever list the call uses.
+  const size_t n_tiles = std::max(tiles.size(), pl.gemm256.size());
   // Workspace layout.
   const int64_t nc = n_seq;
   Carver c(nullptr);
@@ -211,6 +213,12 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   APACK_CHECK(workspace_bytes >= pl.ws_bytes, APACK_E_WORKSPACE, "workspace of %zu bytes < %zu needed",
               workspace_bytes, pl.ws_bytes);
 
+  // bf16 inputs with dim a multiple of 64 take the 256 x 256 gate GEMM.
+  if (dtype == APACK_BF16 && !pl.gemm256.empty()) {
+    pl.use256 = true;
+    pl.gemm = pl.gemm256;
+    pl.gemm_tiles = (int64_t)pl.gemm.size();
+  }
   Staging* blk;
   void* host;
   if ((st = staging_acquire(pl.blob_bytes, &blk, &host)) != APACK_OK) return st;

@@ -48,6 +48,8 @@ struct DynPlan {
   int64_t gemm_tiles = 0;            // gate GEMM workgroups over all clips
   int32_t spatial_tiles = 0;         // spatial CKA Gram tiles per frame (0 unless selected)
   std::vector<GemmTileDev> gemm;
+  std::vector<GemmTileDev> gemm256;  // 256 x 256 tiles (dim a multiple of 64), XCD-ordered
+  bool use256 = false;               // set per call: bf16 inputs and gemm256 planned
   // Workspace layout (byte offsets).
   size_t off_clips = 0, off_frames = 0, off_gemm = 0, blob_bytes = 0;
   size_t off_v = 0, off_a = 0, off_q = 0, off_band_v = 0, off_band_a = 0, off_vq = 0, off_qq = 0;
@@ -55,6 +57,17 @@ struct DynPlan {
   size_t off_spatial = 0;
   size_t ws_bytes = 0;
 };
+
+// Order-preserving 32-bit keys of fp32 values, so an integer atomicMax
+// finds the largest cosine whatever its sign (the visual max-cosine slots
+// start at key 0, below every real value).
+__device__ __forceinline__ uint32_t order_key(float x) {
+  const uint32_t u = __float_as_uint(x);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+__device__ __forceinline__ float key_value(uint32_t k) {
+  return __uint_as_float((k & 0x80000000u) ? (k & 0x7FFFFFFFu) : ~k);
+}
 
 // Per-frame plan written by k_plan and read by the token-selection kernels.
 struct FramePlanDev {
@@ -79,6 +92,15 @@ struct DynPtrs {
   uint32_t* maxkey;
   FramePlanDev* plan;
 };
+
+// The gate GEMM on 256 x 256 tiles for bf16 inputs whose dim is a multiple
+// of 64 (gate_gemm.hip); `tiles` holds one tile per workgroup, already in
+// the order the launch expects.
+apack_status launch_gate_gemm256(const ClipDev* clips, const GemmTileDev* tiles, int64_t n_tiles, int dim,
+                                 const uint16_t* xv, const uint16_t* xa, const double* na, uint32_t* maxkey,
+                                 hipStream_t stream);
+std::vector<GemmTileDev> gate_gemm256_tiles(const std::vector<ClipDev>& clips);
+constexpr int kGemm256K = 64;   // dim must be a multiple of this for the 256-tile kernel
 
 apack_status launch_dynamics(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& prm, apack_dtype dt,
                              int dim, const void* visual, const void* audio, const void* query, int64_t visual_rows,

@@ -1,0 +1,220 @@
+// Gate GEMM of the direct audio-visual distance (Section 3.1, "Gated fine
+// pass"; the fine-pass term of Eq. 2): for every visual token i of a clip
+// whose gate fired, max_j x_A[j] . x_V[i] / |x_A[j]|, from C = X_A X_V^T on
+// bf16 MFMA with fp32 accumulation.  This is the kernel for bf16 inputs
+// whose dim is a multiple of 64; k_gate_gemm in dynamics.hip covers the rest.
+//
+// Each workgroup owns a 256 x 256 tile (audio rows x visual columns); its
+// four waves own 128 x 128 quadrants as 4 x 4 blocks of
+// v_mfma_f32_32x32x16_bf16, so a wave reads 8 fragments from LDS per 16
+// MFMAs.  K streams through two 64-element LDS stages (2 x 64 KiB), filled
+// by 16-byte direct-to-LDS loads while the other stage is consumed; the
+// 128-byte rows are stored with their 16-byte chunks XOR-swizzled by the
+// row index, so the fragment reads of consecutive rows hit distinct banks
+// without padding.  Every output element sees the same sequence of MFMAs
+// (K in order, 16 at a time) as in k_gate_gemm, so the results are the same
+// bits.  The epilogue scales by the inverse audio norms and folds the
+// column maxima into order-preserving keys with atomicMax.
+//
+// Workgroups are dealt to the eight XCDs round-robin by index, so the host
+// lists the tiles so that each XCD gets whole column blocks (all their row
+// tiles) and the workgroups resident on one XCD share their operands in
+// that XCD's L2.
+#include <algorithm>
+#include <cmath>
+
+#include "common.hpp"
+#include "dynamics_plan.hpp"
+
+namespace apack {
+namespace {
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+typedef __attribute__((address_space(1))) void* glb_ptr_t;
+
+constexpr int kTile = 256;                     // rows and columns per workgroup
+constexpr int kK = kGemm256K;                  // K elements per LDS stage
+constexpr int kStages = 2;                     // stages in flight (loads kStages-1 ahead)
+constexpr int kRowB = kK * 2;                  // bytes of one row per stage
+constexpr int kChunks = kRowB / 16;            // 16-byte chunks per row
+constexpr int kOpB = kTile * kRowB;            // one operand's stage
+constexpr int kStageB = 2 * kOpB;
+constexpr int kWaves = 4;
+constexpr int kLoadsPerWave = kOpB / 1024 / kWaves;  // 1 KiB loads per wave per operand
+constexpr int kXcds = 8;
+
+// Chunk c of row r sits at chunk c ^ swz(r).  A 16-byte LDS read is served
+// sixteen lanes at a time across 64 four-byte banks (256 bytes); the
+// sixteen consecutive rows those lanes read must then fill the 256 bytes
+// once.  Rows share a 256-byte window kRowsPer256 at a time, so the XOR key
+// is the row's index among the rows that fall on the same banks.
+constexpr int kRowsPer256 = 256 / kRowB;
+__device__ __forceinline__ int swz(int r) { return (r / kRowsPer256) & (kChunks - 1); }
+
+// One operand's stage: rows r0 .. r0+255 (clamped to the last valid row),
+// elements [k0, k0 + kK).  Load j fills LDS bytes [1024 j, 1024 j + 1024);
+// lane l's 16 bytes land at row r = (1024 j + 16 l) / kRowB, chunk c, and
+// come from global chunk c ^ swz(r).
+__device__ __forceinline__ void issue_operand(char* lds, const uint16_t* base, int64_t r0, int64_t n_rows, int dim,
+                                              int k0, int wave, int lane) {
+#pragma unroll
+  for (int i = 0; i < kLoadsPerWave; ++i) {
+    const int j = wave * kLoadsPerWave + i;
+    const int byte = j * 1024 + lane * 16;
+    const int r = byte / kRowB;
+    const int c = ((byte % kRowB) >> 4) ^ swz(r);
+    int64_t row = r0 + r;
+    if (row >= n_rows) row = n_rows - 1;
+    const char* src = reinterpret_cast<const char*>(base + row * dim + k0) + c * 16;
+    __builtin_amdgcn_global_load_lds((glb_ptr_t)src, (lds_ptr_t)(lds + j * 1024), 16, 0, 0);
+  }
+}
+
+// MFMA operand of rows row .. row+31 (row a multiple of 32 plus lane % 32)
+// and K elements [16 ks, 16 ks + 16): lane l holds 8 elements at
+// 16 ks + 8 (l / 32).
+__device__ __forceinline__ bf16x8 lds_frag(const char* lds, int row, int ks, int lane) {
+  const int c = (ks * 2 + (lane >> 5)) ^ swz(row);
+  return *reinterpret_cast<const bf16x8*>(lds + row * kRowB + c * 16);
+}
+
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gate_gemm256(
+    const ClipDev* __restrict__ clips, const GemmTileDev* __restrict__ tiles, int dim, const uint16_t* __restrict__ xv,
+    const uint16_t* __restrict__ xa, const double* __restrict__ na, uint32_t* __restrict__ maxkey) {
+  __shared__ __attribute__((aligned(16))) char lds[kStages * kStageB];
+  const GemmTileDev tl = tiles[blockIdx.x];
+  if (tl.clip < 0) return;  // padding of an XCD's share
+  const ClipDev c = clips[tl.clip];
+  if (!c.gate) return;
+  const int64_t n_a = c.n_audio, n_v = (int64_t)c.n_frames * c.per_frame;
+  const uint16_t* A = xa + c.aud_off * dim;
+  const uint16_t* B = xv + c.vis_off * dim;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int wm = wave >> 1, wn = wave & 1;
+
+  f32x16 acc[4][4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+
+  const int n_k = dim / kK;
+  auto issue = [&](int k_stage) {
+    char* st = lds + (k_stage % kStages) * kStageB;
+    issue_operand(st, A, tl.m0, n_a, dim, k_stage * kK, wave, lane);
+    issue_operand(st + kOpB, B, tl.n0, n_v, dim, k_stage * kK, wave, lane);
+  };
+  // Loads run kStages - 1 stages ahead of the MFMAs.
+  for (int p = 0; p < kStages - 1 && p < n_k; ++p) issue(p);
+  for (int it = 0; it < n_k; ++it) {
+    const int buf = it % kStages;
+    // Stage it has landed: each wave waits until at most the loads of the
+    // later stages it issued are outstanding, then the barrier makes every
+    // wave's share visible and guarantees the stage about to be refilled
+    // (read at it - 1) is no longer read.
+    const int ahead = std::min(kStages - 2, n_k - 1 - it);   // stages issued after this one
+    if (ahead >= 2)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * 2 * kLoadsPerWave) : "memory");
+    else if (ahead == 1)
+      asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kLoadsPerWave) : "memory");
+    else
+      asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    __syncthreads();
+    if (it + kStages - 1 < n_k) issue(it + kStages - 1);
+    const char* la = lds + buf * kStageB;
+    const char* lb = la + kOpB;
+    // Fragments of K slice ks + 1 are read while slice ks's 16 MFMAs run.
+    bf16x8 fa[2][4], fb[2][4];
+    auto read = [&](int ks, int h) {
+#pragma unroll
+      for (int i = 0; i < 4; ++i) fa[h][i] = lds_frag(la, wm * 128 + i * 32 + (lane & 31), ks, lane);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) fb[h][j] = lds_frag(lb, wn * 128 + j * 32 + (lane & 31), ks, lane);
+    };
+    read(0, 0);
+#pragma unroll
+    for (int ks = 0; ks < kK / 16; ++ks) {
+      const int h = ks & 1;
+      if (ks + 1 < kK / 16) read(ks + 1, h ^ 1);
+      // Keep the reads of slice ks + 1 ahead of slice ks's MFMAs: the
+      // scheduler would otherwise sink each read to its first use.
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[h][i], fb[h][j], acc[i][j], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+  }
+
+  // Epilogue.  Inverse audio norms of the tile's rows in LDS (-inf past the
+  // clip's audio, so those rows never win); acc[i][j][e] of lane l is audio
+  // row wm*128 + 32i + 8(e/4) + 4(l/32) + e%4, visual column
+  // wn*128 + 32j + l%32.
+  __syncthreads();
+  float* inv = reinterpret_cast<float*>(lds);
+  for (int r = tid; r < kTile; r += kWaves * 64) {
+    const int64_t row = tl.m0 + r;
+    float s = -INFINITY;
+    if (row < n_a) {
+      const double nn = na[c.aud_off + row];
+      s = nn > 0.0 ? (float)(1.0 / sqrt(nn)) : 0.0f;
+    }
+    inv[r] = s;
+  }
+  __syncthreads();
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    float m = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const float s = inv[wm * 128 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)];
+        m = fmaxf(m, s == -INFINITY ? -INFINITY : acc[i][j][e] * s);
+      }
+    m = fmaxf(m, __shfl_xor(m, 32));
+    const int64_t col = tl.n0 + wn * 128 + j * 32 + (lane & 31);
+    if (lane < 32 && col < n_v && m > -INFINITY) atomicMax(&maxkey[c.vis_off + col], order_key(m));
+  }
+}
+
+}  // namespace
+
+std::vector<GemmTileDev> gate_gemm256_tiles(const std::vector<ClipDev>& clips) {
+  // Column blocks (clip, n0) are dealt to the XCDs in turn; an XCD's share
+  // lists every row tile of its blocks, block after block.
+  std::vector<std::vector<GemmTileDev>> share(kXcds);
+  int next = 0;
+  for (size_t s = 0; s < clips.size(); ++s) {
+    const ClipDev& c = clips[s];
+    const int64_t nv = (int64_t)c.n_frames * c.per_frame;
+    if (nv == 0 || c.n_audio == 0) continue;
+    const int mb = (int)((c.n_audio + kTile - 1) / kTile), nb = (int)((nv + kTile - 1) / kTile);
+    for (int n = 0; n < nb; ++n, next = (next + 1) % kXcds)
+      for (int m = 0; m < mb; ++m) share[next].push_back({(int32_t)s, m * kTile, n * kTile, 0});
+  }
+  size_t rounds = 0;
+  for (auto& q : share) rounds = std::max(rounds, q.size());
+  std::vector<GemmTileDev> out;
+  out.reserve(rounds * kXcds);
+  for (size_t r = 0; r < rounds; ++r)
+    for (int x = 0; x < kXcds; ++x) out.push_back(r < share[x].size() ? share[x][r] : GemmTileDev{-1, 0, 0, 0});
+  // Trailing padding only costs empty workgroups; drop it.
+  while (!out.empty() && out.back().clip < 0) out.pop_back();
+  return out;
+}
+
+apack_status launch_gate_gemm256(const ClipDev* clips, const GemmTileDev* tiles, int64_t n_tiles, int dim,
+                                 const uint16_t* xv, const uint16_t* xa, const double* na, uint32_t* maxkey,
+                                 hipStream_t stream) {
+  if (n_tiles == 0) return APACK_OK;
+  hipLaunchKernelGGL(k_gate_gemm256, dim3((unsigned)n_tiles), dim3(kWaves * 64), 0, stream, clips, tiles, dim, xv, xa,
+                     na, maxkey);
+  return launch_status("k_gate_gemm256");
+}
+
+}  // namespace apack

@@ -18,7 +18,8 @@
 //                MFMA)
 //   k_dafps      one wave per anchor frame: density-aware farthest-point
 //                sampling
-//   k_dedup      one workgroup per non-anchor frame: keep the positions least
+//   k_dedup_sim, k_dedup_pick  one wave per token, then one workgroup per
+//                non-anchor frame: keep the positions least
 //                similar to the anchor
 //
 // Every discrete decision (gate, cuts, budgets, DA-FPS argmax, dedup ranks)
@@ -876,7 +877,8 @@ __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
 // in the same order), so thread i reads column i and a wave's loads for one
 // j are contiguous; loads are issued eight at a time.
 template <int KM>
-__device__ __forceinline__ double dafps_density(const double* S, int P, int i, int k, double cover) {
+__device__ __forceinline__ double dafps_density(const double* S, const double* Sl, int R, int P, int i, int k,
+                                                double cover) {
   double top[KM];
 #pragma unroll
   for (int q = 0; q < KM; ++q) top[q] = -INFINITY;
@@ -884,7 +886,10 @@ __device__ __forceinline__ double dafps_density(const double* S, int P, int i, i
   for (int j0 = 0; j0 < P; j0 += 8) {
     double vals[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) vals[u] = j0 + u < P ? S[(int64_t)(j0 + u) * P + i] : 0.0;
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + u;
+      vals[u] = j >= P ? 0.0 : j < R ? Sl[j * P + i] : S[(int64_t)j * P + i];
+    }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int j = j0 + u;
@@ -910,38 +915,22 @@ __device__ __forceinline__ double dafps_density(const double* S, int P, int i, i
   return fmax(knn, 0.0) * (1.0 + cov);
 }
 
-// Block-wide lexicographic (value desc, index asc) argmax; every thread
-// gets the winning index.
-__device__ __forceinline__ int block_argmax(double v, int idx, double* sv, int* si) {
-  wave_argmax(v, idx);
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (lane == 0) {
-    sv[wave] = v;
-    si[wave] = idx;
-  }
-  __syncthreads();
-  double bv = sv[0];
-  int bi = si[0];
-#pragma unroll
-  for (int w = 1; w < kMaxPerFrame / 64; ++w)
-    if (sv[w] > bv || (sv[w] == bv && si[w] < bi)) {
-      bv = sv[w];
-      bi = si[w];
-    }
-  __syncthreads();
-  return bi;
-}
 
 // ---------------------------------------------------------------------------
 // DA-FPS on an anchor frame: one workgroup, thread i owns token i.
 // ---------------------------------------------------------------------------
+// The anchor's first R rows of S (as many as fit) are copied to LDS; the
+// pick loop then runs in one wave, which holds up to four tokens per lane
+// and finds each pick with a shuffle argmax, so a pick costs one LDS row
+// read (a global one for the few rows past R) and no barrier.
+constexpr int kDafpsLdsDoubles = 20200;   // 161600 bytes of S rows; 160 KiB of LDS in all
+
 __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restrict__ clips,
                                                         const FrameDev* __restrict__ frames,
                                                         const FramePlanDev* __restrict__ plan, DynParamsDev prm,
                                                         const double* __restrict__ gram, int32_t* __restrict__ kept) {
-  __shared__ double sv[kMaxPerFrame / 64];
-  __shared__ int si[kMaxPerFrame / 64];
-  __shared__ int wcount[kMaxPerFrame / 64];
+  __shared__ double Sl[kDafpsLdsDoubles];
+  __shared__ double rho_sh[kMaxPerFrame];
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
   const int64_t frame = c.frame_off + fr.f;
@@ -950,34 +939,95 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
   const int P = c.per_frame, i = threadIdx.x;
   const int k = min(fp.budget, P);
   const double* S = gram + c.gram_off + (int64_t)fr.f * P * P;
-  const bool mine = i < P;
-  double rho = -INFINITY, wgt = 0.0, smax = 0.0;
-  bool taken = !mine;
-  if (mine) {
-    rho = prm.dafps_k <= 8    ? dafps_density<8>(S, P, i, prm.dafps_k, prm.cover)
-          : prm.dafps_k <= 16 ? dafps_density<16>(S, P, i, prm.dafps_k, prm.cover)
-                              : dafps_density<32>(S, P, i, prm.dafps_k, prm.cover);
-    wgt = pow(rho, prm.power);
+  const int R = min(P, kDafpsLdsDoubles / P);
+  // Eight independent loads in flight per thread.
+  for (int e0 = i; e0 < R * P; e0 += 8 * kMaxPerFrame) {
+    double v[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + u * kMaxPerFrame;
+      v[u] = e < R * P ? S[e] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int e = e0 + u * kMaxPerFrame;
+      if (e < R * P) Sl[e] = v[u];
+    }
   }
+  __syncthreads();
+  // Density of every token (thread per token).
+  if (i < P)
+    rho_sh[i] = prm.dafps_k <= 8    ? dafps_density<8>(S, Sl, R, P, i, prm.dafps_k, prm.cover)
+                : prm.dafps_k <= 16 ? dafps_density<16>(S, Sl, R, P, i, prm.dafps_k, prm.cover)
+                                    : dafps_density<32>(S, Sl, R, P, i, prm.dafps_k, prm.cover);
+  __syncthreads();
+  if (i >= 64) return;
+  // Wave 0: token t = lane + 64 u, u < 4.
+  constexpr int kU = kMaxPerFrame / 64;
+  const int lane = i;
+  double wgt[kU], smax[kU], rho[kU];
+  bool taken[kU];
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int t = lane + 64 * u;
+    taken[u] = t >= P;
+    rho[u] = taken[u] ? -INFINITY : rho_sh[t];
+    wgt[u] = taken[u] ? 0.0 : pow(rho[u], prm.power);
+    smax[u] = 0.0;
+  }
+  // Lexicographic (value desc, token asc) argmax: the wave's largest value
+  // first, then the lowest token holding it -- tokens 64u + lane ascend
+  // with u and then with the lane, so the first non-empty ballot in u order
+  // names it.
+  auto pick_of = [&](const double (&v)[kU]) {
+    double m = -INFINITY;
+#pragma unroll
+    for (int u = 0; u < kU; ++u)
+      if (!taken[u]) m = fmax(m, v[u]);
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) m = fmax(m, __shfl_xor(m, off));
+    int best = 0x7FFFFFFF;
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const uint64_t b = __ballot(!taken[u] && v[u] == m);
+      if (b && best == 0x7FFFFFFF) best = 64 * u + (int)__builtin_ctzll(b);
+    }
+    return best;
+  };
   // First pick: the densest token; then the farthest from the picked set,
   // weighted by density.
-  int pick = block_argmax(taken ? -INFINITY : rho, taken ? 0x7FFFFFFF : i, sv, si);
+  int pick = pick_of(rho);
   for (int n = 0;; ++n) {
-    if (i == pick) taken = true;
-    if (mine) smax = n == 0 ? S[(int64_t)pick * P + i] : fmax(smax, S[(int64_t)pick * P + i]);
+    double sv[kU];
+    if (pick < R) {  // the same branch for the whole wave
+#pragma unroll
+      for (int u = 0; u < kU; ++u) sv[u] = lane + 64 * u < P ? Sl[pick * P + lane + 64 * u] : 0.0;
+    } else {
+#pragma unroll
+      for (int u = 0; u < kU; ++u) sv[u] = lane + 64 * u < P ? S[(int64_t)pick * P + lane + 64 * u] : 0.0;
+    }
+#pragma unroll
+    for (int u = 0; u < kU; ++u) {
+      const int t = lane + 64 * u;
+      if (t == pick) taken[u] = true;
+      if (t < P) smax[u] = n == 0 ? sv[u] : fmax(smax[u], sv[u]);
+    }
     if (n + 1 >= k) break;
-    const double val = (1.0 - smax) * wgt;
-    pick = block_argmax(taken ? -INFINITY : val, taken ? 0x7FFFFFFF : i, sv, si);
+    double val[kU];
+#pragma unroll
+    for (int u = 0; u < kU; ++u) val[u] = (1.0 - smax[u]) * wgt[u];
+    pick = pick_of(val);
   }
   // Ascending output of the picked positions.
-  const bool kp = mine && taken;
-  const uint64_t bal = __ballot(kp);
-  const int lane = i & 63, wave = i >> 6;
-  if (lane == 0) wcount[wave] = __popcll(bal);
-  __syncthreads();
   int64_t pos = fp.out_off;
-  for (int w = 0; w < wave; ++w) pos += wcount[w];
-  if (kp) kept[pos + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(c.vis_off + (int64_t)fr.f * P + i);
+#pragma unroll
+  for (int u = 0; u < kU; ++u) {
+    const int t = lane + 64 * u;
+    const bool kp = t < P && taken[u];
+    const uint64_t bal = __ballot(kp);
+    if (kp) kept[pos + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(c.vis_off + (int64_t)fr.f * P + t);
+    pos += __popcll(bal);
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -985,36 +1035,55 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
 // token at the same position (lower position first on ties).
 // ---------------------------------------------------------------------------
 template <class T>
-__global__ __launch_bounds__(kBlk) void k_dedup(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
-                                                const FramePlanDev* __restrict__ plan, int dim,
-                                                const T* __restrict__ xv, const double* __restrict__ nv,
-                                                int32_t* __restrict__ kept) {
+__global__ __launch_bounds__(kBlk) void k_dedup_sim(const ClipDev* __restrict__ clips,
+                                                    const FrameDev* __restrict__ frames,
+                                                    const FramePlanDev* __restrict__ plan, int dim,
+                                                    const T* __restrict__ xv, const double* __restrict__ nv,
+                                                    double* __restrict__ sim) {
+  // One wave per position: cosine of token p of frame f with token p of its
+  // anchor, written to sim at the token's row.
+  const FrameDev fr = frames[blockIdx.x];
+  const ClipDev c = clips[fr.clip];
+  const FramePlanDev fp = plan[c.frame_off + fr.f];
+  if (fp.is_anchor || fp.budget == 0) return;
+  const int P = c.per_frame;
+  const int lane = threadIdx.x & 63;
+  const int p = blockIdx.y * (kBlk / 64) + (threadIdx.x >> 6);
+  if (p >= P) return;
+  const int64_t rowf = c.vis_off + (int64_t)fr.f * P + p, rowa = c.vis_off + (int64_t)fp.anchor * P + p;
+  const T* x = xv + rowf * dim;
+  const T* y = xv + rowa * dim;
+  double acc = 0.0, o[8], q[8];
+  for (int d = lane * 8; d < dim; d += 64 * 8) {
+    load8(x + d, o);
+    load8(y + d, q);
+#pragma unroll
+    for (int e = 0; e < 8; ++e) acc += o[e] * q[e];
+  }
+  acc = wave_sum(acc);
+  if (lane == 0) {
+    const double nx = sqrt(nv[rowf]), ny = sqrt(nv[rowa]);
+    sim[rowf - c.vis_off + c.token_off] = (nx == 0.0 || ny == 0.0) ? 0.0 : acc / (nx * ny);
+  }
+}
+
+__global__ __launch_bounds__(kBlk) void k_dedup_pick(const ClipDev* __restrict__ clips,
+                                                     const FrameDev* __restrict__ frames,
+                                                     const FramePlanDev* __restrict__ plan,
+                                                     const double* __restrict__ simg, int32_t* __restrict__ kept) {
+  // The k_f positions least similar to the anchor, lower position first on
+  // ties, written in ascending order.
   __shared__ double sim[kMaxPerFrame];
   __shared__ int wcount[kBlk / 64];
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
-  const int64_t frame = c.frame_off + fr.f;
-  const FramePlanDev fp = plan[frame];
+  const FramePlanDev fp = plan[c.frame_off + fr.f];
   if (fp.is_anchor || fp.budget == 0) return;
   const int P = c.per_frame;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int64_t rowf = c.vis_off + (int64_t)fr.f * P, rowa = c.vis_off + (int64_t)fp.anchor * P;
-  for (int p = wave; p < P; p += kBlk / 64) {
-    const T* x = xv + (rowf + p) * dim;
-    const T* y = xv + (rowa + p) * dim;
-    double acc = 0.0, o[8], q[8];
-    for (int d = lane * 8; d < dim; d += 64 * 8) {
-      load8(x + d, o);
-      load8(y + d, q);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc += o[e] * q[e];
-    }
-    acc = wave_sum(acc);
-    if (lane == 0) {
-      const double nx = sqrt(nv[rowf + p]), ny = sqrt(nv[rowa + p]);
-      sim[p] = (nx == 0.0 || ny == 0.0) ? 0.0 : acc / (nx * ny);
-    }
-  }
+  const int64_t rowf = c.vis_off + (int64_t)fr.f * P;
+  const double* sg = simg + c.token_off + (int64_t)fr.f * P;
+  for (int q = threadIdx.x; q < P; q += kBlk) sim[q] = sg[q];
   __syncthreads();
   const int p = threadIdx.x;
   bool kp = false;
@@ -1102,8 +1171,11 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
     if ((st = launch_status("k_gram")) != APACK_OK) return st;
     hipLaunchKernelGGL(k_dafps, dim3(nf), dim3(kMaxPerFrame), 0, s, dp.clips, dp.frames, dp.plan, prm, dp.gram, kept);
     if ((st = launch_status("k_dafps")) != APACK_OK) return st;
-    hipLaunchKernelGGL(k_dedup<T>, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dp.plan, dim, xv, dp.nv, kept);
-    if ((st = launch_status("k_dedup")) != APACK_OK) return st;
+    hipLaunchKernelGGL(k_dedup_sim<T>, dim3(nf, (pl.max_per_frame + kBlk / 64 - 1) / (kBlk / 64)), dim3(kBlk), 0, s,
+                       dp.clips, dp.frames, dp.plan, dim, xv, dp.nv, dp.sim);
+    if ((st = launch_status("k_dedup_sim")) != APACK_OK) return st;
+    hipLaunchKernelGGL(k_dedup_pick, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dp.plan, dp.sim, kept);
+    if ((st = launch_status("k_dedup_pick")) != APACK_OK) return st;
   }
   return APACK_OK;
 }

@@ -34,7 +34,7 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
   apack_status st = check_params(p);
   if (st != APACK_OK) return st;
   pl = DynPlan();
-  int64_t frames = 0, kept = 0, gram = 0, vis_end = 0, aud_end = 0;
+  int64_t frames = 0, kept = 0, gram = 0, vis_end = 0, aud_end = 0, tokens = 0;
   for (int s = 0; s < n_seq; ++s) {
     const apack_av_seq& a = seqs[s];
     APACK_CHECK(a.n_frames >= 0 && a.tokens_per_frame >= 1 && a.tokens_per_frame <= kMaxPerFrame, APACK_E_SHAPE,
@@ -51,7 +51,7 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
     c.n_frames = a.n_frames;
     c.per_frame = a.tokens_per_frame;
     c.frame_off = frames;
-    c.token_off = 0;
+    c.token_off = tokens;
     c.kept_off = kept;
     c.gram_off = gram;
     const int64_t nv = (int64_t)a.n_frames * a.tokens_per_frame;
@@ -60,6 +60,7 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
     pl.budgets.push_back(c.budget);
     for (int f = 0; f < a.n_frames; ++f) pl.frames.push_back({s, f});
     frames += a.n_frames;
+    tokens += nv;
     kept += c.budget;
     gram += nv * a.tokens_per_frame;
     vis_end = std::max(vis_end, a.vis_off + nv);
@@ -136,6 +137,8 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
   c.take<double>(gram);
   pl.off_scratch = c.used;
   c.take<double>(16 * (frames + nc + 1));
+  pl.off_sim = c.used;
+  c.take<double>(tokens);
   pl.off_spatial = c.used;
   c.take<double>((size_t)frames * pl.spatial_tiles * 3);
   pl.ws_bytes = std::max<size_t>(c.used, kAlign);
@@ -248,6 +251,7 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   dp.gram = reinterpret_cast<double*>(ws + pl.off_gram);
   dp.scratch = reinterpret_cast<double*>(ws + pl.off_scratch);
   dp.spatial = reinterpret_cast<double*>(ws + pl.off_spatial);
+  dp.sim = reinterpret_cast<double*>(ws + pl.off_sim);
   DynParamsDev prm;
   prm.tau_gate = p->tau_gate;
   prm.beta = p->beta;

@@ -16,7 +16,7 @@ struct ClipDev {
   int64_t vis_off, aud_off, qry_off;  // first rows in the packed inputs
   int64_t n_audio, n_query;
   int64_t frame_off;                  // first frame in the [sum F] arrays
-  int64_t token_off;                  // first visual token in [sum F*P] arrays (== frame_off * P for uniform P)
+  int64_t token_off;                  // first visual token of the clip in [sum F*P] arrays
   int64_t kept_off;                   // first slot of the clip in kept_visual
   int64_t gram_off;                   // first anchor-Gram slot: frame f uses [gram_off + f*P*P ...)
   int64_t budget;                     // B_v
@@ -54,7 +54,7 @@ struct DynPlan {
   size_t off_clips = 0, off_frames = 0, off_gemm = 0, blob_bytes = 0;
   size_t off_v = 0, off_a = 0, off_q = 0, off_band_v = 0, off_band_a = 0, off_vq = 0, off_qq = 0;
   size_t off_cka = 0, off_nv = 0, off_na = 0, off_maxkey = 0, off_plan = 0, off_gram = 0, off_scratch = 0;
-  size_t off_spatial = 0;
+  size_t off_spatial = 0, off_sim = 0;
   size_t ws_bytes = 0;
 };
 
@@ -88,7 +88,7 @@ struct DynPtrs {
   ClipDev* clips;
   FrameDev* frames;
   GemmTileDev* gemm;
-  double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *na, *gram, *scratch, *spatial;
+  double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *na, *gram, *scratch, *spatial, *sim;
   uint32_t* maxkey;
   FramePlanDev* plan;
 };

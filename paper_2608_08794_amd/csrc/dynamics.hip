@@ -10,7 +10,8 @@
 //   k_gate_gemm  only where the gate fired: X_A . X_V^T on bf16 MFMA, scaled
 //                by 1/|a_j|, max over audio tokens in-lane, merged across
 //                tiles by atomicMax on order-preserving uint keys
-//   k_plan       one workgroup per clip: direct distance, Eq. 2 blend,
+//   k_plan       one 1024-thread workgroup per clip, arrays in LDS:
+//                direct distance, Eq. 2 blend,
 //                continuity smoothing and cuts, Eq. 3 segment scores, frame
 //                scores, Eq. 4 segment budgets and frame budgets (capped
 //                largest remainder), anchors and output offsets
@@ -67,7 +68,9 @@ __device__ __forceinline__ double wave_sum(double v) {
   return v;
 }
 
-// Block-wide reductions (kBlk threads; every thread gets the result).
+// Block-wide reductions over NT threads (sh holds NT / 64 words); every
+// thread gets the result.
+template <int NT = kBlk>
 __device__ double block_sum(double v, double* sh) {
   v = wave_sum(v);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -75,10 +78,11 @@ __device__ double block_sum(double v, double* sh) {
   if (lane == 0) sh[wave] = v;
   __syncthreads();
   double t = 0.0;
-  for (int w = 0; w < kBlk / 64; ++w) t += sh[w];
+  for (int w = 0; w < NT / 64; ++w) t += sh[w];
   __syncthreads();
   return t;
 }
+template <int NT = kBlk>
 __device__ double block_max(double v, double* sh) {
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off));
@@ -87,11 +91,12 @@ __device__ double block_max(double v, double* sh) {
   if (lane == 0) sh[wave] = v;
   __syncthreads();
   double t = sh[0];
-  for (int w = 1; w < kBlk / 64; ++w) t = fmax(t, sh[w]);
+  for (int w = 1; w < NT / 64; ++w) t = fmax(t, sh[w]);
   __syncthreads();
   return t;
 }
-__device__ double block_min(double v, double* sh) { return -block_max(-v, sh); }
+template <int NT = kBlk>
+__device__ double block_min(double v, double* sh) { return -block_max<NT>(-v, sh); }
 
 // ---------------------------------------------------------------------------
 // Coarse pass (Section 3.1): v_f, a_f and the query mean.
@@ -436,130 +441,182 @@ __global__ __launch_bounds__(kBlk) void k_gate_gemm(const ClipDev* __restrict__ 
 
 // ---------------------------------------------------------------------------
 // Capped largest-remainder apportionment of `total` over items [0, n) with
-// weights w[i] and caps cap[i] (block-wide; scratch arrays in global memory).
-// Water-filling first (items whose quota exceeds their cap are fixed at the
-// cap, the rest re-shared), then floors and the leftover units to the
-// largest fractional parts, lower index first on ties.
+// weights w[i] and caps cap[i], run by one wave: lane l owns items l, l + 64,
+// ... and alone writes their fixed, quota and alloc entries.  Water-filling
+// first (items whose quota exceeds their cap are fixed at the cap, the rest
+// re-shared), then floors and the leftover units to the largest fractional
+// parts, lower index first on ties.
 // ---------------------------------------------------------------------------
-__device__ void apportion(int64_t total, int n, const double* w, const int64_t* cap, int32_t* fixed,
-                          double* quota, int64_t* alloc, double* sh) {
-  for (int i = threadIdx.x; i < n; i += kBlk) fixed[i] = 0;
-  __syncthreads();
+__device__ __forceinline__ void wave_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_ACQ_REL, "workgroup");
+  __builtin_amdgcn_wave_barrier();
+}
+
+__device__ void apportion_wave(int64_t total, int n, const double* w, const int64_t* cap, int32_t* fixed,
+                               double* quota, int64_t* alloc) {
+  const int lane = threadIdx.x & 63;
+  for (int i = lane; i < n; i += 64) fixed[i] = 0;
   for (int round = 0; round <= n; ++round) {
     double fixed_caps = 0.0, sw = 0.0, nfree = 0.0;
-    for (int i = threadIdx.x; i < n; i += kBlk) {
+    for (int i = lane; i < n; i += 64) {
       if (fixed[i]) fixed_caps += (double)cap[i];
       else {
         sw += w[i];
         nfree += 1.0;
       }
     }
-    fixed_caps = block_sum(fixed_caps, sh);
-    sw = block_sum(sw, sh);
-    nfree = block_sum(nfree, sh);
+    fixed_caps = wave_sum(fixed_caps);
+    sw = wave_sum(sw);
+    nfree = wave_sum(nfree);
     const double remaining = (double)total - fixed_caps;
-    double over = 0.0;
-    for (int i = threadIdx.x; i < n; i += kBlk) {
+    bool over = false;
+    for (int i = lane; i < n; i += 64) {
       if (fixed[i]) continue;
       const double qv = sw > 0.0 ? remaining * w[i] / sw : remaining / nfree;
       quota[i] = qv;
-      if (qv > (double)cap[i]) over += 1.0;
+      if (qv > (double)cap[i]) {  // fixed at its cap from the next round on
+        fixed[i] = 1;
+        over = true;
+      }
     }
-    over = block_sum(over, sh);
-    if (over == 0.0) break;
-    for (int i = threadIdx.x; i < n; i += kBlk)
-      if (!fixed[i] && quota[i] > (double)cap[i]) fixed[i] = 1;
-    __syncthreads();
+    if (__ballot(over) == 0) break;
   }
   double used = 0.0;
-  for (int i = threadIdx.x; i < n; i += kBlk) {
-    const int64_t a = fixed[i] ? cap[i] : (int64_t)floor(quota[i]);
+  for (int i = lane; i < n; i += 64) {
+    const double fl = floor(quota[i]);
+    const int64_t a = fixed[i] ? cap[i] : (int64_t)fl;
     alloc[i] = a;
     used += (double)a;
+    quota[i] = fixed[i] ? -1.0 : quota[i] - fl;  // fractional part; fixed items take no leftover unit
   }
-  used = block_sum(used, sh);
+  used = wave_sum(used);
   const int64_t left = total - (int64_t)used;
-  for (int i = threadIdx.x; i < n; i += kBlk) {
-    if (fixed[i]) continue;
-    const double fi = quota[i] - floor(quota[i]);
+  if (left <= 0) return;
+  wave_sync();
+  for (int i = lane; i < n; i += 64) {
+    const double fi = quota[i];
+    if (fi < 0.0) continue;
     int64_t rank = 0;
     for (int j = 0; j < n; ++j) {
-      if (fixed[j] || j == i) continue;
-      const double fj = quota[j] - floor(quota[j]);
-      if (fj > fi || (fj == fi && j < i)) ++rank;
+      const double fj = quota[j];
+      rank += (fj > fi || (fj == fi && j < i)) ? 1 : 0;
     }
     if (rank < left) alloc[i] += 1;
   }
+}
+
+// Inclusive scan of one value per thread over a block of NT threads; sh
+// holds NT / 64 words and `total` receives the block's sum.
+template <int NT>
+__device__ __forceinline__ uint32_t block_scan_u32(uint32_t v, uint32_t* sh, uint32_t& total) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int off = 1; off < 64; off <<= 1) {
+    const uint32_t o = __shfl_up(v, off);
+    if (lane >= off) v += o;
+  }
+  if (lane == 63) sh[wave] = v;
   __syncthreads();
+  uint32_t base = 0;
+  total = 0;
+#pragma unroll
+  for (int w = 0; w < NT / 64; ++w) {
+    const uint32_t x = sh[w];
+    if (w < wave) base += x;
+    total += x;
+  }
+  __syncthreads();
+  return v + base;
 }
 
 // ---------------------------------------------------------------------------
-// Per-clip plan: scores, segments and budgets.  Scratch arrays hold
-// (sum F + n_clips) entries; clip c uses the F_c + 1 entries starting at
-// frame_off + c.
+// Per-clip plan: scores, segments and budgets, one 1024-thread workgroup per
+// clip.  Its per-frame arrays (F + 1 entries each) sit in LDS for clips of
+// fewer than kPlanLds frames; longer clips use the global scratch, which
+// holds (sum F + n_clips) entries per array, clip c at frame_off + c.  The
+// code reaches both through the same generic pointers.
 // ---------------------------------------------------------------------------
+constexpr int kPlanBlk = 1024;
+constexpr int kPlanLds = 1024;
+
 struct PlanScratch {
   double *d, *alpha, *cont, *smooth, *rel, *score, *g, *quota, *fquota;
   int64_t *cap, *alloc, *fcap, *falloc;
   int32_t *fixed, *ffixed, *start;
 };
 
-__global__ __launch_bounds__(kBlk) void k_plan(ClipDev* __restrict__ clips, DynParamsDev prm,
-                                               const double* __restrict__ cka, const double* __restrict__ band_v,
-                                               const double* __restrict__ vq, const double* __restrict__ qq,
-                                               const double* __restrict__ nv, const uint32_t* __restrict__ maxkey,
-                                               FramePlanDev* __restrict__ plan, PlanScratch scr,
-                                               float* __restrict__ frame_score, int32_t* __restrict__ frame_budget,
-                                               int32_t* __restrict__ segment_id) {
-  __shared__ double sh[kBlk / 64];
-  __shared__ int n_seg_sh;
+// Nine fp64, four int64 and three int32 arrays of n entries each, in that
+// order, starting `o` entries into each.
+__device__ __forceinline__ PlanScratch carve_plan(double* b, int64_t n, int64_t o) {
+  int64_t* ib = reinterpret_cast<int64_t*>(b + 9 * n);
+  int32_t* jb = reinterpret_cast<int32_t*>(ib + 4 * n);
+  PlanScratch s;
+  s.d = b + o; s.alpha = b + n + o; s.cont = b + 2 * n + o; s.smooth = b + 3 * n + o; s.rel = b + 4 * n + o;
+  s.score = b + 5 * n + o; s.g = b + 6 * n + o; s.quota = b + 7 * n + o; s.fquota = b + 8 * n + o;
+  s.cap = ib + o; s.alloc = ib + n + o; s.fcap = ib + 2 * n + o; s.falloc = ib + 3 * n + o;
+  s.fixed = jb + o; s.ffixed = jb + n + o; s.start = jb + 2 * n + o;
+  return s;
+}
+constexpr int kPlanLdsBytes = kPlanLds * (9 * 8 + 4 * 8 + 3 * 4);
+
+__global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, DynParamsDev prm,
+                                                   const double* __restrict__ cka, const double* __restrict__ band_v,
+                                                   const double* __restrict__ vq, const double* __restrict__ qq,
+                                                   const double* __restrict__ nv, const uint32_t* __restrict__ maxkey,
+                                                   FramePlanDev* __restrict__ plan, double* scratch,
+                                                   int64_t scratch_n, float* __restrict__ frame_score,
+                                                   int32_t* __restrict__ frame_budget,
+                                                   int32_t* __restrict__ segment_id) {
+  __shared__ double sh[kPlanBlk / 64];
+  __shared__ uint32_t shu[kPlanBlk / 64];
+  __shared__ __align__(16) double lds[kPlanLdsBytes / 8];
   ClipDev* cp = &clips[blockIdx.x];
   const ClipDev c = *cp;
   const int F = c.n_frames, P = c.per_frame;
   if (F == 0) return;
   const int64_t f0 = c.frame_off;
-  const int64_t o = f0 + blockIdx.x;
-  double* d = scr.d + o;
-  double* alpha = scr.alpha + o;
-  double* cont = scr.cont + o;
-  double* smooth = scr.smooth + o;
-  double* rel = scr.rel + o;
-  double* score = scr.score + o;
-  double* g = scr.g + o;
-  double* quota = scr.quota + o;
-  double* fquota = scr.fquota + o;
-  int64_t* cap = scr.cap + o;
-  int64_t* alloc = scr.alloc + o;
-  int64_t* fcap = scr.fcap + o;
-  int64_t* falloc = scr.falloc + o;
-  int32_t* fixed = scr.fixed + o;
-  int32_t* ffixed = scr.ffixed + o;
-  int32_t* start = scr.start + o;
+  const int tid = threadIdx.x;
+  const PlanScratch w = F + 1 <= kPlanLds ? carve_plan(lds, kPlanLds, 0)
+                                          : carve_plan(scratch, scratch_n, f0 + blockIdx.x);
+  double *d = w.d, *alpha = w.alpha, *cont = w.cont, *smooth = w.smooth, *rel = w.rel, *score = w.score;
+  double *g = w.g, *quota = w.quota, *fquota = w.fquota;
+  int64_t *cap = w.cap, *alloc = w.alloc, *fcap = w.fcap, *falloc = w.falloc;
+  int32_t *fixed = w.fixed, *ffixed = w.ffixed, *start = w.start;
 
-  // Direct distance and the Eq. 2 blend.
+  // Direct distance (eight threads per frame) and the Eq. 2 blend.
   if (c.gate) {
-    double lo = INFINITY, hi = -INFINITY;
-    for (int f = threadIdx.x; f < F; f += kBlk) {
+    const int sub = tid & 7;
+    for (int f = tid >> 3; f < F; f += kPlanBlk / 8) {  // the eight threads of a frame share the trip count
+      const int64_t row0 = c.vis_off + (int64_t)f * P;
       double sm = 0.0;
-      for (int p = 0; p < P; ++p) {
-        const int64_t row = c.vis_off + (int64_t)f * P + p;
-        const double nn = nv[row];
-        sm += nn > 0.0 ? (double)key_value(maxkey[row]) * (1.0 / sqrt(nn)) : 0.0;
+#pragma unroll 6
+      for (int p = sub; p < P; p += 8) {
+        const double nn = nv[row0 + p];
+        sm += nn > 0.0 ? (double)key_value(maxkey[row0 + p]) * (1.0 / sqrt(nn)) : 0.0;
       }
-      const double df = 1.0 - sm / P;
-      d[f] = df;
-      lo = fmin(lo, df);
-      hi = fmax(hi, df);
+      sm += __shfl_xor(sm, 1);
+      sm += __shfl_xor(sm, 2);
+      sm += __shfl_xor(sm, 4);
+      if (sub == 0) {
+        const double df = 1.0 - sm / P;
+        d[f] = df;
+        plan[f0 + f].dist = df;
+      }
     }
-    lo = block_min(lo, sh);
-    hi = block_max(hi, sh);
-    for (int f = threadIdx.x; f < F; f += kBlk) {
+    __syncthreads();
+    double lo = INFINITY, hi = -INFINITY;
+    for (int f = tid; f < F; f += kPlanBlk) {
+      lo = fmin(lo, d[f]);
+      hi = fmax(hi, d[f]);
+    }
+    lo = block_min<kPlanBlk>(lo, sh);
+    hi = block_max<kPlanBlk>(hi, sh);
+    for (int f = tid; f < F; f += kPlanBlk) {
       const double dh = hi == lo ? 0.0 : (d[f] - lo) / (hi - lo);
       alpha[f] = (1.0 - prm.beta) * cka[f0 + f] + prm.beta * (1.0 - dh);
-      plan[f0 + f].dist = d[f];
     }
   } else {
-    for (int f = threadIdx.x; f < F; f += kBlk) {
+    for (int f = tid; f < F; f += kPlanBlk) {
       alpha[f] = cka[f0 + f];
       plan[f0 + f].dist = 0.0;
     }
@@ -567,7 +624,7 @@ __global__ __launch_bounds__(kBlk) void k_plan(ClipDev* __restrict__ clips, DynP
   // Continuity cs_f = cos(v_f, v_{f+1}), its Gaussian smoothing (half-sample
   // symmetric ends, truncated at 4 sigma) and the relevance r_f.
   const double qn = sqrt(qq[blockIdx.x]);
-  for (int f = threadIdx.x; f < F; f += kBlk) {
+  for (int f = tid; f < F; f += kPlanBlk) {
     const double nx = sqrt(band_v[(f0 + f) * kMaxWindow]);
     if (f + 1 < F) {
       const double ny = sqrt(band_v[(f0 + f + 1) * kMaxWindow]);
@@ -579,7 +636,7 @@ __global__ __launch_bounds__(kBlk) void k_plan(ClipDev* __restrict__ clips, DynP
   __syncthreads();
   const int n = F - 1;
   const int radius = (int)(4.0 * prm.sigma + 0.5);
-  for (int i = threadIdx.x; i < n; i += kBlk) {
+  for (int i = tid; i < n; i += kPlanBlk) {
     double wsum = 0.0;
     for (int k = -radius; k <= radius; ++k) wsum += exp(-0.5 * ((k / prm.sigma) * (k / prm.sigma)));
     double acc = 0.0;
@@ -593,32 +650,35 @@ __global__ __launch_bounds__(kBlk) void k_plan(ClipDev* __restrict__ clips, DynP
     smooth[i] = acc;
   }
   __syncthreads();
-  // Cuts: one per maximal run below tau_sim, after the run's minimum.
-  if (threadIdx.x == 0) {
-    int ns = 0;
-    start[ns++] = 0;
-    int f = 0;
-    while (f < n) {
-      if (smooth[f] < prm.tau_sim) {
-        int e = f, best = f;
-        while (e + 1 < n && smooth[e + 1] < prm.tau_sim) {
-          ++e;
-          if (smooth[e] < smooth[best]) best = e;
-        }
-        start[ns++] = best + 1;
-        f = e + 1;
-      } else {
-        ++f;
+  // Cuts: one per maximal run of the smoothed continuity below tau_sim,
+  // after the run's first minimum.  The thread at a run's first frame walks
+  // the run; a block scan places the cuts in frame order.
+  int n_seg = 1;
+  for (int c0 = 0; c0 < n; c0 += kPlanBlk) {
+    const int f = c0 + tid;
+    const bool run_start = f < n && smooth[f] < prm.tau_sim && (f == 0 || !(smooth[f - 1] < prm.tau_sim));
+    int cut = 0;
+    if (run_start) {
+      int e = f, best = f;
+      while (e + 1 < n && smooth[e + 1] < prm.tau_sim) {
+        ++e;
+        if (smooth[e] < smooth[best]) best = e;
       }
+      cut = best + 1;
     }
-    start[ns] = F;
-    n_seg_sh = ns;
-    cp->n_seg = ns;
+    uint32_t total;
+    const uint32_t incl = block_scan_u32<kPlanBlk>(run_start ? 1u : 0u, shu, total);
+    if (run_start) start[n_seg + (int)incl - 1] = cut;
+    n_seg += (int)total;
+  }
+  if (tid == 0) {
+    start[0] = 0;
+    start[n_seg] = F;
+    cp->n_seg = n_seg;
   }
   __syncthreads();
-  const int n_seg = n_seg_sh;
   // Segment scores g_m (Eq. 3) and caps |G_m| P.
-  for (int m = threadIdx.x; m < n_seg; m += kBlk) {
+  for (int m = tid; m < n_seg; m += kPlanBlk) {
     const int b = start[m], e = start[m + 1];
     double mx = -INFINITY, sm = 0.0;
     for (int f = b; f < e; ++f) {
@@ -631,43 +691,52 @@ __global__ __launch_bounds__(kBlk) void k_plan(ClipDev* __restrict__ clips, DynP
   }
   __syncthreads();
   double gmax = -INFINITY;
-  for (int m = threadIdx.x; m < n_seg; m += kBlk) gmax = fmax(gmax, g[m]);
-  gmax = block_max(gmax, sh);
-  // Frame scores s_f = gamma u_f + (1 - gamma) alpha_f with u_f = g_m / max g.
-  for (int m = threadIdx.x; m < n_seg; m += kBlk) {
-    const int b = start[m], e = start[m + 1];
-    const double u = g[m] / gmax;
-    for (int f = b; f < e; ++f) {
-      const double sv = prm.gamma * u + (1.0 - prm.gamma) * alpha[f];
-      score[f] = sv;
-      plan[f0 + f].score = sv;
-      plan[f0 + f].seg = m;
-      plan[f0 + f].anchor = b;
-      plan[f0 + f].is_anchor = f == b ? 1 : 0;
-      if (frame_score) frame_score[f0 + f] = (float)sv;
-      if (segment_id) segment_id[f0 + f] = m;
+  for (int m = tid; m < n_seg; m += kPlanBlk) gmax = fmax(gmax, g[m]);
+  gmax = block_max<kPlanBlk>(gmax, sh);
+  // Frame scores s_f = gamma u_f + (1 - gamma) alpha_f with u_f = g_m / max g;
+  // frame f lies in the last segment m with start[m] <= f.
+  for (int f = tid; f < F; f += kPlanBlk) {
+    int lo = 0, hi = n_seg - 1;
+    while (lo < hi) {
+      const int mid = (lo + hi + 1) >> 1;
+      if (start[mid] <= f) lo = mid;
+      else hi = mid - 1;
     }
+    const int m = lo, b = start[m];
+    const double sv = prm.gamma * (g[m] / gmax) + (1.0 - prm.gamma) * alpha[f];
+    score[f] = sv;
+    plan[f0 + f].score = sv;
+    plan[f0 + f].seg = m;
+    plan[f0 + f].anchor = b;
+    plan[f0 + f].is_anchor = f == b ? 1 : 0;
+    if (frame_score) frame_score[f0 + f] = (float)sv;
+    if (segment_id) segment_id[f0 + f] = m;
+  }
+  // Segment budgets (Eq. 4), capped at |G_m| P, by wave 0; then frame
+  // budgets within each segment by s_f, capped at P, one wave per segment
+  // (a segment's entries of the per-frame arrays are its own frames').
+  if (tid < 64) apportion_wave(c.budget, n_seg, g, cap, fixed, quota, alloc);
+  __syncthreads();
+  const int wave = tid >> 6, lane = tid & 63;
+  for (int m = wave; m < n_seg; m += kPlanBlk / 64) {
+    const int b = start[m], e = start[m + 1];
+    for (int i = lane; i < e - b; i += 64) fcap[b + i] = P;
+    apportion_wave(alloc[m], e - b, score + b, fcap + b, ffixed + b, fquota + b, falloc + b);
+    for (int i = lane; i < e - b; i += 64) plan[f0 + b + i].budget = (int32_t)falloc[b + i];
   }
   __syncthreads();
-  // Segment budgets (Eq. 4), capped at |G_m| P; then frame budgets within
-  // each segment by s_f, capped at P.
-  apportion(c.budget, n_seg, g, cap, fixed, quota, alloc, sh);
-  for (int m = 0; m < n_seg; ++m) {
-    const int b = start[m], e = start[m + 1];
-    for (int i = threadIdx.x; i < e - b; i += kBlk) fcap[i] = P;
-    __syncthreads();
-    apportion(alloc[m], e - b, score + b, fcap, ffixed, fquota, falloc, sh);
-    for (int i = threadIdx.x; i < e - b; i += kBlk) plan[f0 + b + i].budget = (int32_t)falloc[i];
-    __syncthreads();
-  }
   // Output offsets: exclusive prefix of k_f over the clip's frames.
-  if (threadIdx.x == 0) {
-    int64_t off = c.kept_off;
-    for (int f = 0; f < F; ++f) {
-      plan[f0 + f].out_off = off;
-      off += plan[f0 + f].budget;
-      if (frame_budget) frame_budget[f0 + f] = plan[f0 + f].budget;
+  int64_t base = c.kept_off;
+  for (int c0 = 0; c0 < F; c0 += kPlanBlk) {
+    const int f = c0 + tid;
+    const uint32_t k = f < F ? (uint32_t)falloc[f] : 0u;
+    uint32_t total;
+    const uint32_t incl = block_scan_u32<kPlanBlk>(k, shu, total);
+    if (f < F) {
+      plan[f0 + f].out_off = base + (int64_t)(incl - k);
+      if (frame_budget) frame_budget[f0 + f] = (int32_t)k;
     }
+    base += total;
   }
 }
 
@@ -1149,19 +1218,9 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
       if ((st = launch_status("k_gate_gemm")) != APACK_OK) return st;
     }
   }
-  PlanScratch scr;
-  {
-    const int64_t n = pl.total_frames + nc;
-    double* b = dp.scratch;
-    scr.d = b; scr.alpha = b + n; scr.cont = b + 2 * n; scr.smooth = b + 3 * n; scr.rel = b + 4 * n;
-    scr.score = b + 5 * n; scr.g = b + 6 * n; scr.quota = b + 7 * n; scr.fquota = b + 8 * n;
-    int64_t* ib = reinterpret_cast<int64_t*>(b + 9 * n);
-    scr.cap = ib; scr.alloc = ib + n; scr.fcap = ib + 2 * n; scr.falloc = ib + 3 * n;
-    int32_t* jb = reinterpret_cast<int32_t*>(ib + 4 * n);
-    scr.fixed = jb; scr.ffixed = jb + n; scr.start = jb + 2 * n;
-  }
-  hipLaunchKernelGGL(k_plan, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm, dp.cka, dp.band_v, dp.vq, dp.qq, dp.nv,
-                     dp.maxkey, dp.plan, scr, frame_score, frame_budget, segment_id);
+  hipLaunchKernelGGL(k_plan, dim3(nc), dim3(kPlanBlk), 0, s, dp.clips, prm, dp.cka, dp.band_v, dp.vq, dp.qq, dp.nv,
+                     dp.maxkey, dp.plan, dp.scratch, (int64_t)(pl.total_frames + nc), frame_score, frame_budget,
+                     segment_id);
   if ((st = launch_status("k_plan")) != APACK_OK) return st;
   if (nf > 0) {
     const int nt = (pl.max_per_frame + kGramTile - 1) / kGramTile;

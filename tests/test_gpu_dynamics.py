@@ -132,6 +132,20 @@ def test_ragged_batch_of_clips_with_edge_shapes():
     _compare(case, _run(case), want)
 
 
+def test_long_clips_on_both_plan_paths():
+    """The per-clip plan keeps its per-frame arrays in LDS up to 1023 frames
+    and in global memory past that: one clip at the LDS limit, one past it
+    (112 segments, the gate fired)."""
+    parts = [
+        W.dynamics_small("shared", seed=42, frames=1023, per_frame=3, audio=2046),
+        W.dynamics_small("offset", seed=43, frames=1500, per_frame=8, audio=3000),
+    ]
+    case = _packed(parts, {"window": 3, "r_pre": 0.5})
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
 @pytest.mark.parametrize("r_pre", [1.0, 0.05, 0.6])
 def test_budget_extremes(r_pre):
     case = W.dynamics_small("offset", seed=31)

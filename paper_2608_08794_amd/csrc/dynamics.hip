@@ -563,8 +563,9 @@ __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, 
                                                    const double* __restrict__ cka, const double* __restrict__ band_v,
                                                    const double* __restrict__ vq, const double* __restrict__ qq,
                                                    const double* __restrict__ nv, const uint32_t* __restrict__ maxkey,
-                                                   FramePlanDev* __restrict__ plan, double* scratch,
-                                                   int64_t scratch_n, float* __restrict__ frame_score,
+                                                   FramePlanDev* __restrict__ plan, int32_t* __restrict__ anchors,
+                                                   double* scratch, int64_t scratch_n,
+                                                   float* __restrict__ frame_score,
                                                    int32_t* __restrict__ frame_budget,
                                                    int32_t* __restrict__ segment_id) {
   __shared__ double sh[kPlanBlk / 64];
@@ -677,6 +678,7 @@ __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, 
     cp->n_seg = n_seg;
   }
   __syncthreads();
+  for (int m = tid; m < n_seg; m += kPlanBlk) anchors[f0 + m] = start[m];
   // Segment scores g_m (Eq. 3) and caps |G_m| P.
   for (int m = tid; m < n_seg; m += kPlanBlk) {
     const int b = start[m], e = start[m + 1];
@@ -742,8 +744,11 @@ __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, 
 
 // ---------------------------------------------------------------------------
 // Cosine Gram of an anchor frame's P tokens in fp64 on the matrix cores
-// (v_mfma_f64_16x16x4f64).  One wave per 16 x 16 tile of the upper triangle;
-// each tile is written twice, (i, j) and (j, i), so S is exactly symmetric.
+// (v_mfma_f64_16x16x4f64).  One workgroup per 16 x 16 tile of the upper
+// triangle of an anchor frame, looping over the batch's (anchor, tile)
+// items; its kGramSplit waves take contiguous slices of the embedding and
+// add their partial tiles in wave order through LDS.  Each tile is written
+// twice, (i, j) and (j, i), so S is exactly symmetric.
 // MFMA operands: lane l supplies A[l % 16][k = l / 16] and B[k = l / 16][l % 16];
 // accumulator element e of lane l is D[4e + l / 16][l % 16].  Each lane
 // loads 8 consecutive elements of its row and feeds them to 8 MFMAs, lane
@@ -752,59 +757,154 @@ __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, 
 // ---------------------------------------------------------------------------
 typedef double f64x4 __attribute__((ext_vector_type(4)));
 constexpr int kGramTile = 16;
-constexpr int kGramWaves = 4;  // tiles per workgroup
+constexpr int kGramWaves = 4;  // tiles per workgroup of the spatial Gram
+constexpr int kGramSplit = 8;  // K slices (waves) per workgroup of the anchor Gram
+constexpr int kGramBlocks = 512;  // workgroups of the anchor Gram at most: two per CU
+constexpr int kGramAhead = 4;  // K steps in flight per wave
+
+// Eight consecutive input elements held as loaded, widened to fp64 on use.
+template <class T>
+struct Raw8;
+template <>
+struct Raw8<bf16_t> {
+  uint4 u;
+  // Always loads (from the row's last 8 elements when k is past dim - 8), so
+  // the loads carry no branch; get() zeroes a step past the limit.
+  __device__ __forceinline__ void load(const bf16_t* row, int k, int dim) {
+    u = *reinterpret_cast<const uint4*>(row + min(k, dim - 8));
+  }
+  __device__ __forceinline__ void get(double (&o)[8], bool valid) const {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = valid ? (double)__uint_as_float(w[i] << 16) : 0.0;
+      o[2 * i + 1] = valid ? (double)__uint_as_float(w[i] & 0xFFFF0000u) : 0.0;
+    }
+  }
+};
+template <>
+struct Raw8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* row, int k, int dim) {
+    const float4* p = reinterpret_cast<const float4*>(row + min(k, dim - 8));
+    a = p[0];
+    b = p[1];
+  }
+  __device__ __forceinline__ void get(double (&o)[8], bool valid) const {
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = valid ? (double)v[e] : 0.0;
+  }
+};
 
 template <class T>
-__global__ __launch_bounds__(kGramWaves * 64) void k_gram(const ClipDev* __restrict__ clips,
-                                                          const FrameDev* __restrict__ frames,
+__global__ __launch_bounds__(kGramSplit * 64) void k_gram(const ClipDev* __restrict__ clips, int n_clips,
+                                                          const int32_t* __restrict__ anchors,
                                                           const FramePlanDev* __restrict__ plan, int dim,
                                                           const T* __restrict__ xv, const double* __restrict__ nv,
                                                           double* __restrict__ gram) {
-  const FrameDev fr = frames[blockIdx.x];
-  const ClipDev c = clips[fr.clip];
-  const int64_t frame = c.frame_off + fr.f;
-  const FramePlanDev fp = plan[frame];
-  if (!fp.is_anchor || fp.budget == 0) return;
-  const int P = c.per_frame;
-  const int nt = (P + kGramTile - 1) / kGramTile;
-  int t = blockIdx.y * kGramWaves + (threadIdx.x >> 6);
-  if (t >= nt * (nt + 1) / 2) return;
-  int ti = 0;
-  while (t >= nt - ti) {  // row-major upper triangle: tile (ti, tj), tj >= ti
-    t -= nt - ti;
-    ++ti;
-  }
-  const int tj = ti + t;
-  const int lane = threadIdx.x & 63, g = lane >> 4, r16 = lane & 15;
-  const int64_t row0 = c.vis_off + (int64_t)fr.f * P;
-  const int ra = min(ti * kGramTile + r16, P - 1), rb = min(tj * kGramTile + r16, P - 1);
-  const T* xa = xv + (row0 + ra) * dim;
-  const T* xb = xv + (row0 + rb) * dim;
-  f64x4 acc = {0.0, 0.0, 0.0, 0.0};
-  for (int k0 = 0; k0 < dim; k0 += 32) {
-    const int kk = k0 + 8 * g;
-    double a[8], b[8];
-    if (kk < dim) {
-      load8(xa + kk, a);
-      load8(xb + kk, b);
-    } else {
-#pragma unroll
-      for (int e = 0; e < 8; ++e) a[e] = b[e] = 0.0;
+  __shared__ double red[kGramSplit - 1][4 * 64];
+  const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, r16 = lane & 15;
+  // This wave's K slice, in 32-element steps.
+  const int nsteps = (dim + 31) / 32;
+  const int per = (nsteps + kGramSplit - 1) / kGramSplit;
+  const int s_begin = min(nsteps, wave * per), s_end = min(nsteps, s_begin + per);
+  const int lim = min(dim, 32 * s_end);
+  // Anchors go to XCDs round-robin (workgroup b runs on XCD b % 8), so an
+  // anchor's rows are fetched into one L2; the XCD's slots share its
+  // anchors' tiles in turn.  Every workgroup walks the same anchor sequence.
+  const int xcd = blockIdx.x & 7, slot = blockIdx.x >> 3, nslot = gridDim.x >> 3;
+  int c = 0;
+  int64_t seg_before = 0;  // anchors of clips [0, c)
+  int64_t jbase = 0;       // tiles of this XCD's earlier anchors
+  for (int64_t an = xcd;; an += 8) {
+    while (c < n_clips) {
+      const int64_t ns = clips[c].n_frames > 0 ? clips[c].n_seg : 0;
+      if (an < seg_before + ns) break;
+      seg_before += ns;
+      ++c;
     }
+    if (c >= n_clips) return;
+    const ClipDev cc = clips[c];
+    const int P = cc.per_frame, nt = (P + kGramTile - 1) / kGramTile, tiles = nt * (nt + 1) / 2;
+    const int f = anchors[cc.frame_off + (an - seg_before)];
+    const int64_t j0 = jbase + ((slot - jbase % nslot) % nslot + nslot) % nslot;
+    const int64_t jend = jbase + tiles;
+    jbase = jend;
+    if (plan[cc.frame_off + f].budget == 0) continue;  // the same for the whole workgroup
+    for (int64_t jj = j0; jj < jend; jj += nslot) {
+      int t = (int)(jj - (jend - tiles)), ti = 0;
+      while (t >= nt - ti) {  // row-major upper triangle: tile (ti, tj), tj >= ti
+        t -= nt - ti;
+        ++ti;
+      }
+      const int tj = ti + t;
+      const int64_t row0 = cc.vis_off + (int64_t)f * P;
+      const int ra = min(ti * kGramTile + r16, P - 1), rb = min(tj * kGramTile + r16, P - 1);
+      const T* xa = xv + (row0 + ra) * dim;
+      const T* xb = xv + (row0 + rb) * dim;
+      // kGramAhead steps loaded ahead of the MFMAs (the next group's loads
+      // are issued before this group's MFMAs); steps past the slice add
+      // zero products.
+      Raw8<T> pa[kGramAhead], pb[kGramAhead];
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a[e], b[e], acc, 0, 0, 0);
-  }
-  double* G = gram + c.gram_off + (int64_t)fr.f * P * P;
-  const int col = tj * kGramTile + r16;
-  const double nc = col < P ? sqrt(nv[row0 + col]) : 0.0;
+      for (int u = 0; u < kGramAhead; ++u) {
+        const int kk = 32 * (s_begin + u) + 8 * g;
+        pa[u].load(xa, kk, dim);
+        pb[u].load(xb, kk, dim);
+      }
+      f64x4 acc = {0.0, 0.0, 0.0, 0.0};
+      for (int s0 = s_begin; s0 < s_end; s0 += kGramAhead) {
+        Raw8<T> qa[kGramAhead], qb[kGramAhead];
 #pragma unroll
-  for (int e = 0; e < 4; ++e) {
-    const int row = ti * kGramTile + 4 * e + g;
-    if (row >= P || col >= P) continue;
-    const double nr = sqrt(nv[row0 + row]);
-    const double v = (nr == 0.0 || nc == 0.0) ? 0.0 : acc[e] / (nr * nc);
-    G[(int64_t)row * P + col] = v;
-    G[(int64_t)col * P + row] = v;
+        for (int u = 0; u < kGramAhead; ++u) {
+          const int kk = 32 * (s0 + kGramAhead + u) + 8 * g;
+          qa[u].load(xa, kk, dim);
+          qb[u].load(xb, kk, dim);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kGramAhead; ++u) {
+          const bool valid = 32 * (s0 + u) + 8 * g < lim;
+          double a[8], b[8];
+          pa[u].get(a, valid);
+          pb[u].get(b, valid);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc = __builtin_amdgcn_mfma_f64_16x16x4f64(a[e], b[e], acc, 0, 0, 0);
+        }
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int u = 0; u < kGramAhead; ++u) {
+          pa[u] = qa[u];
+          pb[u] = qb[u];
+        }
+      }
+      // Partial tiles added in wave order.
+      if (wave > 0) {
+#pragma unroll
+        for (int e = 0; e < 4; ++e) red[wave - 1][e * 64 + lane] = acc[e];
+      }
+      __syncthreads();
+      if (wave == 0) {
+#pragma unroll
+        for (int q = 0; q < kGramSplit - 1; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) acc[e] += red[q][e * 64 + lane];
+        double* G = gram + cc.gram_off + (int64_t)f * P * P;
+        const int col = tj * kGramTile + r16;
+        const double nc = col < P ? sqrt(nv[row0 + col]) : 0.0;
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          const int row = ti * kGramTile + 4 * e + g;
+          if (row >= P || col >= P) continue;
+          const double nr = sqrt(nv[row0 + row]);
+          const double v = (nr == 0.0 || nc == 0.0) ? 0.0 : acc[e] / (nr * nc);
+          G[(int64_t)row * P + col] = v;
+          G[(int64_t)col * P + row] = v;
+        }
+      }
+      __syncthreads();
+    }
   }
 }
 
@@ -1219,14 +1319,16 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
     }
   }
   hipLaunchKernelGGL(k_plan, dim3(nc), dim3(kPlanBlk), 0, s, dp.clips, prm, dp.cka, dp.band_v, dp.vq, dp.qq, dp.nv,
-                     dp.maxkey, dp.plan, dp.scratch, (int64_t)(pl.total_frames + nc), frame_score, frame_budget,
+                     dp.maxkey, dp.plan, dp.anchors, dp.scratch, (int64_t)(pl.total_frames + nc), frame_score,
+                     frame_budget,
                      segment_id);
   if ((st = launch_status("k_plan")) != APACK_OK) return st;
   if (nf > 0) {
-    const int nt = (pl.max_per_frame + kGramTile - 1) / kGramTile;
-    const unsigned gy = (unsigned)((nt * (nt + 1) / 2 + kGramWaves - 1) / kGramWaves);
-    hipLaunchKernelGGL(k_gram<T>, dim3(nf, gy), dim3(kGramWaves * 64), 0, s, dp.clips, dp.frames, dp.plan, dim, xv,
-                       dp.nv, dp.gram);
+    if (pl.gram_items > 0) {
+      const unsigned gb = (unsigned)std::min<int64_t>((pl.gram_items + 7) / 8 * 8, kGramBlocks);
+      hipLaunchKernelGGL(k_gram<T>, dim3(gb), dim3(kGramSplit * 64), 0, s, dp.clips, nc, dp.anchors, dp.plan, dim,
+                         xv, dp.nv, dp.gram);
+    }
     if ((st = launch_status("k_gram")) != APACK_OK) return st;
     hipLaunchKernelGGL(k_dafps, dim3(nf), dim3(kMaxPerFrame), 0, s, dp.clips, dp.frames, dp.plan, prm, dp.gram, kept);
     if ((st = launch_status("k_dafps")) != APACK_OK) return st;

@@ -63,6 +63,8 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
     tokens += nv;
     kept += c.budget;
     gram += nv * a.tokens_per_frame;
+    const int64_t nt = (a.tokens_per_frame + 15) / 16;
+    pl.gram_items += (int64_t)a.n_frames * (nt * (nt + 1) / 2);
     vis_end = std::max(vis_end, a.vis_off + nv);
     aud_end = std::max(aud_end, a.aud_off + a.n_audio);
     pl.max_per_frame = std::max(pl.max_per_frame, a.tokens_per_frame);
@@ -141,6 +143,8 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
   c.take<double>(tokens);
   pl.off_spatial = c.used;
   c.take<double>((size_t)frames * pl.spatial_tiles * 3);
+  pl.off_anchors = c.used;
+  c.take<int32_t>(frames);
   pl.ws_bytes = std::max<size_t>(c.used, kAlign);
   pl.gemm = std::move(tiles);
   return APACK_OK;
@@ -252,6 +256,7 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   dp.scratch = reinterpret_cast<double*>(ws + pl.off_scratch);
   dp.spatial = reinterpret_cast<double*>(ws + pl.off_spatial);
   dp.sim = reinterpret_cast<double*>(ws + pl.off_sim);
+  dp.anchors = reinterpret_cast<int32_t*>(ws + pl.off_anchors);
   DynParamsDev prm;
   prm.tau_gate = p->tau_gate;
   prm.beta = p->beta;

@@ -54,7 +54,8 @@ struct DynPlan {
   size_t off_clips = 0, off_frames = 0, off_gemm = 0, blob_bytes = 0;
   size_t off_v = 0, off_a = 0, off_q = 0, off_band_v = 0, off_band_a = 0, off_vq = 0, off_qq = 0;
   size_t off_cka = 0, off_nv = 0, off_na = 0, off_maxkey = 0, off_plan = 0, off_gram = 0, off_scratch = 0;
-  size_t off_spatial = 0, off_sim = 0;
+  size_t off_spatial = 0, off_sim = 0, off_anchors = 0;
+  int64_t gram_items = 0;            // (frame, Gram tile) pairs over all clips: the anchor Gram's items at most
   size_t ws_bytes = 0;
 };
 
@@ -91,6 +92,7 @@ struct DynPtrs {
   double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *na, *gram, *scratch, *spatial, *sim;
   uint32_t* maxkey;
   FramePlanDev* plan;
+  int32_t* anchors;  // first frame of each segment, clip c's at frame_off + m
 };
 
 // The gate GEMM on 256 x 256 tiles for bf16 inputs whose dim is a multiple

@@ -6,7 +6,10 @@
 //   out[i] = in[src_rows[i]],  i < n_out.
 // Work items are 16 KB slabs (1024 units of 16 bytes, 4 per thread) so each
 // thread keeps four independent 16-byte loads in flight before its stores;
-// HBM-bound by design.  Rows whose index is outside [0, n_in) are skipped.
+// HBM-bound by design.  The source rows of a slab are read once into LDS
+// before its data loads: one index load per row rather than one per 16-byte
+// unit (a 256-byte K/V row spans 16 units).  Rows whose index is outside
+// [0, n_in) are skipped.
 #include <algorithm>
 #include <cstring>
 
@@ -30,6 +33,7 @@ struct GatherArgs {
   int64_t row_units;          // units per K/V row
   int64_t hs_in, hs_out;      // head strides in units
   int64_t kv_rows_per_item, kv_items_per_plane, kv_items;
+  int32_t row_magic, h_row_magic;   // div_magic(row_units), div_magic(h_row_units)
   // hidden
   const void* h_in;
   void* h_out;
@@ -43,35 +47,50 @@ struct GatherArgs {
   void* out[kMaxTensors];
 };
 
+// u / d for 0 <= u < 1024 and 1 <= d <= 1024 as (u * magic) >> 20 with
+// magic = ceil(2^20 / d): exact on that range (the product stays below 2^30).
+inline int32_t div_magic(int64_t d) { return (int32_t)(((int64_t(1) << 20) + d - 1) / d); }
+
+// rows * row_units <= kItemUnits, so rows <= kItemUnits and row_units <= kItemUnits.
+// Every thread of the workgroup calls this (it holds a barrier).  The four
+// index reads from LDS are issued together, then the four data loads.
 template <class U>
 __device__ __forceinline__ void copy_rows(const U* __restrict__ in, U* __restrict__ out,
-                                          const int32_t* __restrict__ src, int64_t r0, int64_t rows,
-                                          int64_t row_units, int64_t n_out, int64_t n_in) {
-  U v[kPerThread];
-  int64_t dst[kPerThread];
-  const int64_t units = rows * row_units;
+                                          const int32_t* __restrict__ src, int64_t r0, int rows,
+                                          int row_units, int magic, int64_t n_out, int64_t n_in,
+                                          int32_t* sidx) {
+  for (int i = threadIdx.x; i < rows; i += kThreads) {
+    const int64_t r = r0 + i;
+    int32_t s = -1;
+    if (r < n_out) {
+      s = src[r];
+      if (s < 0 || s >= n_in) s = -1;
+    }
+    sidx[i] = s;
+  }
+  __syncthreads();
+  const int units = rows * row_units;
+  int32_t s[kPerThread];
+  int rl[kPerThread], c[kPerThread];
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i) {
-    const int64_t u = threadIdx.x + (int64_t)i * kThreads;
-    dst[i] = -1;
-    if (u < units) {
-      const int64_t r = r0 + u / row_units, c = u % row_units;
-      if (r < n_out) {
-        const int64_t s = src[r];
-        if (s >= 0 && s < n_in) {
-          v[i] = __builtin_nontemporal_load(in + s * row_units + c);
-          dst[i] = r * row_units + c;
-        }
-      }
-    }
+    const int u = threadIdx.x + i * kThreads;
+    rl[i] = (u * magic) >> 20;
+    c[i] = u - rl[i] * row_units;
+    s[i] = u < units ? sidx[rl[i]] : -1;
   }
+  U v[kPerThread];
 #pragma unroll
   for (int i = 0; i < kPerThread; ++i)
-    if (dst[i] >= 0) __builtin_nontemporal_store(v[i], out + dst[i]);
+    if (s[i] >= 0) v[i] = __builtin_nontemporal_load(in + (int64_t)s[i] * row_units + c[i]);
+#pragma unroll
+  for (int i = 0; i < kPerThread; ++i)
+    if (s[i] >= 0) __builtin_nontemporal_store(v[i], out + (r0 + rl[i]) * row_units + c[i]);
 }
 
 template <class U>
 __global__ __launch_bounds__(kThreads) void k_gather(const GatherArgs a) {
+  __shared__ int32_t sidx[kItemUnits];
   int64_t item = blockIdx.x;
   if (item < a.kv_items) {
     const int64_t plane = item / a.kv_items_per_plane;
@@ -79,13 +98,14 @@ __global__ __launch_bounds__(kThreads) void k_gather(const GatherArgs a) {
     const int t = (int)(plane / a.heads), h = (int)(plane % a.heads);
     const U* in = static_cast<const U*>(a.in[t]) + h * a.hs_in;
     U* out = static_cast<U*>(a.out[t]) + h * a.hs_out;
-    copy_rows<U>(in, out, a.src, r0, a.kv_rows_per_item, a.row_units, a.n_out, a.n_in);
+    copy_rows<U>(in, out, a.src, r0, (int)a.kv_rows_per_item, (int)a.row_units, a.row_magic, a.n_out, a.n_in,
+                 sidx);
     return;
   }
   item -= a.kv_items;
   if (item < a.h_items) {
     copy_rows<U>(static_cast<const U*>(a.h_in), static_cast<U*>(a.h_out), a.src, item * a.h_rows_per_item,
-                 a.h_rows_per_item, a.h_row_units, a.n_out, a.n_in);
+                 (int)a.h_rows_per_item, (int)a.h_row_units, a.h_row_magic, a.n_out, a.n_in, sidx);
     return;
   }
   item -= a.h_items;
@@ -209,6 +229,7 @@ extern "C" apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows,
     a.hs_in = head_stride_in * (int64_t)es / ub;
     a.hs_out = head_stride_out * (int64_t)es / ub;
     a.kv_rows_per_item = std::max<int64_t>(1, kItemUnits / a.row_units);
+    a.row_magic = div_magic(a.row_units);
     a.kv_items_per_plane = (n_out + a.kv_rows_per_item - 1) / a.kv_rows_per_item;
     a.kv_items = a.kv_items_per_plane * a.n_tensors * hkv;
     for (int l = 0; l < n_layers; ++l) {
@@ -232,6 +253,7 @@ extern "C" apack_status apack_compact_kv(int64_t n_out, const int32_t* src_rows,
     APACK_CHECK(a.h_row_units <= kItemUnits, APACK_E_UNSUPPORTED, "hidden rows longer than %d bytes",
                 (int)(kItemUnits * ub));
     a.h_rows_per_item = std::max<int64_t>(1, kItemUnits / a.h_row_units);
+    a.h_row_magic = div_magic(a.h_row_units);
     a.h_items = (n_out + a.h_rows_per_item - 1) / a.h_rows_per_item;
   }
   if (has_p) {

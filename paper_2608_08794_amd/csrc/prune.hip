@@ -163,6 +163,14 @@ struct KFrags {
 
 __device__ __forceinline__ float fast_exp2(float x) { return __builtin_amdgcn_exp2f(x); }
 
+// v + (the value of the lane 32 away), added lower half first in every lane,
+// through v_permlane32_swap: no LDS round trip, so no LDS wait that would
+// also wait for the K-fragment reads in flight.
+__device__ __forceinline__ float add_halves(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // ---------------------------------------------------------------------------
 // Software pipeline of both passes.  Each wave issues the MFMAs of key
 // block b while its VALU works on the logits of block b-1, so the matrix
@@ -462,7 +470,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   };
   // Column sums of a finished key block into its tile's slot (lanes < 32).
   auto flush_block = [&](int slot, int blk) {
-    const float c = cs + __shfl_xor(cs, 32);
+    const float c = add_halves(cs);
     if (lane < 32) red[slot][wave][blk * 32 + lane] = c;
     cs = 0.f;
   };

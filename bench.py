@@ -141,23 +141,23 @@ def main():
     torch.cuda.synchronize()
     log(f"uploaded {sum(x.numel() * 2 for x in k_in + v_in) / 1e9:.2f} GB cache in {time.time() - t0:.1f}s")
 
+    # Per prune step two events: after its scores/select (= before its gather)
+    # and after its gather (= before the next prune).  Neighbouring phases share
+    # an event, so a step records 6 markers rather than 12.
     def events():
-        return [[torch.cuda.Event(enable_timing=True) for _ in range(4)] for _ in steps]
+        return [[torch.cuda.Event(enable_timing=True) for _ in range(2)] for _ in steps]
 
     def run_step(ev):
         kk, vv, hh, pp = k_in, v_in, h_in, p_in
         for i, st in enumerate(steps):
-            if ev:
-                ev[i][0].record()
             A.apack_prune_layer(queries[i], kk[st["layer"]], [st["seq"]], scores=st["scores"],
                                 kept_rows=st["kept"], workspace=st["ws"])
             if ev:
-                ev[i][1].record()
-                ev[i][2].record()
+                ev[i][0].record()
             A.apack_compact_kv(st["kept"], st["n_in"], kk, vv, st["k_out"], st["v_out"], hh, st["h_out"],
                                pp, st["p_out"])
             if ev:
-                ev[i][3].record()
+                ev[i][1].record()
             kk, vv, hh, pp = st["k_out"], st["v_out"], st["h_out"], st["p_out"]
 
     for _ in range(args.warmup):
@@ -178,8 +178,12 @@ def main():
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
-    prune_ms = [sum(ev[i][0].elapsed_time(ev[i][1]) for ev in step_events) for i in range(len(steps))]
-    gather_ms = [sum(ev[i][2].elapsed_time(ev[i][3]) for ev in step_events) for i in range(len(steps))]
+    # The scores/select phase of prune i runs from the previous gather's end
+    # (the step's start for the first prune) to the event after it.
+    prev = [start] + [ev[-1][1] for ev in step_events[:-1]]
+    prune_ms = [sum((p if i == 0 else ev[i - 1][1]).elapsed_time(ev[i][0]) for p, ev in zip(prev, step_events))
+                for i in range(len(steps))]
+    gather_ms = [sum(ev[i][0].elapsed_time(ev[i][1]) for ev in step_events) for i in range(len(steps))]
     log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
 
     # Throughput and algorithmic bytes.

@@ -362,7 +362,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
       const float ss = s_run[rb] * fast_exp2(m_run[rb] - mm) + so * fast_exp2(mo - mm);
       const int rho = row0 + rb * 32 + lane;
       if (lane < 32 && rho < rg_end)
-        st_agent(&stats[sq.stats_off + ((int64_t)tl.g * sq.rows_pad + rho) * sq.n_chunks + tl.chunk],
+        st_agent(&stats[sq.stats_off + ((int64_t)tl.g * sq.n_chunks + tl.chunk) * sq.rows_pad + rho],
                  make_float2(mm, ss));
     }
   }
@@ -374,13 +374,16 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   for (int rho = r_lo + tid; rho < r_lo + sq.rows_per_rg; rho += NW * kWave) {
     float m = -FLT_MAX, s = 0.f;
     if (rho < rows_g) {
-      const float2* p = stats + sq.stats_off + ((int64_t)tl.g * sq.rows_pad + rho) * sq.n_chunks;
-      // Loads in batches (all in flight together), merged in chunk order.
+      // Partials are [g][chunk][row]: a wave's loads of one chunk are
+      // contiguous.  Loads in batches (all in flight together), merged in
+      // chunk order.
+      const float2* p = stats + sq.stats_off + (int64_t)tl.g * sq.n_chunks * sq.rows_pad + rho;
       constexpr int CB = 16;
       for (int c0 = 0; c0 < sq.n_chunks; c0 += CB) {
         float2 v[CB];
 #pragma unroll
-        for (int i = 0; i < CB; ++i) v[i] = c0 + i < sq.n_chunks ? ld_agent(p + c0 + i) : make_float2(0.f, 0.f);
+        for (int i = 0; i < CB; ++i)
+          v[i] = c0 + i < sq.n_chunks ? ld_agent(p + (int64_t)(c0 + i) * sq.rows_pad) : make_float2(0.f, 0.f);
 #pragma unroll
         for (int i = 0; i < CB; ++i)
           if (c0 + i < sq.n_chunks) merge(m, s, v[i].x, v[i].y);

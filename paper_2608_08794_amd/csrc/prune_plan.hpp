@@ -32,7 +32,7 @@ struct SeqDev {
   int64_t out_off;      // first slot in kept_rows
   int64_t n_kept;       // kept rows of the sequence (bound on the scan's writes)
   int64_t tag_off;      // first byte of the sequence in the tag array
-  int64_t stats_off;    // first (max, sum) partial: [g][rows_pad][chunk]
+  int64_t stats_off;    // first (max, sum) partial: [g][chunk][rows_pad]
   int64_t bias_off;     // first b entry: [g][rows_pad], row rho = (h % n_rep)*q_len + t
   int64_t colpart_off;  // first per-group column partial: [g*n_rg + rg][n_tokens]
   int32_t q_len;

@@ -71,7 +71,10 @@ apack_status staging_acquire(size_t bytes, Staging** blk, void** host) {
     return fail(APACK_E_HIP, "hipHostMalloc(%zu): %s", bytes, hipGetErrorString(e));
   }
   e = hipHostGetDevicePointer(&s->mapped, s->host, 0);
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->done, hipEventDisableTiming);
+  // The event only tells the host that the upload kernel has finished reading
+  // the block; no device write has to become visible to the host, so it skips
+  // the system-scope release (an L2 writeback that stalled the stream ~5 us).
+  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->done, hipEventDisableTiming | hipEventDisableSystemFence);
   if (e != hipSuccess) {
     (void)hipHostFree(s->host);
     delete s;

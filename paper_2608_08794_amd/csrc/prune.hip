@@ -266,7 +266,9 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
   __shared__ __attribute__((aligned(16))) char lds[2][G::kTileBytes];
-  __shared__ __attribute__((aligned(16))) float lmask[2][kKeyTile];
+  // Accumulator start (0 or -inf) of every key of the chunk, built once
+  // before the loop so that no tile waits on a load of its tags.
+  __shared__ __attribute__((aligned(16))) float lmask[kMaxChunk];
 
   const TileDev tl = tiles[blockIdx.x];
   const SeqDev sq = seqs[tl.seq];
@@ -304,14 +306,31 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
     pend[rb] = neg_inf16();
   }
 
+  // Tags are read in batches of 8 per thread, all in flight together (the
+  // index is clamped to a valid row; rows past the chunk get -inf), before
+  // the first K tile is requested.
+  {
+    constexpr int kB = 8;
+    const int n_mask = n_tiles * kKeyTile;
+    for (int b0 = 0; b0 < n_mask; b0 += kB * NW * kWave) {
+      uint8_t t[kB];
+#pragma unroll
+      for (int j = 0; j < kB; ++j) {
+        const int64_t r = key_begin + b0 + tid + j * NW * kWave;
+        t[j] = tg[r < key_end ? r : key_end - 1];
+      }
+#pragma unroll
+      for (int j = 0; j < kB; ++j) {
+        const int i = b0 + tid + j * NW * kWave;
+        if (i < n_mask) lmask[i] = (key_begin + i < key_end && t[j] != 0) ? 0.0f : -INFINITY;
+      }
+    }
+  }
   if (n_tiles > 0) KTileLoad<T, D, NW>::issue(lds[0], kbase, key_begin, key_end, wave, lane);
   for (int it = 0; it < n_tiles; ++it) {
     const int buf = it & 1;
     const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
-    for (int i = tid; i < kKeyTile; i += NW * kWave) {
-      const bool cand = (t0 + i < key_end) && tg[t0 + i] != 0;
-      lmask[buf][i] = cand ? 0.0f : -INFINITY;
-    }
+    const float* lm = lmask + it * kKeyTile;
     wait_tile_loads();
     __syncthreads();
     if (it + 1 < n_tiles) KTileLoad<T, D, NW>::issue(lds[buf ^ 1], kbase, t0 + kKeyTile, key_end, wave, lane);
@@ -322,17 +341,17 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
       KFrags<T, D> kf[NB];
       f32x16 init[NB];
       kf[0].load(lds[buf], 0, lane);
-      init[0] = mask_init(lmask[buf], 0, lane);
+      init[0] = mask_init(lm, 0, lane);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
         const int c = kb % NB;
         if (NB == 1 && kb > 0) {
           kf[0].load(lds[buf], kb, lane);
-          init[0] = mask_init(lmask[buf], kb, lane);
+          init[0] = mask_init(lm, kb, lane);
         }
         if (NB == 2 && kb + 1 < NKB) {
           kf[(kb + 1) % NB].load(lds[buf], kb + 1, lane);
-          init[(kb + 1) % NB] = mask_init(lmask[buf], kb + 1, lane);
+          init[(kb + 1) % NB] = mask_init(lm, kb + 1, lane);
         }
         f32x16 cur[kRB];
 #pragma unroll
@@ -404,8 +423,14 @@ template <int NKB, int NW>
 __device__ __forceinline__ void col_flush(float (&red)[3][NW][NKB * 32], int slot, int n_active, int64_t tile0,
                                           int64_t key_end, float* out, int tid) {
   for (int i = tid; i < NKB * 32; i += NW * kWave) {
+    // All NW reads are issued before the fixed-order sum.
+    float r[NW];
+#pragma unroll
+    for (int w = 0; w < NW; ++w) r[w] = w < n_active ? red[slot][w][i] : 0.f;
     float v = 0.f;
-    for (int w = 0; w < n_active; ++w) v += red[slot][w][i];
+#pragma unroll
+    for (int w = 0; w < NW; ++w)
+      if (w < n_active) v += r[w];
     if (tile0 + i < key_end) st_agent(&out[tile0 + i], v);
   }
 }

@@ -121,7 +121,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     if (sd.n_cand == 0) continue;
     int64_t ch = (weighted + target - 1) / target;
     ch = (ch + kKeyTile - 1) / kKeyTile * kKeyTile;
-    ch = std::max<int64_t>(kKeyTile, std::min<int64_t>(ch, 4096));
+    ch = std::max<int64_t>(kKeyTile, std::min<int64_t>(ch, kMaxChunk));
     sd.chunk = (int32_t)ch;
     sd.n_chunks = (int32_t)((sd.n_tokens + ch - 1) / ch);
     sd.stats_off = stats;

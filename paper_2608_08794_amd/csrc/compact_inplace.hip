@@ -169,8 +169,10 @@ __device__ __forceinline__ bool unit_of(const InplaceArgs& a, const Slice<U>& g,
   return c < a.p_rows && r < a.n_out;
 }
 
+// sidx holds src of the rows of stripes sa, sa + 1, ... (kStripe each).
 template <class U>
-__device__ __forceinline__ void load_item(const InplaceArgs& a, int64_t item, ItemRegs<U>& q) {
+__device__ __forceinline__ void load_item(const InplaceArgs& a, int64_t item, const int32_t* sidx, int64_t sa,
+                                          ItemRegs<U>& q) {
   const int64_t s = item / a.items_per_stripe;
   const Slice<U> g = slice_of<U>(a, (int)(item % a.items_per_stripe));
   q.live = 0;
@@ -179,7 +181,7 @@ __device__ __forceinline__ void load_item(const InplaceArgs& a, int64_t item, It
     int64_t r;
     int c;
     if (!unit_of(a, g, s, i, r, c)) continue;
-    const int64_t sr = a.src[r];
+    const int64_t sr = sidx[(s - sa) * kStripe + (r - s * kStripe)];
     if (sr < 0 || sr >= a.n_in || sr == r) continue;   // nothing to move
     if (!g.pos) {
       q.v[i] = __builtin_nontemporal_load(g.base + sr * g.stride + g.c0 + c);
@@ -235,6 +237,7 @@ __device__ __forceinline__ void reader_stripes(const InplaceArgs& a, int64_t t, 
 template <class U>
 __global__ __launch_bounds__(kThreads) void k_compact_inplace(const InplaceArgs a) {
   __shared__ uint32_t sh_ticket;
+  __shared__ int32_t sidx[kGroup * kStripe];   // src of the ticket's output rows
   const int tid = threadIdx.x;
   int64_t waited = -1;  // latest stripe whose readers thread 0 has seen complete
   for (;;) {
@@ -250,11 +253,20 @@ __global__ __launch_bounds__(kThreads) void k_compact_inplace(const InplaceArgs 
     if (tid == 0)
 #pragma unroll
       for (int j = 0; j <= kGroup; ++j) fr[j] = t0 + j <= sb + 1 ? a.first_reader[t0 + j] : 0;
+    // The ticket's items lie in at most kGroup stripes; their source rows
+    // are read once into LDS (one index load per row, not one per unit).
+    // The previous ticket's reads of sidx ended before its count barrier.
+    const int64_t sa = i0 / a.items_per_stripe;
+    for (int j = tid; j < (int)(sb - sa + 1) * kStripe; j += kThreads) {
+      const int64_t r = sa * kStripe + j;
+      sidx[j] = r < a.n_out ? a.src[r] : -1;
+    }
+    __syncthreads();
     ItemRegs<U> q[kGroup];
 #pragma unroll
     for (int p = 0; p < kGroup; ++p) {
       q[p].live = 0;
-      if (i0 + p < i1) load_item<U>(a, i0 + p, q[p]);
+      if (i0 + p < i1) load_item<U>(a, i0 + p, sidx, sa, q[p]);
     }
     bool pending = false;
     if (tid == 0)

@@ -52,11 +52,15 @@ struct Carver {
 };
 
 // Pinned host staging for small descriptor uploads.  acquire() returns a
-// pinned block of at least `bytes`; upload() copies it to `dst` on `stream`
-// and marks the block busy until the copy has completed on the device.
+// pinned block of at least `bytes`; upload() copies it to `dst` on `stream`;
+// release() (called once the call's other launches are queued, whatever their
+// status) records the event that frees the block once the stream reaches it.
+// Recording after the launches keeps the event's packet from sitting between
+// the upload and the first kernel that reads the descriptors.
 struct Staging;
 apack_status staging_acquire(size_t bytes, Staging** blk, void** host);
 apack_status staging_upload(Staging* blk, void* dst, size_t bytes, hipStream_t stream);
+apack_status staging_release(Staging* blk, hipStream_t stream);
 
 // Byte ranges [a, a+na) and [b, b+nb) overlap.
 inline bool overlaps(const void* a, size_t na, const void* b, size_t nb) {

@@ -271,8 +271,11 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   prm.alignment = p->alignment;
   // AV cosine is the fine-pass term alone: the Eq. 2 blend with beta = 1.
   if (p->alignment == APACK_ALIGN_AV_COSINE) prm.beta = 1.0;
-  return launch_dynamics(pl, dp, prm, dtype, dim, visual, audio, query, pl.total_tokens, pl.total_audio, frame_cka,
-                         frame_score, frame_budget, segment_id, gate_fired, kept_visual, hs);
+  const apack_status ls = launch_dynamics(pl, dp, prm, dtype, dim, visual, audio, query, pl.total_tokens,
+                                          pl.total_audio, frame_cka, frame_score, frame_budget, segment_id, gate_fired,
+                                          kept_visual, hs);
+  const apack_status rs = staging_release(blk, hs);
+  return ls != APACK_OK ? ls : rs;
 }
 
 }  // extern "C"

@@ -264,7 +264,10 @@ apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype
   dp.stats = reinterpret_cast<float2*>(ws + pl.off_stats);
   dp.bias = reinterpret_cast<float*>(ws + pl.off_bias);
   dp.colpart = reinterpret_cast<float*>(ws + pl.off_colpart);
-  return launch_prune(pl, dp, dtype, d, hq, hkv, q, q_head_stride, k, k_head_stride, scores, kept_rows, hs);
+  const apack_status ls = launch_prune(pl, dp, dtype, d, hq, hkv, q, q_head_stride, k, k_head_stride, scores,
+                                       kept_rows, hs);
+  const apack_status rs = staging_release(blk, hs);
+  return ls != APACK_OK ? ls : rs;
 }
 
 }  // extern "C"

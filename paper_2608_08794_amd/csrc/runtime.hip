@@ -108,12 +108,19 @@ apack_status staging_upload(Staging* blk, void* dst, size_t bytes, hipStream_t s
   } else {
     e = hipMemcpyAsync(dst, blk->host, bytes, hipMemcpyHostToDevice, stream);
   }
-  if (e == hipSuccess) e = hipEventRecord(blk->done, stream);
   if (e != hipSuccess) {
     std::lock_guard<std::mutex> lk(g_pool_mu);
     blk->busy = false;  // nothing was enqueued that still reads the block
     return fail(APACK_E_HIP, "staging upload: %s", hipGetErrorString(e));
   }
+  return APACK_OK;
+}
+
+apack_status staging_release(Staging* blk, hipStream_t stream) {
+  // If the record fails the block stays busy for good: the upload may still
+  // be queued, so it cannot be handed out again.
+  const hipError_t e = hipEventRecord(blk->done, stream);
+  if (e != hipSuccess) return fail(APACK_E_HIP, "staging event: %s", hipGetErrorString(e));
   return APACK_OK;
 }
 

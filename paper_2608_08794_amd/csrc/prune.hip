@@ -178,23 +178,34 @@ __device__ __forceinline__ float add_halves(float v) {
 // that interleave for the bf16 MFMA (the fp32 MFMA path keeps the
 // compiler's order).
 // ---------------------------------------------------------------------------
-enum : int { kSchedVALU = 0x002, kSchedMFMA = 0x008 };
+// Scheduling-group masks: VALU (which on gfx950 excludes the transcendental
+// unit's instructions), MFMA, and TRANS (v_exp_f32 and the like).
+enum : int { kSchedVALU = 0x002, kSchedMFMA = 0x008, kSchedTRANS = 0x400 };
 
-// VALU instructions placed after each MFMA of a block (0: no placement).
+// VALU and transcendental instructions placed after each MFMA of a block
+// (0 VALU: no placement).  The exponentials must be placed too, or they
+// pile up behind the first MFMAs and leave the last ones bare.
 #ifndef APACK_RS_VALU_PER_MFMA
 #define APACK_RS_VALU_PER_MFMA 8
 #endif
 #ifndef APACK_CS_VALU_PER_MFMA
 #define APACK_CS_VALU_PER_MFMA 7
 #endif
+#ifndef APACK_RS_TRANS_PER_MFMA
+#define APACK_RS_TRANS_PER_MFMA 2
+#endif
+#ifndef APACK_CS_TRANS_PER_MFMA
+#define APACK_CS_TRANS_PER_MFMA 2
+#endif
 
-template <class T, int N_MFMA, int N_PER>
+template <class T, int N_MFMA, int N_PER, int N_TRANS>
 __device__ __forceinline__ void interleave_hint() {
   if constexpr (sizeof(T) == 2 && N_PER > 0) {
 #pragma unroll
     for (int i = 0; i < N_MFMA; ++i) {
       __builtin_amdgcn_sched_group_barrier(kSchedMFMA, 1, 0);
       __builtin_amdgcn_sched_group_barrier(kSchedVALU, N_PER, 0);
+      if constexpr (N_TRANS > 0) __builtin_amdgcn_sched_group_barrier(kSchedTRANS, N_TRANS, 0);
     }
   }
 }
@@ -364,7 +375,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
         // kb*32 + 8*(e/4) + 4*(lane/32) + e%4.
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
-        interleave_hint<T, kRB * G::kSteps, APACK_RS_VALU_PER_MFMA>();
+        interleave_hint<T, kRB * G::kSteps, APACK_RS_VALU_PER_MFMA, APACK_RS_TRANS_PER_MFMA>();
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) pend[rb] = cur[rb];
         __builtin_amdgcn_sched_barrier(0);  // keep later blocks' LDS reads out of this one
@@ -534,7 +545,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
           // used yet.
           add_pend(rb == 0 ? kRB - 1 : rb - 1);
           if (rb == 0) flush_block(kb == 0 ? prev_slot : slot, kb == 0 ? NKB - 1 : kb - 1);
-          interleave_hint<T, G::kSteps, APACK_CS_VALU_PER_MFMA>();
+          interleave_hint<T, G::kSteps, APACK_CS_VALU_PER_MFMA, APACK_CS_TRANS_PER_MFMA>();
           pend = cur;
           __builtin_amdgcn_sched_barrier(0);
         }

@@ -101,55 +101,90 @@ __device__ double block_min(double v, double* sh) { return -block_max<NT>(-v, sh
 // ---------------------------------------------------------------------------
 // Coarse pass (Section 3.1): v_f, a_f and the query mean.
 // grid.x: every frame of every clip, then one block per clip for the query.
-// grid.y: 2048-element slices of the embedding (8 per thread).
+// grid.y: 512-element slices of the embedding (8 per lane).
+// The block's four waves take every fourth row of the frame's visual tokens,
+// of its audio bin (or of the clip's query span); their fp64 partial sums
+// meet in LDS and are added in wave order.  Four times the rows in flight of
+// one wave per slice keeps HBM busy on short clips.
 // ---------------------------------------------------------------------------
+constexpr int kPoolWaves = kBlk / 64;      // row groups per block
+constexpr int kPoolSlice = 64 * 8;         // embedding elements per block
+
 template <class T>
 __global__ __launch_bounds__(kBlk) void k_pool(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
                                                int64_t total_frames, int dim, const T* __restrict__ xv,
                                                const T* __restrict__ xa, const T* __restrict__ xq,
                                                double* __restrict__ v, double* __restrict__ a,
                                                double* __restrict__ q) {
-  const int d0 = (blockIdx.y * kBlk + threadIdx.x) * 8;
-  if (d0 >= dim) return;
-  double acc[8], o[8];
-  if ((int64_t)blockIdx.x < total_frames) {
+  __shared__ double part[2][kPoolWaves - 1][kPoolSlice];
+  const int lane = threadIdx.x & 63, rg = threadIdx.x >> 6;
+  const int d0 = blockIdx.y * kPoolSlice + lane * 8;
+  const bool live = d0 < dim;  // no early return: the block meets at a barrier
+  double av[8], aa[8], o[8];
+#pragma unroll
+  for (int e = 0; e < 8; ++e) av[e] = aa[e] = 0.0;
+  const bool is_frame = (int64_t)blockIdx.x < total_frames;
+  int64_t frame = 0, lo = 0, hi = 0, rows_v = 1;
+  int ci = 0;
+  if (is_frame) {
     const FrameDev fr = frames[blockIdx.x];
     const ClipDev c = clips[fr.clip];
-    const int64_t frame = c.frame_off + fr.f;
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-    const T* base = xv + (c.vis_off + (int64_t)fr.f * c.per_frame) * dim + d0;
-    for (int p = 0; p < c.per_frame; ++p) {
-      load8(base + (int64_t)p * dim, o);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += o[e];
-    }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) v[frame * dim + d0 + e] = acc[e] / (double)c.per_frame;
+    frame = c.frame_off + fr.f;
+    rows_v = c.per_frame;
     // Adaptive average-pool bin of the audio rows for this frame.
-    const int64_t lo = ((int64_t)fr.f * c.n_audio) / c.n_frames;
-    const int64_t hi = (((int64_t)fr.f + 1) * c.n_audio + c.n_frames - 1) / c.n_frames;
+    lo = ((int64_t)fr.f * c.n_audio) / c.n_frames;
+    hi = (((int64_t)fr.f + 1) * c.n_audio + c.n_frames - 1) / c.n_frames;
+    if (live) {
+      const T* base = xv + (c.vis_off + (int64_t)fr.f * c.per_frame) * dim + d0;
+#pragma unroll 4
+      for (int p = rg; p < c.per_frame; p += kPoolWaves) {
+        load8(base + (int64_t)p * dim, o);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-    for (int64_t r = lo; r < hi; ++r) {
-      load8(xa + (c.aud_off + r) * dim + d0, o);
+        for (int e = 0; e < 8; ++e) av[e] += o[e];
+      }
+      for (int64_t r = lo + rg; r < hi; r += kPoolWaves) {
+        load8(xa + (c.aud_off + r) * dim + d0, o);
 #pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += o[e];
+        for (int e = 0; e < 8; ++e) aa[e] += o[e];
+      }
     }
-#pragma unroll
-    for (int e = 0; e < 8; ++e) a[frame * dim + d0 + e] = hi > lo ? acc[e] / (double)(hi - lo) : 0.0;
   } else {
-    const int ci = (int)(blockIdx.x - total_frames);
+    ci = (int)(blockIdx.x - total_frames);
     const ClipDev c = clips[ci];
+    rows_v = c.n_query;
+    if (live) {
+#pragma unroll 4
+      for (int64_t r = rg; r < c.n_query; r += kPoolWaves) {
+        load8(xq + (c.qry_off + r) * dim + d0, o);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc[e] = 0.0;
-    for (int64_t r = 0; r < c.n_query; ++r) {
-      load8(xq + (c.qry_off + r) * dim + d0, o);
-#pragma unroll
-      for (int e = 0; e < 8; ++e) acc[e] += o[e];
+        for (int e = 0; e < 8; ++e) av[e] += o[e];
+      }
     }
+  }
+  if (rg > 0) {
 #pragma unroll
-    for (int e = 0; e < 8; ++e) q[(int64_t)ci * dim + d0 + e] = acc[e] / (double)c.n_query;
+    for (int e = 0; e < 8; ++e) {
+      part[0][rg - 1][lane * 8 + e] = av[e];
+      part[1][rg - 1][lane * 8 + e] = aa[e];
+    }
+  }
+  __syncthreads();
+  if (rg != 0 || !live) return;
+  for (int w = 0; w < kPoolWaves - 1; ++w)
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      av[e] += part[0][w][lane * 8 + e];
+      aa[e] += part[1][w][lane * 8 + e];
+    }
+  if (is_frame) {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      v[frame * dim + d0 + e] = av[e] / (double)rows_v;
+      a[frame * dim + d0 + e] = hi > lo ? aa[e] / (double)(hi - lo) : 0.0;
+    }
+  } else {
+#pragma unroll
+    for (int e = 0; e < 8; ++e) q[(int64_t)ci * dim + d0 + e] = av[e] / (double)rows_v;
   }
 }
 
@@ -1277,7 +1312,7 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
                       int64_t audio_rows, hipStream_t s) {
   apack_status st;
   const int nf = (int)pl.frames.size(), nc = (int)pl.clips.size();
-  const unsigned dchunks = (unsigned)((dim + kBlk * 8 - 1) / (kBlk * 8));
+  const unsigned dchunks = (unsigned)((dim + kPoolSlice - 1) / kPoolSlice);
   hipLaunchKernelGGL(k_pool<T>, dim3(nf + nc, dchunks), dim3(kBlk), 0, s, dp.clips, dp.frames, (int64_t)nf, dim,
                      xv, xa, xq, dp.v, dp.a, dp.q);
   if ((st = launch_status("k_pool")) != APACK_OK) return st;

@@ -190,50 +190,54 @@ __global__ __launch_bounds__(kBlk) void k_pool(const ClipDev* __restrict__ clips
 
 // ---------------------------------------------------------------------------
 // Band Gram entries of one frame: v_f.v_{f+d}, a_f.a_{f+d} for d < w, v_f.q
-// (and q.q for the first frame of the clip).
+// (and q.q for the first frame of the clip).  W bounds the partners a frame
+// needs (w, and 2 for the continuity cosine), so only 2W + 2 sums are formed
+// and reduced; entries are stored kMaxWindow apart.
 // ---------------------------------------------------------------------------
+template <int W>
 __global__ __launch_bounds__(kBlk) void k_band(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
                                                int dim, int w, const double* __restrict__ v,
                                                const double* __restrict__ a, const double* __restrict__ q,
                                                double* __restrict__ band_v, double* __restrict__ band_a,
                                                double* __restrict__ vq, double* __restrict__ qq) {
-  __shared__ double sh[kBlk / 64][2 * kMaxWindow + 2];
+  constexpr int NA = 2 * W + 2;
+  __shared__ double sh[kBlk / 64][NA];
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
   const int64_t f0 = c.frame_off + fr.f;
   const int nd = min(max(w, 2), c.n_frames - fr.f);  // partners f .. f+nd-1 (f+1 for continuity)
   const double* qv = q + (int64_t)fr.clip * dim;
-  double acc[2 * kMaxWindow + 2];
+  double acc[NA];
 #pragma unroll
-  for (int i = 0; i < 2 * kMaxWindow + 2; ++i) acc[i] = 0.0;
+  for (int i = 0; i < NA; ++i) acc[i] = 0.0;
   for (int d = threadIdx.x; d < dim; d += kBlk) {
     const double vf = v[f0 * dim + d], af = a[f0 * dim + d], qd = qv[d];
 #pragma unroll
-    for (int dd = 0; dd < kMaxWindow; ++dd) {
+    for (int dd = 0; dd < W; ++dd) {
       if (dd < nd) {
         acc[dd] += vf * v[(f0 + dd) * dim + d];
-        acc[kMaxWindow + dd] += af * a[(f0 + dd) * dim + d];
+        acc[W + dd] += af * a[(f0 + dd) * dim + d];
       }
     }
-    acc[2 * kMaxWindow] += vf * qd;
-    acc[2 * kMaxWindow + 1] += qd * qd;
+    acc[2 * W] += vf * qd;
+    acc[2 * W + 1] += qd * qd;
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int i = 0; i < 2 * kMaxWindow + 2; ++i) {
+  for (int i = 0; i < NA; ++i) {
     const double s = wave_sum(acc[i]);
     if (lane == 0) sh[wave][i] = s;
   }
   __syncthreads();
   const int i = threadIdx.x;
-  if (i < 2 * kMaxWindow + 2) {
+  if (i < NA) {
     double s = 0.0;
     for (int ww = 0; ww < kBlk / 64; ++ww) s += sh[ww][i];
-    if (i < kMaxWindow) {
+    if (i < W) {
       if (i < nd) band_v[f0 * kMaxWindow + i] = s;
-    } else if (i < 2 * kMaxWindow) {
-      if (i - kMaxWindow < nd) band_a[f0 * kMaxWindow + (i - kMaxWindow)] = s;
-    } else if (i == 2 * kMaxWindow) {
+    } else if (i < 2 * W) {
+      if (i - W < nd) band_a[f0 * kMaxWindow + (i - W)] = s;
+    } else if (i == 2 * W) {
       vq[f0] = s;
     } else if (fr.f == 0) {
       qq[fr.clip] = s;
@@ -1317,7 +1321,10 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
                      xv, xa, xq, dp.v, dp.a, dp.q);
   if ((st = launch_status("k_pool")) != APACK_OK) return st;
   if (nf > 0) {
-    hipLaunchKernelGGL(k_band, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dim, prm.window, dp.v, dp.a, dp.q,
+    // Partners per frame: max(w, 2) <= kMaxWindow (checked on the host).
+    const int wb = std::max(prm.window, 2);
+    auto band = wb <= 2 ? k_band<2> : wb <= 4 ? k_band<4> : wb <= 8 ? k_band<8> : k_band<kMaxWindow>;
+    hipLaunchKernelGGL(band, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dim, prm.window, dp.v, dp.a, dp.q,
                        dp.band_v, dp.band_a, dp.vq, dp.qq);
     if ((st = launch_status("k_band")) != APACK_OK) return st;
   }

@@ -204,10 +204,30 @@ __global__ __launch_bounds__(kT) void k_keep_write(const SeqDev* __restrict__ se
 // LDS histograms, the threshold, and the ordered kept list, in one launch
 // instead of four.  Same rules as above: rows above the threshold, then the
 // first `need` rows equal to it in row order.
+// Wave w holds rows [1024 w, 1024 (w + 1)), lane l of it rows 1024 w + 64 u + l
+// (u < 16), so every load is coalesced; ranks among ties and output slots
+// come from ballots inside a wave and a scan over the 16 wave totals.
 // ---------------------------------------------------------------------------
 constexpr int kST = 1024;                 // threads
-constexpr int kSPer = 16;                 // contiguous rows per thread
+constexpr int kSPer = 16;                 // rows per thread
+constexpr int kSWaves = kST / 64;
 constexpr int kSmallRows = kST * kSPer;
+
+// Lanes below this one with their bit set in a wave-wide mask.
+__device__ __forceinline__ uint32_t below(uint64_t m) {
+  return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+// Exclusive prefix of the per-wave values in s[0 .. kSWaves) for wave w;
+// every thread calls it (it holds a barrier before the reads).
+__device__ __forceinline__ uint32_t wave_base(const uint32_t* s, int w) {
+  __syncthreads();
+  uint32_t b = 0;
+#pragma unroll
+  for (int i = 0; i < kSWaves; ++i)
+    if (i < w) b += s[i];
+  return b;
+}
 
 __global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__ seqs,
                                                       const uint8_t* __restrict__ tags,
@@ -215,17 +235,23 @@ __global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__
   __shared__ uint32_t lh[2 * kBins1];
   __shared__ uint32_t sh[kST / 64];
   __shared__ uint32_t s_prefix[2], s_kk[2], s_thr[2], s_need[2];
+  __shared__ uint32_t s_wave[2][kSWaves];
   const SeqDev& sq = seqs[blockIdx.x];
   const int n = (int)sq.n_tokens;
   if (n == 0) return;
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int row0 = wave * (64 * kSPer) + lane;   // row of u = 0; row(u) = row0 + 64 u
   const uint8_t* tg = tags + sq.tag_off;
   uint32_t bits[kSPer];
   uint8_t mt[kSPer];
 #pragma unroll
   for (int u = 0; u < kSPer; ++u) {
-    const int i = tid * kSPer + u;
+    const int i = row0 + 64 * u;
     mt[u] = i < n ? tg[i] : 0xFF;
+  }
+#pragma unroll
+  for (int u = 0; u < kSPer; ++u) {
+    const int i = row0 + 64 * u;
     bits[u] = 0;
     if (mt[u] == 1 || mt[u] == 2) bits[u] = clamp_bits(scores[sq.tok_off + i]);
     // Scores of sequences with candidates are written by the score kernels;
@@ -252,77 +278,86 @@ __global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__
       if (digit_of(bits[u], pass, a ? pre0 : pre1, d)) atomicAdd(&lh[(a ? 0 : kBins1) + d], 1u);
     }
     __syncthreads();
-    // Bin holding the kk-th largest value: thread t covers bins
-    // nb-1-2t and nb-2-2t (descending), a block scan finds it.
+    // Bin holding the kk-th largest value of each modality: thread t covers
+    // bins nb-1-2t and nb-2-2t (descending); one block scan serves both
+    // modalities, their counts (at most kSmallRows) packed in 16-bit halves.
     const int nb = pass == 2 ? 512 : kRadixBins;
+    uint32_t c[2][2], sum = 0;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int b = nb - 1 - (tid * 2 + j);
+      c[0][j] = b >= 0 ? lh[b] : 0u;
+      c[1][j] = b >= 0 ? lh[kBins1 + b] : 0u;
+      sum += c[0][j] | (c[1][j] << 16);
+    }
+    // Ranks and prefixes are read before the scan, whose barriers keep every
+    // read ahead of the writes below.
+    const uint32_t kk[2] = {s_kk[0], s_kk[1]}, pf[2] = {s_prefix[0], s_prefix[1]};
+    uint32_t total;
+    const uint32_t incl = block_scan<kST>(sum, sh, total);
     for (int m = 0; m < 2; ++m) {
       if (!(m == 0 ? act0 : act1)) continue;
-      uint32_t c[2], sum = 0;
-#pragma unroll
-      for (int j = 0; j < 2; ++j) {
-        const int b = nb - 1 - (tid * 2 + j);
-        c[j] = b >= 0 ? lh[m * kBins1 + b] : 0u;
-        sum += c[j];
-      }
-      // Rank and prefix are read before the scan, whose barrier keeps every
-      // read ahead of the single write below.
-      const uint32_t kk = s_kk[m], prefix0 = s_prefix[m];
-      uint32_t total;
-      const uint32_t incl = block_scan<kST>(sum, sh, total);
-      uint32_t before = incl - sum;
-      if (before < kk && incl >= kk) {
+      const uint32_t in_m = (incl >> (16 * m)) & 0xFFFFu, s_m = c[m][0] + c[m][1];
+      uint32_t before = in_m - s_m;
+      if (before < kk[m] && in_m >= kk[m]) {
 #pragma unroll
         for (int j = 0; j < 2; ++j) {
-          if (before < kk && before + c[j] >= kk) {
+          if (before < kk[m] && before + c[m][j] >= kk[m]) {
             const uint32_t b = (uint32_t)(nb - 1 - (tid * 2 + j));
-            const uint32_t prefix = (prefix0 << (pass == 1 ? 11 : 9)) | b;
+            const uint32_t prefix = (pf[m] << (pass == 1 ? 11 : 9)) | b;
             s_prefix[m] = prefix;
-            s_kk[m] = kk - before;
+            s_kk[m] = kk[m] - before;
             if (pass == 2) {
               s_thr[m] = prefix;
-              s_need[m] = kk - before;
+              s_need[m] = kk[m] - before;
             }
           }
-          before += c[j];
+          before += c[m][j];
         }
       }
-      __syncthreads();
     }
+    __syncthreads();
   }
-  // Kept list: ties ranked in row order, then positions by a block scan.
+  // Ranks of the rows equal to each threshold, in row order: wave totals,
+  // then within the wave by u and by lane.
   const uint32_t thr0 = s_thr[0], thr1 = s_thr[1], need0 = s_need[0], need1 = s_need[1];
-  uint32_t ea = 0, ev = 0;
+  uint32_t ta = 0, tv = 0;
 #pragma unroll
   for (int u = 0; u < kSPer; ++u) {
-    ea += mt[u] == 1 && bits[u] == thr0;
-    ev += mt[u] == 2 && bits[u] == thr1;
+    ta += __popcll(__ballot(mt[u] == 1 && bits[u] == thr0));
+    tv += __popcll(__ballot(mt[u] == 2 && bits[u] == thr1));
   }
-  uint32_t tot;
-  const uint32_t packed = ea | (ev << 16);
-  const uint32_t ex = block_scan<kST>(packed, sh, tot) - packed;
-  // keep(u) with the tie ranks running from (ra, rv); the ranks advance.
-  auto keep_row = [&](int u, uint32_t& ra, uint32_t& rv) {
-    const uint8_t m = mt[u];
-    if (m == 0) return true;
-    if (m == 1) return bits[u] > thr0 || (bits[u] == thr0 && ra++ < need0);
-    if (m == 2) return bits[u] > thr1 || (bits[u] == thr1 && rv++ < need1);
-    return false;
-  };
-  uint32_t nk = 0;
-  {
-    uint32_t ra = ex & 0xFFFFu, rv = ex >> 16;
+  if (lane == 0) {
+    s_wave[0][wave] = ta;
+    s_wave[1][wave] = tv;
+  }
+  uint32_t ra = wave_base(s_wave[0], wave), rv = wave_base(s_wave[1], wave);
+  uint32_t keepbits = 0, nk = 0;
 #pragma unroll
-    for (int u = 0; u < kSPer; ++u) nk += keep_row(u, ra, rv);
+  for (int u = 0; u < kSPer; ++u) {
+    const uint64_t ma = __ballot(mt[u] == 1 && bits[u] == thr0);
+    const uint64_t mv = __ballot(mt[u] == 2 && bits[u] == thr1);
+    bool kp = false;
+    if (mt[u] == 0) kp = true;
+    else if (mt[u] == 1) kp = bits[u] > thr0 || (bits[u] == thr0 && ra + below(ma) < need0);
+    else if (mt[u] == 2) kp = bits[u] > thr1 || (bits[u] == thr1 && rv + below(mv) < need1);
+    ra += __popcll(ma);
+    rv += __popcll(mv);
+    keepbits |= (uint32_t)kp << u;
+    nk += __popcll(__ballot(kp));
   }
-  uint32_t pos = block_scan<kST>(nk, sh, tot) - nk;
+  __syncthreads();   // every wave has read s_wave
+  if (lane == 0) s_wave[0][wave] = nk;
+  uint32_t pos = wave_base(s_wave[0], wave);
   int32_t* out = kept + sq.out_off;
-  uint32_t ra = ex & 0xFFFFu, rv = ex >> 16;
 #pragma unroll
-  for (int u = 0; u < kSPer; ++u)
-    if (keep_row(u, ra, rv)) {
-      if (pos < (uint32_t)sq.n_kept) out[pos] = (int32_t)(sq.tok_off + tid * kSPer + u);
-      ++pos;
-    }
+  for (int u = 0; u < kSPer; ++u) {
+    const bool kp = (keepbits >> u) & 1u;
+    const uint64_t mk = __ballot(kp);
+    const uint32_t at = pos + below(mk);
+    if (kp && at < (uint32_t)sq.n_kept) out[at] = (int32_t)(sq.tok_off + row0 + 64 * u);
+    pos += __popcll(mk);
+  }
 }
 
 }  // namespace

@@ -1064,6 +1064,50 @@ __global__ __launch_bounds__(kBlk) void k_spatial_reduce(int64_t n_frames, int t
   cka[f] = den == 0.0 ? 0.0 : s_av / den;
 }
 
+// Maximum of v over the 64 lanes of a wave, in every lane, without the LDS
+// crossbar: DPP swaps within quads (xor 1, xor 2), rotations by 4 and 8
+// within 16-lane rows, then v_permlane16_swap (rows 0<->1, 2<->3) and
+// v_permlane32_swap (halves).  All 64 lanes must be active.
+__device__ __forceinline__ double dpp_f64(double v, int ctrl) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const int lo = (int)(uint32_t)b, hi = (int)(uint32_t)(b >> 32);
+  int rl, rh;
+  switch (ctrl) {
+    case 0: rl = __builtin_amdgcn_update_dpp(lo, lo, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
+            rh = __builtin_amdgcn_update_dpp(hi, hi, 0xB1, 0xF, 0xF, false); break;
+    case 1: rl = __builtin_amdgcn_update_dpp(lo, lo, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
+            rh = __builtin_amdgcn_update_dpp(hi, hi, 0x4E, 0xF, 0xF, false); break;
+    case 2: rl = __builtin_amdgcn_update_dpp(lo, lo, 0x124, 0xF, 0xF, false);  // row_ror:4
+            rh = __builtin_amdgcn_update_dpp(hi, hi, 0x124, 0xF, 0xF, false); break;
+    default: rl = __builtin_amdgcn_update_dpp(lo, lo, 0x128, 0xF, 0xF, false); // row_ror:8
+             rh = __builtin_amdgcn_update_dpp(hi, hi, 0x128, 0xF, 0xF, false); break;
+  }
+  return __longlong_as_double((long long)(((uint64_t)(uint32_t)rh << 32) | (uint32_t)rl));
+}
+__device__ __forceinline__ double swap_max_f64(double v, bool rows16) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)b, hi = (uint32_t)(b >> 32);
+  uint32_t l0, l1, h0, h1;
+  if (rows16) {
+    const auto l = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto h = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    l0 = l[0]; l1 = l[1]; h0 = h[0]; h1 = h[1];
+  } else {
+    const auto l = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+    const auto h = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+    l0 = l[0]; l1 = l[1]; h0 = h[0]; h1 = h[1];
+  }
+  const double x = __longlong_as_double((long long)(((uint64_t)h0 << 32) | l0));
+  const double y = __longlong_as_double((long long)(((uint64_t)h1 << 32) | l1));
+  return fmax(x, y);
+}
+__device__ __forceinline__ double wave_max_f64(double v) {
+#pragma unroll
+  for (int c = 0; c < 4; ++c) v = fmax(v, dpp_f64(v, c));
+  v = swap_max_f64(v, true);
+  return swap_max_f64(v, false);
+}
+
 // Lexicographic (value desc, index asc) argmax across a wave.
 __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
 #pragma unroll
@@ -1137,7 +1181,7 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
                                                         const FrameDev* __restrict__ frames,
                                                         const FramePlanDev* __restrict__ plan, DynParamsDev prm,
                                                         const double* __restrict__ gram, int32_t* __restrict__ kept) {
-  __shared__ double Sl[kDafpsLdsDoubles];
+  __shared__ __attribute__((aligned(16))) double Sl[kDafpsLdsDoubles];
   __shared__ double rho_sh[kMaxPerFrame];
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
@@ -1148,18 +1192,35 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
   const int k = min(fp.budget, P);
   const double* S = gram + c.gram_off + (int64_t)fr.f * P * P;
   const int R = min(P, kDafpsLdsDoubles / P);
-  // Eight independent loads in flight per thread.
-  for (int e0 = i; e0 < R * P; e0 += 8 * kMaxPerFrame) {
-    double v[8];
-#pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int e = e0 + u * kMaxPerFrame;
-      v[u] = e < R * P ? S[e] : 0.0;
+  if (((uintptr_t)S & 15) == 0) {
+    // Rows [0, R) of S into LDS with 16-byte direct-to-LDS loads, all in
+    // flight together: wave load j fills bytes [1024 j, 1024 j + 1024), lane
+    // l the 16 bytes at 1024 j + 16 l (lanes past the end stay idle).
+    typedef __attribute__((address_space(3))) void* lds_ptr_t;
+    typedef __attribute__((address_space(1))) void* glb_ptr_t;
+    const int bytes = R * P * 8;
+    const int lane = i & 63, wave = i >> 6;
+    for (int j = wave; j * 1024 < bytes; j += kMaxPerFrame / 64) {
+      const int off = j * 1024 + lane * 16;
+      if (off < bytes)
+        __builtin_amdgcn_global_load_lds((glb_ptr_t)(reinterpret_cast<const char*>(S) + off),
+                                         (lds_ptr_t)(reinterpret_cast<char*>(Sl) + j * 1024), 16, 0, 0);
     }
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  } else {
+    // Odd P * P: S is only 8-byte aligned; eight loads in flight per thread.
+    for (int e0 = i; e0 < R * P; e0 += 8 * kMaxPerFrame) {
+      double v[8];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      const int e = e0 + u * kMaxPerFrame;
-      if (e < R * P) Sl[e] = v[u];
+      for (int u = 0; u < 8; ++u) {
+        const int e = e0 + u * kMaxPerFrame;
+        v[u] = e < R * P ? S[e] : 0.0;
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        const int e = e0 + u * kMaxPerFrame;
+        if (e < R * P) Sl[e] = v[u];
+      }
     }
   }
   __syncthreads();
@@ -1192,8 +1253,7 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
 #pragma unroll
     for (int u = 0; u < kU; ++u)
       if (!taken[u]) m = fmax(m, v[u]);
-#pragma unroll
-    for (int off = 32; off >= 1; off >>= 1) m = fmax(m, __shfl_xor(m, off));
+    m = wave_max_f64(m);
     int best = 0x7FFFFFFF;
 #pragma unroll
     for (int u = 0; u < kU; ++u) {

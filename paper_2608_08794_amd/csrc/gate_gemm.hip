@@ -5,8 +5,9 @@
 // whose dim is a multiple of 64; k_gate_gemm in dynamics.hip covers the rest.
 //
 // Each workgroup owns a 256 x 256 tile (audio rows x visual columns); its
-// four waves own 128 x 128 quadrants as 4 x 4 blocks of
-// v_mfma_f32_32x32x16_bf16, so a wave reads 8 fragments from LDS per 16
+// eight waves (two per SIMD, so one wave's loads, waits and LDS reads hide
+// under the other's MFMAs) own 128 x 64 blocks as 4 x 2 blocks of
+// v_mfma_f32_32x32x16_bf16, so a wave reads 6 fragments from LDS per 8
 // MFMAs.  K streams through two 64-element LDS stages (2 x 64 KiB), filled
 // by 16-byte direct-to-LDS loads while the other stage is consumed; the
 // 128-byte rows are stored with their 16-byte chunks XOR-swizzled by the
@@ -41,7 +42,10 @@ constexpr int kRowB = kK * 2;                  // bytes of one row per stage
 constexpr int kChunks = kRowB / 16;            // 16-byte chunks per row
 constexpr int kOpB = kTile * kRowB;            // one operand's stage
 constexpr int kStageB = 2 * kOpB;
-constexpr int kWaves = 4;
+constexpr int kWaves = 8;
+constexpr int kWN = 4;                         // waves along the visual columns
+constexpr int kBI = kTile / (kWaves / kWN) / 32; // 32-row blocks per wave
+constexpr int kBJ = kTile / kWN / 32;            // 32-column blocks per wave
 constexpr int kLoadsPerWave = kOpB / 1024 / kWaves;  // 1 KiB loads per wave per operand
 constexpr int kXcds = 8;
 
@@ -80,7 +84,7 @@ __device__ __forceinline__ bf16x8 lds_frag(const char* lds, int row, int ks, int
   return *reinterpret_cast<const bf16x8*>(lds + row * kRowB + c * 16);
 }
 
-__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(1, 1))) void k_gate_gemm256(
+__global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 2))) void k_gate_gemm256(
     const ClipDev* __restrict__ clips, const GemmTileDev* __restrict__ tiles, int dim, const uint16_t* __restrict__ xv,
     const uint16_t* __restrict__ xa, const double* __restrict__ na, uint32_t* __restrict__ maxkey) {
   __shared__ __attribute__((aligned(16))) char lds[kStages * kStageB];
@@ -92,13 +96,13 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(1, 
   const uint16_t* A = xa + c.aud_off * dim;
   const uint16_t* B = xv + c.vis_off * dim;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / kWN, wn = wave % kWN;
 
-  f32x16 acc[4][4];
+  f32x16 acc[kBI][kBJ];
 #pragma unroll
-  for (int i = 0; i < 4; ++i)
+  for (int i = 0; i < kBI; ++i)
 #pragma unroll
-    for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
+    for (int j = 0; j < kBJ; ++j) acc[i][j] = f32x16{};
 
   const int n_k = dim / kK;
   auto issue = [&](int k_stage) {
@@ -125,13 +129,13 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(1, 
     if (it + kStages - 1 < n_k) issue(it + kStages - 1);
     const char* la = lds + buf * kStageB;
     const char* lb = la + kOpB;
-    // Fragments of K slice ks + 1 are read while slice ks's 16 MFMAs run.
-    bf16x8 fa[2][4], fb[2][4];
+    // Fragments of K slice ks + 1 are read while slice ks's MFMAs run.
+    bf16x8 fa[2][kBI], fb[2][kBJ];
     auto read = [&](int ks, int h) {
 #pragma unroll
-      for (int i = 0; i < 4; ++i) fa[h][i] = lds_frag(la, wm * 128 + i * 32 + (lane & 31), ks, lane);
+      for (int i = 0; i < kBI; ++i) fa[h][i] = lds_frag(la, wm * kBI * 32 + i * 32 + (lane & 31), ks, lane);
 #pragma unroll
-      for (int j = 0; j < 4; ++j) fb[h][j] = lds_frag(lb, wn * 128 + j * 32 + (lane & 31), ks, lane);
+      for (int j = 0; j < kBJ; ++j) fb[h][j] = lds_frag(lb, wn * kBJ * 32 + j * 32 + (lane & 31), ks, lane);
     };
     read(0, 0);
 #pragma unroll
@@ -142,9 +146,9 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(1, 
       // scheduler would otherwise sink each read to its first use.
       __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int i = 0; i < 4; ++i)
+      for (int i = 0; i < kBI; ++i)
 #pragma unroll
-        for (int j = 0; j < 4; ++j)
+        for (int j = 0; j < kBJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[h][i], fb[h][j], acc[i][j], 0, 0, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
@@ -167,17 +171,17 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(1, 
   }
   __syncthreads();
 #pragma unroll
-  for (int j = 0; j < 4; ++j) {
+  for (int j = 0; j < kBJ; ++j) {
     float m = -INFINITY;
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
+    for (int i = 0; i < kBI; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const float s = inv[wm * 128 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)];
+        const float s = inv[wm * kBI * 32 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3)];
         m = fmaxf(m, s == -INFINITY ? -INFINITY : acc[i][j][e] * s);
       }
     m = fmaxf(m, __shfl_xor(m, 32));
-    const int64_t col = tl.n0 + wn * 128 + j * 32 + (lane & 31);
+    const int64_t col = tl.n0 + wn * kBJ * 32 + j * 32 + (lane & 31);
     if (lane < 32 && col < n_v && m > -INFINITY) atomicMax(&maxkey[c.vis_off + col], order_key(m));
   }
 }

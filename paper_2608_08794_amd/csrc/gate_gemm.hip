@@ -156,8 +156,8 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
 
   // Epilogue.  Inverse audio norms of the tile's rows in LDS (-inf past the
   // clip's audio, so those rows never win); acc[i][j][e] of lane l is audio
-  // row wm*128 + 32i + 8(e/4) + 4(l/32) + e%4, visual column
-  // wn*128 + 32j + l%32.
+  // row 32 (kBI wm + i) + 8(e/4) + 4(l/32) + e%4, visual column
+  // 32 (kBJ wn + j) + l%32.
   __syncthreads();
   float* inv = reinterpret_cast<float*>(lds);
   for (int r = tid; r < kTile; r += kWaves * 64) {

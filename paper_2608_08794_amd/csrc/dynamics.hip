@@ -2,11 +2,13 @@
 // first loop of Algorithm 1) on gfx950.
 //
 //   k_pool       coarse pass: frame means v_f, audio-bin means a_f (adaptive
-//                pooling onto the frame axis) and the query mean, in fp64
+//                pooling onto the frame axis) and the query mean, in fp64;
+//                the same read leaves per-slice row sums of squares
 //   k_band       band Gram v_f.v_{f+d}, a_f.a_{f+d} (d < w), v_f.q, q.q
 //   k_cka        Eq. 1 per frame from the centred w x w window Grams, the
 //                clip mean and the gate of Eq. 2
-//   k_norms      squared norms of every visual and audio token (fp64)
+//   k_norms      squared norms of every visual and audio token of the clips
+//                (fp64), from k_pool's per-slice sums
 //   k_gate_gemm  only where the gate fired: X_A . X_V^T on bf16 MFMA, scaled
 //                by 1/|a_j|, max over audio tokens in-lane, merged across
 //                tiles by atomicMax on order-preserving uint keys
@@ -62,10 +64,58 @@ __device__ __forceinline__ void load8(const float* p, double (&o)[8]) {
   o[4] = b.x; o[5] = b.y; o[6] = b.z; o[7] = b.w;
 }
 
+// Cross-lane reductions of a double over the 64 lanes of a wave, in every
+// lane, without the LDS crossbar: DPP within 16-lane rows, then
+// v_permlane16_swap (rows 0<->1, 2<->3) and v_permlane32_swap (halves).
+// All 64 lanes must be active.
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const int lo = __builtin_amdgcn_update_dpp((int)(uint32_t)b, (int)(uint32_t)b, CTRL, 0xF, 0xF, false);
+  const int hi = __builtin_amdgcn_update_dpp((int)(uint32_t)(b >> 32), (int)(uint32_t)(b >> 32), CTRL, 0xF, 0xF, false);
+  return __longlong_as_double((long long)(((uint64_t)(uint32_t)hi << 32) | (uint32_t)lo));
+}
+// The two values of a swap pair (rows 2k and 2k+1, or the two halves), the
+// lower one first, the same in both lanes of the pair.
+template <bool ROWS16>
+__device__ __forceinline__ void swap_pair_f64(double v, double& x, double& y) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  const uint32_t lo = (uint32_t)b, hi = (uint32_t)(b >> 32);
+  uint32_t l0, l1, h0, h1;
+  if constexpr (ROWS16) {
+    const auto l = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
+    const auto h = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
+    l0 = l[0]; l1 = l[1]; h0 = h[0]; h1 = h[1];
+  } else {
+    const auto l = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
+    const auto h = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
+    l0 = l[0]; l1 = l[1]; h0 = h[0]; h1 = h[1];
+  }
+  x = __longlong_as_double((long long)(((uint64_t)h0 << 32) | l0));
+  y = __longlong_as_double((long long)(((uint64_t)h1 << 32) | l1));
+}
+// Sum: every step pairs lanes symmetrically (quad xor 1, quad xor 2,
+// half-row mirror, row mirror, then the swaps), so both lanes of a pair add
+// the same two values and every lane ends with the same bits.
 __device__ __forceinline__ double wave_sum(double v) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v += __shfl_xor(v, off);
-  return v;
+  v += dpp_f64<0xB1>(v);   // quad_perm [1,0,3,2]
+  v += dpp_f64<0x4E>(v);   // quad_perm [2,3,0,1]
+  v += dpp_f64<0x141>(v);  // row_half_mirror
+  v += dpp_f64<0x140>(v);  // row_mirror
+  double x, y;
+  swap_pair_f64<true>(v, x, y);
+  swap_pair_f64<false>(x + y, x, y);
+  return x + y;
+}
+__device__ __forceinline__ double wave_max_f64(double v) {
+  v = fmax(v, dpp_f64<0xB1>(v));
+  v = fmax(v, dpp_f64<0x4E>(v));
+  v = fmax(v, dpp_f64<0x141>(v));
+  v = fmax(v, dpp_f64<0x140>(v));
+  double x, y;
+  swap_pair_f64<true>(v, x, y);
+  swap_pair_f64<false>(fmax(x, y), x, y);
+  return fmax(x, y);
 }
 
 // Block-wide reductions over NT threads (sh holds NT / 64 words); every
@@ -84,8 +134,7 @@ __device__ double block_sum(double v, double* sh) {
 }
 template <int NT = kBlk>
 __device__ double block_max(double v, double* sh) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) v = fmax(v, __shfl_xor(v, off));
+  v = wave_max_f64(v);
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   __syncthreads();
   if (lane == 0) sh[wave] = v;
@@ -100,65 +149,93 @@ __device__ double block_min(double v, double* sh) { return -block_max<NT>(-v, sh
 
 // ---------------------------------------------------------------------------
 // Coarse pass (Section 3.1): v_f, a_f and the query mean.
-// grid.x: every frame of every clip, then one block per clip for the query.
-// grid.y: 512-element slices of the embedding (8 per lane).
+// One block per (item, 512-element slice of the embedding, 8 per lane); the
+// items are every frame of every clip, then one per clip for the query.
+// The slices of an item are consecutive block indices, so the blocks that
+// read the same rows run together and each DRAM page is opened once.
 // The block's four waves take every fourth row of the frame's visual tokens,
 // of its audio bin (or of the clip's query span); their fp64 partial sums
 // meet in LDS and are added in wave order.  Four times the rows in flight of
-// one wave per slice keeps HBM busy on short clips.
+// one wave per slice keeps HBM busy on short clips.  The same pass leaves
+// each visual and audio row's sum of squares over the slice in
+// sqp[slice][row] (audio rows after the n_vis visual rows), so the token
+// norms need no second read of X_V and X_A.
 // ---------------------------------------------------------------------------
 constexpr int kPoolWaves = kBlk / 64;      // row groups per block
-constexpr int kPoolSlice = 64 * 8;         // embedding elements per block
 
 template <class T>
 __global__ __launch_bounds__(kBlk) void k_pool(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
-                                               int64_t total_frames, int dim, const T* __restrict__ xv,
+                                               int64_t total_frames, int dim, int slices, const T* __restrict__ xv,
                                                const T* __restrict__ xa, const T* __restrict__ xq,
                                                double* __restrict__ v, double* __restrict__ a,
-                                               double* __restrict__ q) {
+                                               double* __restrict__ q, int64_t n_vis, int64_t sq_stride,
+                                               double* __restrict__ sqp) {
   __shared__ double part[2][kPoolWaves - 1][kPoolSlice];
   const int lane = threadIdx.x & 63, rg = threadIdx.x >> 6;
-  const int d0 = blockIdx.y * kPoolSlice + lane * 8;
-  const bool live = d0 < dim;  // no early return: the block meets at a barrier
+  const int64_t item = blockIdx.x / slices;
+  const int slice = (int)(blockIdx.x - item * slices);
+  const int d0 = slice * kPoolSlice + lane * 8;
+  // Lanes past dim read nothing and add zeros: every lane of a wave takes
+  // part in the row norms' cross-lane sums, and the block meets at a barrier.
+  const bool live = d0 < dim;
+  auto row8 = [&](const T* p, double (&o)[8]) {
+    if (live) {
+      load8(p, o);
+    } else {
+#pragma unroll
+      for (int e = 0; e < 8; ++e) o[e] = 0.0;
+    }
+  };
+  double* sq = sqp + (int64_t)slice * sq_stride;
   double av[8], aa[8], o[8];
 #pragma unroll
   for (int e = 0; e < 8; ++e) av[e] = aa[e] = 0.0;
-  const bool is_frame = (int64_t)blockIdx.x < total_frames;
+  const bool is_frame = item < total_frames;
   int64_t frame = 0, lo = 0, hi = 0, rows_v = 1;
   int ci = 0;
   if (is_frame) {
-    const FrameDev fr = frames[blockIdx.x];
+    const FrameDev fr = frames[item];
     const ClipDev c = clips[fr.clip];
     frame = c.frame_off + fr.f;
     rows_v = c.per_frame;
     // Adaptive average-pool bin of the audio rows for this frame.
     lo = ((int64_t)fr.f * c.n_audio) / c.n_frames;
     hi = (((int64_t)fr.f + 1) * c.n_audio + c.n_frames - 1) / c.n_frames;
-    if (live) {
-      const T* base = xv + (c.vis_off + (int64_t)fr.f * c.per_frame) * dim + d0;
+    const int64_t row0 = c.vis_off + (int64_t)fr.f * c.per_frame;
+    const T* base = xv + row0 * dim + d0;
 #pragma unroll 4
-      for (int p = rg; p < c.per_frame; p += kPoolWaves) {
-        load8(base + (int64_t)p * dim, o);
+    for (int p = rg; p < c.per_frame; p += kPoolWaves) {
+      row8(base + (int64_t)p * dim, o);
+      double s2 = 0.0;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) av[e] += o[e];
+      for (int e = 0; e < 8; ++e) {
+        av[e] += o[e];
+        s2 = fma(o[e], o[e], s2);
       }
-      for (int64_t r = lo + rg; r < hi; r += kPoolWaves) {
-        load8(xa + (c.aud_off + r) * dim + d0, o);
+      s2 = wave_sum(s2);
+      if (lane == 0) sq[row0 + p] = s2;
+    }
+    // A row shared by two bins gets the same value from both.
+    for (int64_t r = lo + rg; r < hi; r += kPoolWaves) {
+      row8(xa + (c.aud_off + r) * dim + d0, o);
+      double s2 = 0.0;
 #pragma unroll
-        for (int e = 0; e < 8; ++e) aa[e] += o[e];
+      for (int e = 0; e < 8; ++e) {
+        aa[e] += o[e];
+        s2 = fma(o[e], o[e], s2);
       }
+      s2 = wave_sum(s2);
+      if (lane == 0) sq[n_vis + c.aud_off + r] = s2;
     }
   } else {
-    ci = (int)(blockIdx.x - total_frames);
+    ci = (int)(item - total_frames);
     const ClipDev c = clips[ci];
     rows_v = c.n_query;
-    if (live) {
 #pragma unroll 4
-      for (int64_t r = rg; r < c.n_query; r += kPoolWaves) {
-        load8(xq + (c.qry_off + r) * dim + d0, o);
+    for (int64_t r = rg; r < c.n_query; r += kPoolWaves) {
+      row8(xq + (c.qry_off + r) * dim + d0, o);
 #pragma unroll
-        for (int e = 0; e < 8; ++e) av[e] += o[e];
-      }
+      for (int e = 0; e < 8; ++e) av[e] += o[e];
     }
   }
   if (rg > 0) {
@@ -318,31 +395,24 @@ __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w
 }
 
 // ---------------------------------------------------------------------------
-// Squared norms of every visual row and audio row (one wave per row); the
-// visual max-cosine keys start at 0 (below every real key).
+// Squared norms of the visual rows [0, n_vis) and audio rows [0, n_aud) of
+// the clips, from k_pool's per-slice partials added in slice order; the
+// visual max-cosine keys start at 0 (below every real key).  Rows in no
+// clip get whatever their slots held and are never read.
 // ---------------------------------------------------------------------------
-template <class T>
-__global__ __launch_bounds__(kBlk) void k_norms(int64_t n_vis, int64_t n_aud, int dim, const T* __restrict__ xv,
-                                                const T* __restrict__ xa, double* __restrict__ nv,
+__global__ __launch_bounds__(kBlk) void k_norms(int64_t n_vis, int64_t n_aud, int slices,
+                                                const double* __restrict__ sqp, double* __restrict__ nv,
                                                 double* __restrict__ na, uint32_t* __restrict__ maxkey) {
-  const int64_t row = (int64_t)blockIdx.x * (kBlk / 64) + (threadIdx.x >> 6);
-  const int lane = threadIdx.x & 63;
-  if (row >= n_vis + n_aud) return;
-  const T* p = row < n_vis ? xv + row * dim : xa + (row - n_vis) * dim;
-  double acc = 0.0, o[8];
-  for (int d = lane * 8; d < dim; d += 64 * 8) {
-    load8(p + d, o);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) acc += o[e] * o[e];
-  }
-  acc = wave_sum(acc);
-  if (lane == 0) {
-    if (row < n_vis) {
-      nv[row] = acc;
-      maxkey[row] = 0u;
-    } else {
-      na[row - n_vis] = acc;
-    }
+  const int64_t stride = n_vis + n_aud;
+  const int64_t row = (int64_t)blockIdx.x * kBlk + threadIdx.x;
+  if (row >= stride) return;
+  double s = 0.0;
+  for (int k = 0; k < slices; ++k) s += sqp[(int64_t)k * stride + row];
+  if (row < n_vis) {
+    nv[row] = s;
+    maxkey[row] = 0u;
+  } else {
+    na[row - n_vis] = s;
   }
 }
 
@@ -1064,50 +1134,6 @@ __global__ __launch_bounds__(kBlk) void k_spatial_reduce(int64_t n_frames, int t
   cka[f] = den == 0.0 ? 0.0 : s_av / den;
 }
 
-// Maximum of v over the 64 lanes of a wave, in every lane, without the LDS
-// crossbar: DPP swaps within quads (xor 1, xor 2), rotations by 4 and 8
-// within 16-lane rows, then v_permlane16_swap (rows 0<->1, 2<->3) and
-// v_permlane32_swap (halves).  All 64 lanes must be active.
-__device__ __forceinline__ double dpp_f64(double v, int ctrl) {
-  const uint64_t b = (uint64_t)__double_as_longlong(v);
-  const int lo = (int)(uint32_t)b, hi = (int)(uint32_t)(b >> 32);
-  int rl, rh;
-  switch (ctrl) {
-    case 0: rl = __builtin_amdgcn_update_dpp(lo, lo, 0xB1, 0xF, 0xF, false);   // quad_perm [1,0,3,2]
-            rh = __builtin_amdgcn_update_dpp(hi, hi, 0xB1, 0xF, 0xF, false); break;
-    case 1: rl = __builtin_amdgcn_update_dpp(lo, lo, 0x4E, 0xF, 0xF, false);   // quad_perm [2,3,0,1]
-            rh = __builtin_amdgcn_update_dpp(hi, hi, 0x4E, 0xF, 0xF, false); break;
-    case 2: rl = __builtin_amdgcn_update_dpp(lo, lo, 0x124, 0xF, 0xF, false);  // row_ror:4
-            rh = __builtin_amdgcn_update_dpp(hi, hi, 0x124, 0xF, 0xF, false); break;
-    default: rl = __builtin_amdgcn_update_dpp(lo, lo, 0x128, 0xF, 0xF, false); // row_ror:8
-             rh = __builtin_amdgcn_update_dpp(hi, hi, 0x128, 0xF, 0xF, false); break;
-  }
-  return __longlong_as_double((long long)(((uint64_t)(uint32_t)rh << 32) | (uint32_t)rl));
-}
-__device__ __forceinline__ double swap_max_f64(double v, bool rows16) {
-  const uint64_t b = (uint64_t)__double_as_longlong(v);
-  const uint32_t lo = (uint32_t)b, hi = (uint32_t)(b >> 32);
-  uint32_t l0, l1, h0, h1;
-  if (rows16) {
-    const auto l = __builtin_amdgcn_permlane16_swap(lo, lo, false, false);
-    const auto h = __builtin_amdgcn_permlane16_swap(hi, hi, false, false);
-    l0 = l[0]; l1 = l[1]; h0 = h[0]; h1 = h[1];
-  } else {
-    const auto l = __builtin_amdgcn_permlane32_swap(lo, lo, false, false);
-    const auto h = __builtin_amdgcn_permlane32_swap(hi, hi, false, false);
-    l0 = l[0]; l1 = l[1]; h0 = h[0]; h1 = h[1];
-  }
-  const double x = __longlong_as_double((long long)(((uint64_t)h0 << 32) | l0));
-  const double y = __longlong_as_double((long long)(((uint64_t)h1 << 32) | l1));
-  return fmax(x, y);
-}
-__device__ __forceinline__ double wave_max_f64(double v) {
-#pragma unroll
-  for (int c = 0; c < 4; ++c) v = fmax(v, dpp_f64(v, c));
-  v = swap_max_f64(v, true);
-  return swap_max_f64(v, false);
-}
-
 // Lexicographic (value desc, index asc) argmax across a wave.
 __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
 #pragma unroll
@@ -1377,8 +1403,9 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
   apack_status st;
   const int nf = (int)pl.frames.size(), nc = (int)pl.clips.size();
   const unsigned dchunks = (unsigned)((dim + kPoolSlice - 1) / kPoolSlice);
-  hipLaunchKernelGGL(k_pool<T>, dim3(nf + nc, dchunks), dim3(kBlk), 0, s, dp.clips, dp.frames, (int64_t)nf, dim,
-                     xv, xa, xq, dp.v, dp.a, dp.q);
+  const int64_t n_vis = pl.total_tokens, n_aud = pl.total_audio;
+  hipLaunchKernelGGL(k_pool<T>, dim3((unsigned)((nf + nc) * dchunks)), dim3(kBlk), 0, s, dp.clips, dp.frames,
+                     (int64_t)nf, dim, (int)dchunks, xv, xa, xq, dp.v, dp.a, dp.q, n_vis, n_vis + n_aud, dp.sqp);
   if ((st = launch_status("k_pool")) != APACK_OK) return st;
   if (nf > 0) {
     // Partners per frame: max(w, 2) <= kMaxWindow (checked on the host).
@@ -1400,10 +1427,9 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
   hipLaunchKernelGGL(k_cka, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm.window, prm.tau_gate, prm.alignment,
                      dp.band_v, dp.band_a, dp.cka, frame_cka, gate_fired);
   if ((st = launch_status("k_cka")) != APACK_OK) return st;
-  const int64_t rows = visual_rows + audio_rows;
-  if (rows > 0) {
-    hipLaunchKernelGGL(k_norms<T>, dim3((unsigned)((rows + 3) / 4)), dim3(kBlk), 0, s, visual_rows, audio_rows,
-                       dim, xv, xa, dp.nv, dp.na, dp.maxkey);
+  if (n_vis + n_aud > 0) {
+    hipLaunchKernelGGL(k_norms, dim3((unsigned)((n_vis + n_aud + kBlk - 1) / kBlk)), dim3(kBlk), 0, s, n_vis, n_aud,
+                       (int)dchunks, dp.sqp, dp.nv, dp.na, dp.maxkey);
     if ((st = launch_status("k_norms")) != APACK_OK) return st;
   }
   if (pl.gemm_tiles > 0) {

@@ -145,6 +145,8 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
   c.take<double>((size_t)frames * pl.spatial_tiles * 3);
   pl.off_anchors = c.used;
   c.take<int32_t>(frames);
+  pl.off_sqp = c.used;
+  c.take<double>((size_t)((dim + kPoolSlice - 1) / kPoolSlice) * (vis_end + aud_end));
   pl.ws_bytes = std::max<size_t>(c.used, kAlign);
   pl.gemm = std::move(tiles);
   return APACK_OK;
@@ -257,6 +259,7 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   dp.spatial = reinterpret_cast<double*>(ws + pl.off_spatial);
   dp.sim = reinterpret_cast<double*>(ws + pl.off_sim);
   dp.anchors = reinterpret_cast<int32_t*>(ws + pl.off_anchors);
+  dp.sqp = reinterpret_cast<double*>(ws + pl.off_sqp);
   DynParamsDev prm;
   prm.tau_gate = p->tau_gate;
   prm.beta = p->beta;

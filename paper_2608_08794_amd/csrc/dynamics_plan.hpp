@@ -54,7 +54,7 @@ struct DynPlan {
   size_t off_clips = 0, off_frames = 0, off_gemm = 0, blob_bytes = 0;
   size_t off_v = 0, off_a = 0, off_q = 0, off_band_v = 0, off_band_a = 0, off_vq = 0, off_qq = 0;
   size_t off_cka = 0, off_nv = 0, off_na = 0, off_maxkey = 0, off_plan = 0, off_gram = 0, off_scratch = 0;
-  size_t off_spatial = 0, off_sim = 0, off_anchors = 0;
+  size_t off_spatial = 0, off_sim = 0, off_anchors = 0, off_sqp = 0;
   int64_t gram_items = 0;            // (frame, Gram tile) pairs over all clips: the anchor Gram's items at most
   size_t ws_bytes = 0;
 };
@@ -90,6 +90,7 @@ struct DynPtrs {
   FrameDev* frames;
   GemmTileDev* gemm;
   double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *na, *gram, *scratch, *spatial, *sim;
+  double* sqp;       // per-slice row sums of squares [slice][visual rows, then audio rows]
   uint32_t* maxkey;
   FramePlanDev* plan;
   int32_t* anchors;  // first frame of each segment, clip c's at frame_off + m
@@ -103,6 +104,7 @@ apack_status launch_gate_gemm256(const ClipDev* clips, const GemmTileDev* tiles,
                                  hipStream_t stream);
 std::vector<GemmTileDev> gate_gemm256_tiles(const std::vector<ClipDev>& clips);
 constexpr int kGemm256K = 64;   // dim must be a multiple of this for the 256-tile kernel
+constexpr int kPoolSlice = 512;  // embedding elements per coarse-pass block (8 per lane)
 
 apack_status launch_dynamics(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& prm, apack_dtype dt,
                              int dim, const void* visual, const void* audio, const void* query, int64_t visual_rows,

@@ -102,10 +102,25 @@ def test_7b_shape_60s_clip_parity(structure):
     _compare(case, _run(case), want)
 
 
-def _packed(parts, params):
+def _packed(parts, params, gaps=None):
+    """Clips packed one after another; with gaps = (before, between, after),
+    rows that belong to no clip (large random values) sit before the first
+    clip, between clips and after the last one in all three buffers."""
+    rng = np.random.default_rng(99)
     xv, xa, xq, seqs = [], [], [], []
     vo = ao = qo = 0
-    for c in parts:
+    dim = parts[0].dim
+
+    def gap(n):
+        nonlocal vo, ao, qo
+        if n:
+            for buf in (xv, xa, xq):
+                buf.append(W.to_bf16_bits(rng.uniform(-40.0, 40.0, size=(n, dim)).astype(np.float32)))
+            vo, ao, qo = vo + n, ao + n, qo + n
+
+    for i, c in enumerate(parts):
+        if gaps:
+            gap(gaps[0] if i == 0 else gaps[1])
         s = c.seqs[0]
         seqs.append(W.AVSeq(s.n_frames, s.per_frame, s.n_audio, s.n_query, vo, ao, qo, s.seg_starts, s.structure))
         xv.append(c.xv)
@@ -114,8 +129,9 @@ def _packed(parts, params):
         vo += c.xv.shape[0]
         ao += c.xa.shape[0]
         qo += c.xq.shape[0]
-    return W.DynamicsCase("bf16", parts[0].dim, np.concatenate(xv), np.concatenate(xa), np.concatenate(xq),
-                          seqs, params)
+    if gaps:
+        gap(gaps[2])
+    return W.DynamicsCase("bf16", dim, np.concatenate(xv), np.concatenate(xa), np.concatenate(xq), seqs, params)
 
 
 def test_ragged_batch_of_clips_with_edge_shapes():
@@ -127,6 +143,20 @@ def test_ragged_batch_of_clips_with_edge_shapes():
         W.dynamics_small("shared", seed=25, frames=12, per_frame=256, audio=150),  # largest P
     ]
     case = _packed(parts, {"window": 3, "r_pre": 0.5})
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+def test_rows_outside_every_clip_are_ignored():
+    """Buffers longer than the clips need: rows before, between and after
+    the clips (in X_V, X_A and X_Q alike) change nothing, and the norms and
+    max-cosine slots are sized by the clips' rows, not by the buffers'."""
+    parts = [
+        W.dynamics_small("offset", seed=51, frames=16, per_frame=12, audio=60),
+        W.dynamics_small("shared", seed=52, frames=9, per_frame=20, audio=40),
+    ]
+    case = _packed(parts, {"window": 3, "r_pre": 0.5}, gaps=(5, 37, 300))
     want = _oracle(case)
     _certify(want)
     _compare(case, _run(case), want)

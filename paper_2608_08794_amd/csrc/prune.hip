@@ -245,9 +245,12 @@ __device__ __forceinline__ void row_update(const f32x16& x, float scale, float& 
 #pragma unroll
   for (int e = 1; e < 16; ++e) lmax = fmaxf(lmax, x[e]);
   const float m_new = fmaxf(m_run, lmax * scale);
-  float p[4] = {0.f, 0.f, 0.f, 0.f};
+  // Four running sums, each started from its first term (no add to zero).
+  float p[4];
 #pragma unroll
-  for (int e = 0; e < 16; ++e) p[e & 3] += fast_exp2(fmaf(x[e], scale, -m_new));
+  for (int e = 0; e < 4; ++e) p[e] = fast_exp2(fmaf(x[e], scale, -m_new));
+#pragma unroll
+  for (int e = 4; e < 16; ++e) p[e & 3] += fast_exp2(fmaf(x[e], scale, -m_new));
   s_run = fmaf(s_run, fast_exp2(m_run - m_new), (p[0] + p[1]) + (p[2] + p[3]));
   m_run = m_new;
 }
@@ -502,10 +505,14 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   f32x16 pend = neg_inf16();
   float cs = 0.f;
   auto add_pend = [&](int rb) {
-    float p[4] = {0.f, 0.f, 0.f, 0.f};
+    float p[4];
 #pragma unroll
-    for (int e = 0; e < 16; ++e) p[e & 3] += fast_exp2(fmaf(pend[e], scale_log2, -b[rb][e]));
-    cs += (p[0] + p[1]) + (p[2] + p[3]);
+    for (int e = 0; e < 4; ++e) p[e] = fast_exp2(fmaf(pend[e], scale_log2, -b[rb][e]));
+#pragma unroll
+    for (int e = 4; e < 16; ++e) p[e & 3] += fast_exp2(fmaf(pend[e], scale_log2, -b[rb][e]));
+    // The first row block of a key block starts its column sum.
+    const float t = (p[0] + p[1]) + (p[2] + p[3]);
+    cs = rb == 0 ? t : cs + t;
   };
   // Column sums of a finished key block into its tile's slot (lanes < 32).
   auto flush_block = [&](int slot, int blk) {

@@ -269,16 +269,19 @@ __global__ __launch_bounds__(kBlk) void k_pool(const ClipDev* __restrict__ clips
 // Band Gram entries of one frame: v_f.v_{f+d}, a_f.a_{f+d} for d < w, v_f.q
 // (and q.q for the first frame of the clip).  W bounds the partners a frame
 // needs (w, and 2 for the continuity cosine), so only 2W + 2 sums are formed
-// and reduced; entries are stored kMaxWindow apart.
+// and reduced; entries are stored kMaxWindow apart.  NT threads per frame:
+// 1024 when a launch has few frames (each frame's loads then spread over
+// four times the waves), 256 otherwise.
 // ---------------------------------------------------------------------------
-template <int W>
-__global__ __launch_bounds__(kBlk) void k_band(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
+constexpr int kBandWideFrames = 1024;  // below this many frames, 1024 threads per frame
+template <int W, int NT>
+__global__ __launch_bounds__(NT) void k_band(const ClipDev* __restrict__ clips, const FrameDev* __restrict__ frames,
                                                int dim, int w, const double* __restrict__ v,
                                                const double* __restrict__ a, const double* __restrict__ q,
                                                double* __restrict__ band_v, double* __restrict__ band_a,
                                                double* __restrict__ vq, double* __restrict__ qq) {
   constexpr int NA = 2 * W + 2;
-  __shared__ double sh[kBlk / 64][NA];
+  __shared__ double sh[NT / 64][NA];
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
   const int64_t f0 = c.frame_off + fr.f;
@@ -287,7 +290,7 @@ __global__ __launch_bounds__(kBlk) void k_band(const ClipDev* __restrict__ clips
   double acc[NA];
 #pragma unroll
   for (int i = 0; i < NA; ++i) acc[i] = 0.0;
-  for (int d = threadIdx.x; d < dim; d += kBlk) {
+  for (int d = threadIdx.x; d < dim; d += NT) {
     const double vf = v[f0 * dim + d], af = a[f0 * dim + d], qd = qv[d];
 #pragma unroll
     for (int dd = 0; dd < W; ++dd) {
@@ -309,7 +312,7 @@ __global__ __launch_bounds__(kBlk) void k_band(const ClipDev* __restrict__ clips
   const int i = threadIdx.x;
   if (i < NA) {
     double s = 0.0;
-    for (int ww = 0; ww < kBlk / 64; ++ww) s += sh[ww][i];
+    for (int ww = 0; ww < NT / 64; ++ww) s += sh[ww][i];
     if (i < W) {
       if (i < nd) band_v[f0 * kMaxWindow + i] = s;
     } else if (i < 2 * W) {
@@ -1348,6 +1351,7 @@ __global__ __launch_bounds__(kBlk) void k_dedup_sim(const ClipDev* __restrict__ 
   const T* x = xv + rowf * dim;
   const T* y = xv + rowa * dim;
   double acc = 0.0, o[8], q[8];
+#pragma unroll 4
   for (int d = lane * 8; d < dim; d += 64 * 8) {
     load8(x + d, o);
     load8(y + d, q);
@@ -1410,9 +1414,13 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
   if (nf > 0) {
     // Partners per frame: max(w, 2) <= kMaxWindow (checked on the host).
     const int wb = std::max(prm.window, 2);
-    auto band = wb <= 2 ? k_band<2> : wb <= 4 ? k_band<4> : wb <= 8 ? k_band<8> : k_band<kMaxWindow>;
-    hipLaunchKernelGGL(band, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dim, prm.window, dp.v, dp.a, dp.q,
-                       dp.band_v, dp.band_a, dp.vq, dp.qq);
+    const bool wide = nf < kBandWideFrames;
+    auto band = wide ? (wb <= 2 ? k_band<2, 1024> : wb <= 4 ? k_band<4, 1024> : wb <= 8 ? k_band<8, 1024>
+                                                                                      : k_band<kMaxWindow, 1024>)
+                     : (wb <= 2 ? k_band<2, kBlk> : wb <= 4 ? k_band<4, kBlk> : wb <= 8 ? k_band<8, kBlk>
+                                                                                      : k_band<kMaxWindow, kBlk>);
+    hipLaunchKernelGGL(band, dim3(nf), dim3(wide ? 1024 : kBlk), 0, s, dp.clips, dp.frames, dim, prm.window, dp.v,
+                       dp.a, dp.q, dp.band_v, dp.band_a, dp.vq, dp.qq);
     if ((st = launch_status("k_band")) != APACK_OK) return st;
   }
   if (prm.alignment == APACK_ALIGN_SPATIAL_CKA && nf > 0) {

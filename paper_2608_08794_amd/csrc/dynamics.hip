@@ -118,6 +118,27 @@ __device__ __forceinline__ double wave_max_f64(double v) {
   return fmax(x, y);
 }
 
+// Four sums at once, each over the 64 lanes: lane j (< 4) returns the sum
+// of v[j].  Lanes 2k and 2k+1 swap halves (the even lane keeps v[0] and
+// v[2], the odd one v[1] and v[3]), then lanes 4k..4k+3 do the same with
+// what they kept, so lane i holds a four-lane sum of v[i % 4]; rotations
+// by 4 and 8 lanes and the 16- and 32-lane swaps add the lanes with the
+// same i % 4.  The other lanes return partial sums.  All 64 lanes must be
+// active.
+__device__ __forceinline__ double wave_sum4(const double (&v)[4]) {
+  const int lane = threadIdx.x & 63;
+  const bool odd = lane & 1, hi2 = lane & 2;
+  const double x = (odd ? v[1] : v[0]) + dpp_f64<0xB1>(odd ? v[0] : v[1]);
+  const double y = (odd ? v[3] : v[2]) + dpp_f64<0xB1>(odd ? v[2] : v[3]);
+  double t = (hi2 ? y : x) + dpp_f64<0x4E>(hi2 ? x : y);
+  t += dpp_f64<0x124>(t);  // row_ror:4
+  t += dpp_f64<0x128>(t);  // row_ror:8
+  double a, b;
+  swap_pair_f64<true>(t, a, b);
+  swap_pair_f64<false>(a + b, a, b);
+  return a + b;
+}
+
 // Block-wide reductions over NT threads (sh holds NT / 64 words); every
 // thread gets the result.
 template <int NT = kBlk>
@@ -203,17 +224,28 @@ __global__ __launch_bounds__(kBlk) void k_pool(const ClipDev* __restrict__ clips
     hi = (((int64_t)fr.f + 1) * c.n_audio + c.n_frames - 1) / c.n_frames;
     const int64_t row0 = c.vis_off + (int64_t)fr.f * c.per_frame;
     const T* base = xv + row0 * dim + d0;
-#pragma unroll 4
-    for (int p = rg; p < c.per_frame; p += kPoolWaves) {
-      row8(base + (int64_t)p * dim, o);
-      double s2 = 0.0;
+    // The wave's rows rg, rg + 4, ... four at a time: the four loads are
+    // issued together (a row past the frame re-reads its last row and adds
+    // nothing), and the four sums of squares are reduced together.
+    const int P = c.per_frame;
+    for (int p0 = rg; p0 < P; p0 += 4 * kPoolWaves) {
+      double o4[4][8], s2[4];
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        av[e] += o[e];
-        s2 = fma(o[e], o[e], s2);
+      for (int j = 0; j < 4; ++j) row8(base + (int64_t)min(p0 + j * kPoolWaves, P - 1) * dim, o4[j]);
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        s2[j] = 0.0;
+        if (p0 + j * kPoolWaves < P) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            av[e] += o4[j][e];
+            s2[j] = fma(o4[j][e], o4[j][e], s2[j]);
+          }
+        }
       }
-      s2 = wave_sum(s2);
-      if (lane == 0) sq[row0 + p] = s2;
+      const double t = wave_sum4(s2);
+      const int p = p0 + lane * kPoolWaves;
+      if (lane < 4 && p < P) sq[row0 + p] = t;
     }
     // A row shared by two bins gets the same value from both.
     for (int64_t r = lo + rg; r < hi; r += kPoolWaves) {

@@ -364,7 +364,10 @@ __device__ __forceinline__ double band_at(const double* band, int64_t f0, int i,
 
 // ---------------------------------------------------------------------------
 // Eq. 1 per frame over its clamped window, the clip mean and the gate.
+// W >= w bounds the window, so the loops unroll and the row means stay in
+// registers; the Gram entries are read from the band where they are used.
 // ---------------------------------------------------------------------------
+template <int W>
 __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w, double tau, int alignment,
                                               const double* __restrict__ band_v, const double* __restrict__ band_a,
                                               double* __restrict__ cka, float* __restrict__ frame_cka,
@@ -385,32 +388,40 @@ __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w
     int lo = 0;
     if (F > w) lo = min(max(f - w / 2, 0), F - w);
     // Centred Grams K = H G H of the window rows lo .. lo+ww-1.
-    double ga[kMaxWindow][kMaxWindow], gv[kMaxWindow][kMaxWindow];
-    double ra[kMaxWindow], rv[kMaxWindow], ta = 0.0, tv = 0.0;
-    for (int i = 0; i < ww; ++i) {
+    double ra[W], rv[W], ta = 0.0, tv = 0.0;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
       ra[i] = rv[i] = 0.0;
-      for (int j = 0; j < ww; ++j) {
-        ga[i][j] = band_at(band_a, f0, lo + i, lo + j);
-        gv[i][j] = band_at(band_v, f0, lo + i, lo + j);
-        ra[i] += ga[i][j];
-        rv[i] += gv[i][j];
+      if (i < ww) {
+#pragma unroll
+        for (int j = 0; j < W; ++j) {
+          if (j < ww) {
+            ra[i] += band_at(band_a, f0, lo + i, lo + j);
+            rv[i] += band_at(band_v, f0, lo + i, lo + j);
+          }
+        }
+        ra[i] /= ww;
+        rv[i] /= ww;
+        ta += ra[i];
+        tv += rv[i];
       }
-      ra[i] /= ww;
-      rv[i] /= ww;
-      ta += ra[i];
-      tv += rv[i];
     }
     ta /= ww;
     tv /= ww;
     double num = 0.0, na = 0.0, nv = 0.0;
-    for (int i = 0; i < ww; ++i)
-      for (int j = 0; j < ww; ++j) {
-        const double ka = ga[i][j] - ra[i] - ra[j] + ta;
-        const double kv = gv[i][j] - rv[i] - rv[j] + tv;
+#pragma unroll
+    for (int i = 0; i < W; ++i) {
+      if (i >= ww) continue;
+#pragma unroll
+      for (int j = 0; j < W; ++j) {
+        if (j >= ww) continue;
+        const double ka = band_at(band_a, f0, lo + i, lo + j) - ra[i] - ra[j] + ta;
+        const double kv = band_at(band_v, f0, lo + i, lo + j) - rv[i] - rv[j] + tv;
         num += ka * kv;
         na += ka * ka;
         nv += kv * kv;
       }
+    }
     const double den = sqrt(na) * sqrt(nv);
     const double cf = den == 0.0 ? 0.0 : num / den;
     cka[f0 + f] = cf;
@@ -1446,9 +1457,9 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
   if (nf > 0) {
     // Partners per frame: max(w, 2) <= kMaxWindow (checked on the host).
     const int wb = std::max(prm.window, 2);
-    const bool wide = nf < kBandWideFrames;
-    auto band = wide ? (wb <= 2 ? k_band<2, 1024> : wb <= 4 ? k_band<4, 1024> : wb <= 8 ? k_band<8, 1024>
-                                                                                      : k_band<kMaxWindow, 1024>)
+    // (Windows past 8 keep 256 threads: 1024 would leave too few registers for their sums.)
+    const bool wide = nf < kBandWideFrames && wb <= 8;
+    auto band = wide ? (wb <= 2 ? k_band<2, 1024> : wb <= 4 ? k_band<4, 1024> : k_band<8, 1024>)
                      : (wb <= 2 ? k_band<2, kBlk> : wb <= 4 ? k_band<4, kBlk> : wb <= 8 ? k_band<8, kBlk>
                                                                                       : k_band<kMaxWindow, kBlk>);
     hipLaunchKernelGGL(band, dim3(nf), dim3(wide ? 1024 : kBlk), 0, s, dp.clips, dp.frames, dim, prm.window, dp.v,
@@ -1464,8 +1475,9 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
                        pl.spatial_tiles, dp.spatial, dp.cka);
     if ((st = launch_status("k_spatial_reduce")) != APACK_OK) return st;
   }
-  hipLaunchKernelGGL(k_cka, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm.window, prm.tau_gate, prm.alignment,
-                     dp.band_v, dp.band_a, dp.cka, frame_cka, gate_fired);
+  auto cka = prm.window <= 2 ? k_cka<2> : prm.window <= 4 ? k_cka<4> : prm.window <= 8 ? k_cka<8> : k_cka<kMaxWindow>;
+  hipLaunchKernelGGL(cka, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm.window, prm.tau_gate, prm.alignment, dp.band_v,
+                     dp.band_a, dp.cka, frame_cka, gate_fired);
   if ((st = launch_status("k_cka")) != APACK_OK) return st;
   if (n_vis + n_aud > 0) {
     hipLaunchKernelGGL(k_norms, dim3((unsigned)((n_vis + n_aud + kBlk - 1) / kBlk)), dim3(kBlk), 0, s, n_vis, n_aud,

@@ -176,6 +176,16 @@ def test_long_clips_on_both_plan_paths():
     _compare(case, _run(case), want)
 
 
+@pytest.mark.parametrize("window", [1, 2, 5, 9, 16])
+def test_window_sizes(window):
+    """Every window bucket of the band and CKA kernels (up to the largest
+    window, 16), on a 20-frame clip."""
+    case = W.dynamics_small("offset", seed=61, frames=20, per_frame=16, audio=100, window=window)
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
 @pytest.mark.parametrize("r_pre", [1.0, 0.05, 0.6])
 def test_budget_extremes(r_pre):
     case = W.dynamics_small("offset", seed=31)

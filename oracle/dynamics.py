@@ -15,7 +15,14 @@ step:
 * window: exactly w consecutive frames, centred on f (the extra frame of an
   even w lies in the past), clamped inside [0, F); all F frames when F < w;
 * centring: subtract each window stack's column means (linear CKA);
-* a zero denominator or zero-norm cosine gives 0;
+* a degenerate window gives 0: one whose centred Gram has a Frobenius norm
+  of at most CKA_DEGENERATE times the trace of the raw Gram, on the audio
+  or the visual side (a window of repeated frames, or of zero frames, has
+  no variation for Eq. 1 to compare; its centred Gram is pure rounding);
+* cosines are dot(x, y) / sqrt(dot(x, x) dot(y, y)) with every dot product
+  summed by the same rule, so a token and a bitwise copy of it have cosine
+  exactly 1 (the square root of a correctly rounded square is its argument);
+  a zero-norm cosine gives 0;
 * gate: fires when the clip-mean CKA is strictly below tau (Eq. 2);
 * the gate blends the CKA term, and the frame score is
   s_f = gamma * u_f + (1 - gamma) * alpha_f, with alpha_f the Eq. 2 blend;
@@ -82,6 +89,10 @@ DEFAULTS = {
 
 ALIGNMENTS = ("gated_cka", "cka", "av_cosine", "spatial_cka")
 
+# A centred Gram whose Frobenius norm is at most this fraction of the raw
+# Gram's trace marks a degenerate CKA input (see the module docstring).
+CKA_DEGENERATE = 1e-8
+
 
 # --------------------------------------------------------------------------
 # Coarse pass: frame-level pairs (a_f, v_f)
@@ -115,43 +126,68 @@ def window_rows(f, n_frames, w):
     return lo, lo + w
 
 
-def linear_cka(a, v):
+def degenerate_ratio(k_centred, raw_trace):
+    """||K||_F / tr(G) of a centred Gram K against its raw Gram G (0 when
+    the raw trace is 0: the rows are all zero)."""
+    nk = math.sqrt(float(np.sum(k_centred * k_centred)))
+    return nk / raw_trace if raw_trace > 0.0 else 0.0
+
+
+def degenerate_margin(ratio):
+    """Distance of a degeneracy ratio from CKA_DEGENERATE as |ln(ratio / eps)|
+    (infinite for an exact 0)."""
+    return math.inf if ratio == 0.0 else abs(math.log(ratio / CKA_DEGENERATE))
+
+
+def linear_cka(a, v, with_margin=False):
     """Eq. 1 on column-centred stacks A, V in R^{w x d}.
 
     ||V^T A||_F^2 / (||A^T A||_F ||V^T V||_F) equals
     <A A^T, V V^T>_F / (||A A^T||_F ||V V^T||_F) by the trace identity
     tr(A^T V V^T A) = tr(V V^T A A^T); the w x w form is evaluated here.
+    A degenerate side (centred Gram at most CKA_DEGENERATE of the raw
+    trace) gives 0.  With ``with_margin`` also returns the degeneracy
+    decision's margin.
     """
+    tr_a, tr_v = float(np.sum(a * a)), float(np.sum(v * v))
     a = a - a.mean(axis=0, keepdims=True)
     v = v - v.mean(axis=0, keepdims=True)
     ka = a @ a.T
     kv = v @ v.T
-    den = math.sqrt(float(np.sum(ka * ka))) * math.sqrt(float(np.sum(kv * kv)))
-    if den == 0.0:
-        return 0.0
-    return float(np.sum(ka * kv)) / den
+    ra, rv = degenerate_ratio(ka, tr_a), degenerate_ratio(kv, tr_v)
+    margin = min(degenerate_margin(ra), degenerate_margin(rv))
+    if ra <= CKA_DEGENERATE or rv <= CKA_DEGENERATE:
+        c = 0.0
+    else:
+        c = float(np.sum(ka * kv)) / (math.sqrt(float(np.sum(ka * ka))) * math.sqrt(float(np.sum(kv * kv))))
+    return (c, margin) if with_margin else c
 
 
-def frame_cka(a, v, w):
+def frame_cka(a, v, w, with_margin=False):
     """c_f for every frame (Eq. 1 over the clamped window of frame f)."""
     n = a.shape[0]
     out = np.zeros(n, dtype=np.float64)
+    margin = math.inf
     for f in range(n):
         lo, hi = window_rows(f, n, w)
-        out[f] = linear_cka(a[lo:hi], v[lo:hi])
-    return out
+        out[f], m = linear_cka(a[lo:hi], v[lo:hi], with_margin=True)
+        margin = min(margin, m)
+    return (out, margin) if with_margin else out
 
 
 # --------------------------------------------------------------------------
 # Gated fine pass (Eq. 2)
 # --------------------------------------------------------------------------
 
-def spatial_cka(xv, xa, n_frames, per_frame):
+def spatial_cka(xv, xa, n_frames, per_frame, with_margin=False):
     """Per-frame spatial CKA at w = 1 (reading above): linear CKA between the
     feature covariances of the frame's P visual tokens and of the audio
-    tokens of its adaptive-pool bin, each centred by its own mean."""
+    tokens of its adaptive-pool bin, each centred by its own mean.  A
+    degenerate side (as in linear_cka: a bin of one token, or a frame of
+    identical tokens) gives 0."""
     lo_hi = audio_bins(xa.shape[0], n_frames)
     out = np.zeros(n_frames)
+    margin = math.inf
     for f in range(n_frames):
         v = xv[f * per_frame:(f + 1) * per_frame]
         lo, hi = lo_hi[f]
@@ -160,18 +196,47 @@ def spatial_cka(xv, xa, n_frames, per_frame):
             continue
         vc = v - v.mean(axis=0)
         ac = a - a.mean(axis=0)
+        kaa, kvv = ac @ ac.T, vc @ vc.T
+        ra = degenerate_ratio(kaa, float(np.sum(a * a)))
+        rv = degenerate_ratio(kvv, float(np.sum(v * v)))
+        margin = min(margin, degenerate_margin(ra), degenerate_margin(rv))
+        if ra <= CKA_DEGENERATE or rv <= CKA_DEGENERATE:
+            continue
         num = float(np.sum((ac @ vc.T) ** 2))
-        den = float(np.linalg.norm(ac @ ac.T)) * float(np.linalg.norm(vc @ vc.T))
-        out[f] = num / den if den != 0.0 else 0.0
-    return out
+        out[f] = num / (float(np.linalg.norm(kaa)) * float(np.linalg.norm(kvv)))
+    return (out, margin) if with_margin else out
+
+
+def dot(x, y):
+    """x . y summed by one rule for every pair of vectors (NumPy's pairwise
+    sum of the elementwise products): equal vectors give equal sums."""
+    return float(np.sum(x * y))
 
 
 def cosine(x, y):
-    nx = math.sqrt(float(x @ x))
-    ny = math.sqrt(float(y @ y))
+    """dot(x, y) / sqrt(dot(x, x) dot(y, y)); 0 when either norm is 0.  A
+    vector and a bitwise copy of it give exactly 1."""
+    nx, ny = dot(x, x), dot(y, y)
     if nx == 0.0 or ny == 0.0:
         return 0.0
-    return float(x @ y) / (nx * ny)
+    return dot(x, y) / math.sqrt(nx * ny)
+
+
+def cosine_gram(x):
+    """Cosines of every pair of rows of x, S_ij = G_ij / sqrt(G_ii G_jj) from
+    the Gram G of the distinct rows (a bitwise-repeated row is the same row,
+    so its cosine with its copy is exactly 1), made exactly symmetric; 0
+    where a norm is 0."""
+    uniq, inv = np.unique(x, axis=0, return_inverse=True)
+    g = uniq @ uniq.T
+    g = np.triu(g) + np.triu(g, 1).T
+    n = np.diag(g).copy()
+    den = np.sqrt(np.outer(n, n))
+    s = np.zeros_like(g)
+    nz = den > 0.0
+    s[nz] = g[nz] / den[nz]
+    inv = np.asarray(inv).reshape(-1)
+    return s[np.ix_(inv, inv)]
 
 
 def unit_rows(x):
@@ -187,13 +252,17 @@ def direct_distance(xv, xa, n_frames, per_frame, chunk=4096):
     """d_f = 1 - mean over frame f's tokens of max_j cos(x_V, x_A[j]).
 
     Returns (d [F], best [F*P]) where best holds each visual token's maximum
-    cosine over all audio tokens.
+    cosine over all audio tokens.  The maximum is computed once per distinct
+    visual token, so bitwise-repeated tokens (a frame that repeats another)
+    get the same value.
     """
     ua = unit_rows(xa)
-    best = np.empty(xv.shape[0], dtype=np.float64)
-    for i in range(0, xv.shape[0], chunk):
-        uv = unit_rows(xv[i:i + chunk])
-        best[i:i + chunk] = (uv @ ua.T).max(axis=1)
+    uniq, inv = np.unique(xv, axis=0, return_inverse=True)
+    best_u = np.empty(uniq.shape[0], dtype=np.float64)
+    for i in range(0, uniq.shape[0], chunk):
+        uv = unit_rows(uniq[i:i + chunk])
+        best_u[i:i + chunk] = (uv @ ua.T).max(axis=1)
+    best = best_u[np.asarray(inv).reshape(-1)]
     d = 1.0 - best.reshape(n_frames, per_frame).mean(axis=1)
     return d, best
 
@@ -291,6 +360,28 @@ def segment_scores(r, seg, lam):
     return g
 
 
+def frame_alpha(c, dhat, fired, beta):
+    """The alignment term of frame f (Eq. 2): alpha_f = (1 - beta) c_f +
+    beta (1 - dhat_f) when the gate fired, else c_f."""
+    c = np.asarray(c, dtype=np.float64)
+    if not fired:
+        return c.copy()
+    return (1.0 - beta) * c + beta * (1.0 - np.asarray(dhat, dtype=np.float64))
+
+
+def frame_scores(alpha, r, seg, gamma, lam):
+    """Segment scores and frame scores (Eq. 3; Algorithm 1, scoring steps).
+
+    g_m from segment_scores, the broadcast u_f = g_m(f) / max_m g_m and the
+    frame score s_f = gamma u_f + (1 - gamma) alpha_f.  Returns (g, u, s).
+    """
+    seg = np.asarray(seg)
+    g = segment_scores(np.asarray(r, dtype=np.float64), seg, lam)
+    u = g[seg] / float(g.max()) if seg.size else np.zeros(0)
+    s = gamma * u + (1.0 - gamma) * np.asarray(alpha, dtype=np.float64)
+    return g, u, s
+
+
 # --------------------------------------------------------------------------
 # Budgets (Eq. 4; Algorithm 1 sixth step; supplement pre-LLM details)
 # --------------------------------------------------------------------------
@@ -374,6 +465,31 @@ def _cut_gap(desc, k):
     return float(kth - below[0]) if below else math.inf
 
 
+def budgets(bv, g, s, seg, per_frame):
+    """Segment and frame budgets (Eq. 4; Algorithm 1, allocation step).
+
+    B_m apportions the visual budget bv by the segment scores g_m with caps
+    |G_m| P; then k_f apportions B_m over the frames of segment m by their
+    frame scores s_f with caps P.  Returns (B [n_seg], k [F], margins) with
+    the margins of the two apportionments.
+    """
+    seg = np.asarray(seg)
+    n_seg = len(g)
+    seg_len = np.array([int(np.sum(seg == m)) for m in range(n_seg)], dtype=np.int64)
+    if n_seg:
+        bm, m_seg = apportion(bv, g, seg_len * per_frame)
+    else:
+        bm, m_seg = np.zeros(0, np.int64), math.inf
+    kf = np.zeros(seg.size, dtype=np.int64)
+    m_frame = math.inf
+    for m in range(n_seg):
+        frames = np.flatnonzero(seg == m)
+        alloc, mg = apportion(int(bm[m]), np.asarray(s)[frames], np.full(frames.size, per_frame))
+        kf[frames] = alloc
+        m_frame = min(m_frame, mg)
+    return bm, kf, {"segment_budget": m_seg, "frame_budget": m_frame}
+
+
 # --------------------------------------------------------------------------
 # Token selection (Algorithm 1 loop over segments)
 # --------------------------------------------------------------------------
@@ -389,8 +505,7 @@ def dafps(x, k, density_k, cover_thresh, power):
     """
     p = x.shape[0]
     k = min(k, p)
-    u = unit_rows(x)
-    s = u @ u.T
+    s = cosine_gram(x)
     margin = math.inf
     rho = np.zeros(p, dtype=np.float64)
     for i in range(p):
@@ -472,7 +587,10 @@ def score_sequence(xv, xa, xq, n_frames, per_frame, params=None):
     mode = p["alignment"]
     if mode not in ALIGNMENTS:
         raise ValueError(f"unknown alignment {mode!r}")
-    c = spatial_cka(xv, xa, F, P) if mode == "spatial_cka" else frame_cka(a, v, p["window"])
+    if mode == "spatial_cka":
+        c, margins["cka_degenerate"] = spatial_cka(xv, xa, F, P, with_margin=True)
+    else:
+        c, margins["cka_degenerate"] = frame_cka(a, v, p["window"], with_margin=True)
     cbar = float(c.mean()) if F else 0.0
     if mode in ("gated_cka", "spatial_cka"):
         fired = bool(F > 0 and cbar < p["tau_gate"])
@@ -484,11 +602,10 @@ def score_sequence(xv, xa, xq, n_frames, per_frame, params=None):
     if fired:
         d, _ = direct_distance(xv, xa, F, P)
         dhat = minmax(d)
-        alpha = (1.0 - beta) * c + beta * (1.0 - dhat)
     else:
         d = np.zeros(F)
         dhat = np.zeros(F)
-        alpha = c.copy()
+    alpha = frame_alpha(c, dhat, fired, beta)
 
     # Segmentation.
     cs = continuity(v)
@@ -497,23 +614,13 @@ def score_sequence(xv, xa, xq, n_frames, per_frame, params=None):
 
     # Segment score, broadcast and frame score (Eq. 3; Algorithm 1).
     r = relevance(v, qbar)
-    g = segment_scores(r, seg, p["lambda_seg"])
-    u = g[seg] / float(g.max()) if F else np.zeros(0)
-    s = p["gamma"] * u + (1.0 - p["gamma"]) * alpha
+    g, u, s = frame_scores(alpha, r, seg, p["gamma"], p["lambda_seg"])
 
     # Budgets (Eq. 4 at segment level, then frames within each segment).
     bv = visual_budget(p["r_pre"], n_audio, F * P)
     n_seg = g.size
-    seg_len = np.array([int(np.sum(seg == m)) for m in range(n_seg)], dtype=np.int64)
-    bm, margins["segment_budget"] = apportion(bv, g, seg_len * P) if n_seg else (np.zeros(0, np.int64), math.inf)
-    kf = np.zeros(F, dtype=np.int64)
-    mfb = math.inf
-    for m in range(n_seg):
-        frames = np.flatnonzero(seg == m)
-        alloc, mg = apportion(int(bm[m]), s[frames], np.full(frames.size, P))
-        kf[frames] = alloc
-        mfb = min(mfb, mg)
-    margins["frame_budget"] = mfb
+    bm, kf, mb = budgets(bv, g, s, seg, P)
+    margins.update(mb)
 
     # Token selection: DA-FPS on each anchor, dedup on the other frames.
     keep = np.zeros(F * P, dtype=bool)

@@ -424,3 +424,213 @@ def test_alignment_modes_select_their_frame_scores():
     np.testing.assert_array_equal(sp["cka"], OD.spatial_cka(xv, xa, s.n_frames, s.per_frame))
     with pytest.raises(ValueError):
         OD.score_sequence(xv, xa, xq, s.n_frames, s.per_frame, dict(case.params, alignment="ot"))
+
+
+# -- frame scores and budgets, composed by hand (Eq. 2-4; Algorithm 1) -------
+#
+# Five frames, two tokens per frame (P = 2), segments G_0 = {0, 1, 2} and
+# G_1 = {3, 4}; lambda = 0.5, gamma = 0.9, beta = 0.9; N_A = 5 audio tokens
+# and R_pre = 0.8, so B_v = ceil(0.8 * (5 + 10)) - 5 = 12 - 5 = 7.
+#
+#   r = (0.5, 0.9, 0.7 | 0.3, 0.6)
+#   g_0 = sqrt(3) (0.5 * 0.9 + 0.5 * 0.7) = 0.8 sqrt(3)   = 1.3856406460551018
+#   g_1 = sqrt(2) (0.5 * 0.6 + 0.5 * 0.45) = 0.525 sqrt(2) = 0.7424621202458749
+#   u = (1, 1, 1, g_1/g_0, g_1/g_0),  g_1/g_0 = 0.65625 sqrt(2/3) = 0.5358258812338203
+#   c = (0.2, 0.2, 0.6, 0.9, 0.1)       (frames 0 and 1 share a clamped window)
+#   dhat = (0, 0.5, 1, 0.25, 0.75)
+#
+# Segment budgets (Eq. 4) by g with caps (6, 4): quotas 7 g_m / (g_0 + g_1)
+# = (4.5578, 2.4422) -> floors (4, 2), the one leftover unit to the larger
+# fractional part .5578 -> B = (5, 2).  The same with or without the gate.
+
+_HAND = dict(r=[0.5, 0.9, 0.7, 0.3, 0.6], c=[0.2, 0.2, 0.6, 0.9, 0.1],
+             dhat=[0.0, 0.5, 1.0, 0.25, 0.75], seg=[0, 0, 0, 1, 1])
+_G = [1.3856406460551018, 0.7424621202458749]
+_U1 = 0.5358258812338203
+
+
+def _hand(fired):
+    alpha = OD.frame_alpha(_HAND["c"], _HAND["dhat"], fired, 0.9)
+    g, u, s = OD.frame_scores(alpha, _HAND["r"], np.array(_HAND["seg"]), 0.9, 0.5)
+    bv = OD.visual_budget(0.8, 5, 5 * 2)
+    bm, kf, _ = OD.budgets(bv, g, s, np.array(_HAND["seg"]), 2)
+    return bv, alpha, g, u, s, bm, kf
+
+
+def test_frame_scores_and_budgets_by_hand_gate_off():
+    # alpha = c.  s = 0.9 u + 0.1 c:
+    #   (0.9 + 0.02, 0.9 + 0.02, 0.9 + 0.06, 0.9 * 0.5358258812 + 0.09, ... + 0.01)
+    # Frames of G_0 share B_0 = 5 by s, caps 2: quotas 5 s / 2.8 =
+    # (1.642857, 1.642857, 1.714286) -> floors (1, 1, 1); two leftover units
+    # to the largest fractional parts: frame 2 (.714), then frame 0 (ties
+    # with frame 1 at .642857 go to the lower index) -> (2, 1, 2).
+    # G_1: B_1 = 2, quotas 2 s / 1.0644865862 = (1.07515, 0.92485) -> (1, 1).
+    bv, alpha, g, u, s, bm, kf = _hand(False)
+    assert bv == 7
+    np.testing.assert_allclose(alpha, [0.2, 0.2, 0.6, 0.9, 0.1], rtol=0, atol=0)
+    np.testing.assert_allclose(g, _G, rtol=1e-14)
+    np.testing.assert_allclose(u, [1.0, 1.0, 1.0, _U1, _U1], rtol=1e-14)
+    np.testing.assert_allclose(s, [0.92, 0.92, 0.96, 0.5722432931104383, 0.4922432931104383], rtol=1e-14)
+    assert bm.tolist() == [5, 2]
+    assert kf.tolist() == [2, 1, 2, 1, 1]
+
+
+def test_frame_scores_and_budgets_by_hand_gate_fired():
+    # alpha = 0.1 c + 0.9 (1 - dhat) = (0.92, 0.47, 0.06, 0.765, 0.235);
+    # s = 0.9 u + 0.1 alpha = (0.992, 0.947, 0.906, 0.4822432931 + 0.0765,
+    # 0.4822432931 + 0.0235).  G_0: quotas 5 s / 2.845 =
+    # (1.743409, 1.664323, 1.592267) -> floors (1, 1, 1), leftover units to
+    # frames 0 and 1 -> (2, 2, 1).  G_1: quotas (1.04978, 0.95022) -> (1, 1).
+    bv, alpha, g, u, s, bm, kf = _hand(True)
+    np.testing.assert_allclose(alpha, [0.92, 0.47, 0.06, 0.765, 0.235], rtol=1e-14)
+    np.testing.assert_allclose(g, _G, rtol=1e-14)
+    np.testing.assert_allclose(s, [0.992, 0.947, 0.906, 0.5587432931104383, 0.5057432931104383], rtol=1e-14)
+    assert bm.tolist() == [5, 2]
+    assert kf.tolist() == [2, 2, 1, 1, 1]
+
+
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_score_sequence_composes_the_hand_pinned_steps(structure):
+    """The whole scorer's frame scores and budgets are the composition pinned
+    above, applied to its own CKA, distance, relevance and segments."""
+    case = W.dynamics_small(structure)
+    s = case.seqs[0]
+    r = OD.score_sequence(widen(case.xv, "bf16"), widen(case.xa, "bf16"), widen(case.xq, "bf16"),
+                          s.n_frames, s.per_frame, case.params)
+    alpha = OD.frame_alpha(r["cka"], r["dhat"], r["gate"], OD.DEFAULTS["beta"])
+    g, u, sc = OD.frame_scores(alpha, r["relevance"], r["segment"], OD.DEFAULTS["gamma"], 0.5)
+    bm, kf, _ = OD.budgets(r["visual_budget"], g, sc, r["segment"], s.per_frame)
+    np.testing.assert_array_equal(r["score"], sc)
+    np.testing.assert_array_equal(r["segment_budget"], bm)
+    np.testing.assert_array_equal(r["frame_budget"], kf)
+
+
+# -- degenerate inputs: repeated frames, zero tokens, duplicate tokens -------
+
+
+def test_repeated_rows_make_a_degenerate_window():
+    rng = np.random.default_rng(60)
+    # Column means of three copies of a row are not always the row itself,
+    # so the centred stack is rounding noise rather than 0; the window is
+    # degenerate and its CKA is defined as 0.
+    noisy = 0
+    for _ in range(50):
+        x = rng.standard_normal(40)
+        a = np.stack([x, x, x])
+        v = rng.standard_normal((3, 40))
+        noisy += int(np.any(a - a.mean(axis=0) != 0))
+        assert OD.linear_cka(a, v) == 0.0
+        assert OD.linear_cka(v, a) == 0.0
+    assert noisy > 0
+    assert OD.linear_cka(np.zeros((3, 5)), rng.standard_normal((3, 5))) == 0.0
+    # Variation well above the bound is compared by Eq. 1 as usual; far
+    # below it the window counts as degenerate.
+    base, trend = rng.standard_normal(30), rng.standard_normal(30)
+    v = rng.standard_normal((4, 30))
+    a = base + 1e-2 * np.outer(np.arange(4.0), trend)
+    assert OD.linear_cka(a, v) == pytest.approx(_eq1_feature_space(a, v), rel=1e-9)
+    a = base + 1e-7 * np.outer(np.arange(4.0), trend)
+    c, margin = OD.linear_cka(a, v, with_margin=True)
+    assert c == 0.0 and margin > 1.0
+
+
+def test_static_run_gives_zero_frame_cka():
+    rng = np.random.default_rng(61)
+    a, v = rng.standard_normal((12, 8)), rng.standard_normal((12, 8))
+    v[4:9] = v[4]
+    c = OD.frame_cka(a, v, 3)
+    # Windows lying inside frames 4..8: those of frames 5, 6, 7.
+    assert c[5] == c[6] == c[7] == 0.0
+    assert np.all(c[[0, 1, 2, 3, 10, 11]] != 0.0)
+
+
+def test_cosine_of_a_bitwise_copy_is_exactly_one():
+    rng = np.random.default_rng(62)
+    x = widen(W.to_bf16_bits(rng.standard_normal((400, 3584)).astype(np.float32)), "bf16")
+    sqrt_twice = 0
+    for row in x:
+        assert OD.cosine(row, row.copy()) == 1.0
+        n = math.sqrt(float(row @ row))
+        sqrt_twice += int(float(row @ row) / (n * n) != 1.0)
+    assert sqrt_twice > 0   # the sqrt(n) sqrt(n) form misses 1 on some rows
+    assert OD.cosine(x[0], np.zeros(3584)) == 0.0
+    assert OD.cosine(x[0], x[1]) == pytest.approx(float(x[0] @ x[1]) / np.linalg.norm(x[0]) / np.linalg.norm(x[1]),
+                                                  rel=1e-13)
+
+
+def test_cosine_gram_with_duplicates_and_zero_rows():
+    rng = np.random.default_rng(63)
+    x = rng.standard_normal((10, 50))
+    x[[3, 7]] = x[1]
+    x[5] = 0.0
+    s = OD.cosine_gram(x)
+    assert np.array_equal(s, s.T)
+    for i in (1, 3, 7):
+        for j in (1, 3, 7):
+            assert s[i, j] == 1.0
+    assert np.all(s[5] == 0.0) and np.all(s[:, 5] == 0.0)
+    u = x / np.maximum(np.linalg.norm(x, axis=1, keepdims=True), 1e-300)
+    np.testing.assert_allclose(s, u @ u.T, rtol=1e-13, atol=1e-15)
+
+
+def test_dedup_of_a_repeated_frame_takes_zero_tokens_then_lowest_positions():
+    rng = np.random.default_rng(64)
+    anchor = widen(W.to_bf16_bits(rng.standard_normal((16, 64)).astype(np.float32)), "bf16")
+    anchor[6] = 0.0
+    frame = anchor.copy()
+    frame[11] = 0.0
+    for k in range(17):
+        picks, margin = OD.dedup(frame, anchor, k)
+        assert picks == sorted(([6, 11] + [p for p in range(16) if p not in (6, 11)])[:k])
+        assert margin >= 1.0   # only exact ties sit at a cut, or the gap from 0 to 1
+
+
+def test_dafps_duplicate_tokens_tie_to_the_lowest_index():
+    rng = np.random.default_rng(65)
+    x = rng.standard_normal((12, 6)) + 2.0     # all cosines positive
+    x[[4, 8, 9]] = x[2]
+    picks, _ = OD.dafps(x, 12, 3, 0.8, 0.5)
+    # The copies are one point: once one of them is picked, the others have
+    # distance 0 to the picked set and come last, in index order.
+    first = min(i for i in (2, 4, 8, 9) if i in picks[:-3])
+    assert picks[-3:] == sorted({2, 4, 8, 9} - {first})
+    assert sorted(picks) == list(range(12))
+
+
+def test_direct_distance_of_repeated_frames_is_equal():
+    rng = np.random.default_rng(66)
+    xv = rng.standard_normal((6 * 5, 9))
+    xv[10:15] = xv[5:10]
+    xv[20:25] = xv[5:10]
+    d, best = OD.direct_distance(xv, rng.standard_normal((7, 9)), 6, 5, chunk=4)
+    assert d[1] == d[2] == d[4]
+    np.testing.assert_array_equal(best[5:10], best[20:25])
+
+
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_scorer_on_degenerate_inputs(structure):
+    """Zero frame, static scene, duplicate and zero tokens (the edge clip):
+    planted segments recovered (frame 0 alone), zero CKA inside the static
+    scene, and the static non-anchor frames keep the zero token's position
+    and then the lowest positions, with every decision certified."""
+    case = W.dynamics_edge(structure)
+    s = case.seqs[0]
+    r = OD.score_sequence(widen(case.xv, "bf16"), widen(case.xa, "bf16"), widen(case.xq, "bf16"),
+                          s.n_frames, s.per_frame, case.params)
+    starts = [0] + (np.flatnonzero(np.diff(r["segment"]) != 0) + 1).tolist()
+    assert starts == s.seg_starts
+    assert r["gate"] == (structure == "offset")
+    xv = case.xv.reshape(s.n_frames, s.per_frame, -1)
+    static = [m for m in range(1, len(starts))
+              if all(np.array_equal(xv[f], xv[starts[m]])
+                     for f in range(starts[m], (starts + [s.n_frames])[m + 1]))]
+    assert len(static) == 1
+    s0, s1 = starts[static[0]], (starts + [s.n_frames])[static[0] + 1]
+    assert np.all(r["cka"][s0 + 1:s1 - 1] == 0.0)
+    kept = r["kept"]
+    for f in range(s0 + 1, s1):
+        got = (kept[(kept >= f * s.per_frame) & (kept < (f + 1) * s.per_frame)] - f * s.per_frame).tolist()
+        k = int(r["frame_budget"][f])
+        assert got == sorted(([3] + [p for p in range(s.per_frame) if p != 3])[:k])
+    for key, m in r["margins"].items():
+        assert m > (1.0 if key == "cka_degenerate" else 1e-9), key

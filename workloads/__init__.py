@@ -514,6 +514,45 @@ def dynamics_small(structure="offset", seed=7, dim=64, frames=24, per_frame=16,
                         [seq], {"window": window, "r_pre": 0.5})
 
 
+def dynamics_edge(structure="offset", seed=75, dim=64, frames=64, per_frame=16, audio=600,
+                  n_query=8, window=3):
+    """A clip with the scorer's degenerate inputs, built on the planted-scene
+    recipe (raw bits are copied, so repeats are bitwise):
+
+    - frame 0 is all zeros (zero-norm frame: its own segment, cosines 0);
+    - the shortest scene after the first is static: every frame repeats the
+      scene's first frame, and its audio rows repeat one audio token, so its
+      CKA windows have no variation and its non-anchor frames equal their
+      anchor;
+    - the first dynamic anchor repeats its token 0 in tokens 1-4 (exact
+      duplicates inside a DA-FPS frame);
+    - single zero tokens in the static anchor, in a dynamic anchor and in a
+      non-anchor frame, and two zero audio rows.
+    """
+    rng = np.random.default_rng(seed + (0 if structure == "shared" else 500))
+    xv, xa, xq, starts = av_clip(rng, frames, per_frame, audio, n_query, dim, structure)
+    xv = to_bf16_bits(xv).reshape(frames, per_frame, dim)
+    xa = to_bf16_bits(xa)
+    lens = [b - a for a, b in zip(starts, starts[1:] + [frames])]
+    st = min(range(1, len(starts)), key=lambda m: (lens[m], m))
+    s0, L = starts[st], lens[st]
+    xv[s0][3] = 0                                   # zero token in the static anchor
+    xv[s0 + 1:s0 + L] = xv[s0]
+    af = np.minimum((np.arange(audio) * frames) // audio, frames - 1)
+    rows = np.flatnonzero((af >= s0) & (af < s0 + L))
+    xa[rows] = xa[rows[0]]
+    dyn = starts[1] if st != 1 else starts[2]
+    xv[dyn][1:5] = xv[dyn][0]                       # duplicates inside an anchor frame
+    xv[dyn][9] = 0                                  # zero token in a dynamic anchor
+    xv[dyn + 2][5] = 0                              # zero token in a non-anchor frame
+    xa[[3, audio // 2]] = 0                         # zero audio rows
+    xv[0] = 0                                       # zero frame: a segment of its own
+    seg_starts = sorted(set([0, 1] + starts[1:]))
+    seq = AVSeq(frames, per_frame, audio, n_query, 0, 0, 0, seg_starts, structure)
+    return DynamicsCase("bf16", dim, xv.reshape(frames * per_frame, dim), xa, to_bf16_bits(xq),
+                        [seq], {"window": window, "r_pre": 0.5})
+
+
 # --------------------------------------------------------------------------
 # Config 5: ragged batch of 8 clips (scorer + one prune + compaction)
 # --------------------------------------------------------------------------

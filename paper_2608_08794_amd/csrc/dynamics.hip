@@ -17,10 +17,9 @@
 //                continuity smoothing and cuts, Eq. 3 segment scores, frame
 //                scores, Eq. 4 segment budgets and frame budgets (capped
 //                largest remainder), anchors and output offsets
-//   k_gram       fp64 cosine Gram of the tokens of every anchor frame (fp64
-//                MFMA)
-//   k_dafps      one wave per anchor frame: density-aware farthest-point
-//                sampling
+//   k_gram       fp64 Gram of the tokens of every anchor frame (fp64 MFMA)
+//   k_dafps      per anchor frame: cosines from the Gram and its diagonal,
+//                then density-aware farthest-point sampling in one wave
 //   k_dedup_sim, k_dedup_pick  one wave per token, then one workgroup per
 //                non-anchor frame: keep the positions least
 //                similar to the anchor
@@ -387,8 +386,9 @@ __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w
     }
     int lo = 0;
     if (F > w) lo = min(max(f - w / 2, 0), F - w);
-    // Centred Grams K = H G H of the window rows lo .. lo+ww-1.
-    double ra[W], rv[W], ta = 0.0, tv = 0.0;
+    // Centred Grams K = H G H of the window rows lo .. lo+ww-1, and the
+    // traces of the raw Grams G.
+    double ra[W], rv[W], ta = 0.0, tv = 0.0, tra = 0.0, trv = 0.0;
 #pragma unroll
     for (int i = 0; i < W; ++i) {
       ra[i] = rv[i] = 0.0;
@@ -404,6 +404,8 @@ __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w
         rv[i] /= ww;
         ta += ra[i];
         tv += rv[i];
+        tra += band_at(band_a, f0, lo + i, lo + i);
+        trv += band_at(band_v, f0, lo + i, lo + i);
       }
     }
     ta /= ww;
@@ -422,8 +424,9 @@ __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w
         nv += kv * kv;
       }
     }
-    const double den = sqrt(na) * sqrt(nv);
-    const double cf = den == 0.0 ? 0.0 : num / den;
+    // A degenerate side (no variation the Gram resolves) gives 0.
+    const double sa = sqrt(na), sv = sqrt(nv);
+    const double cf = (sa <= kCkaDegenerate * tra || sv <= kCkaDegenerate * trv) ? 0.0 : num / (sa * sv);
     cka[f0 + f] = cf;
     if (frame_cka) frame_cka[f0 + f] = (float)cf;
     sum += cf;
@@ -779,15 +782,11 @@ __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, 
   }
   // Continuity cs_f = cos(v_f, v_{f+1}), its Gaussian smoothing (half-sample
   // symmetric ends, truncated at 4 sigma) and the relevance r_f.
-  const double qn = sqrt(qq[blockIdx.x]);
+  const double qn = qq[blockIdx.x];
   for (int f = tid; f < F; f += kPlanBlk) {
-    const double nx = sqrt(band_v[(f0 + f) * kMaxWindow]);
-    if (f + 1 < F) {
-      const double ny = sqrt(band_v[(f0 + f + 1) * kMaxWindow]);
-      cont[f] = (nx == 0.0 || ny == 0.0) ? 0.0 : band_v[(f0 + f) * kMaxWindow + 1] / (nx * ny);
-    }
-    const double cs = (nx == 0.0 || qn == 0.0) ? 0.0 : vq[f0 + f] / (nx * qn);
-    rel[f] = (1.0 + cs) / 2.0;
+    const double nx = band_v[(f0 + f) * kMaxWindow];
+    if (f + 1 < F) cont[f] = cos_from(band_v[(f0 + f) * kMaxWindow + 1], nx, band_v[(f0 + f + 1) * kMaxWindow]);
+    rel[f] = (1.0 + cos_from(vq[f0 + f], nx, qn)) / 2.0;
   }
   __syncthreads();
   const int n = F - 1;
@@ -898,7 +897,7 @@ __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, 
 }
 
 // ---------------------------------------------------------------------------
-// Cosine Gram of an anchor frame's P tokens in fp64 on the matrix cores
+// Gram of an anchor frame's P tokens in fp64 on the matrix cores
 // (v_mfma_f64_16x16x4f64).  One workgroup per 16 x 16 tile of the upper
 // triangle of an anchor frame, looping over the batch's (anchor, tile)
 // items; its kGramSplit waves take contiguous slices of the embedding and
@@ -956,8 +955,7 @@ template <class T>
 __global__ __launch_bounds__(kGramSplit * 64) void k_gram(const ClipDev* __restrict__ clips, int n_clips,
                                                           const int32_t* __restrict__ anchors,
                                                           const FramePlanDev* __restrict__ plan, int dim,
-                                                          const T* __restrict__ xv, const double* __restrict__ nv,
-                                                          double* __restrict__ gram) {
+                                                          const T* __restrict__ xv, double* __restrict__ gram) {
   __shared__ double red[kGramSplit - 1][4 * 64];
   const int wave = threadIdx.x >> 6, lane = threadIdx.x & 63, g = lane >> 4, r16 = lane & 15;
   // This wave's K slice, in 32-element steps.
@@ -1045,17 +1043,16 @@ __global__ __launch_bounds__(kGramSplit * 64) void k_gram(const ClipDev* __restr
         for (int q = 0; q < kGramSplit - 1; ++q)
 #pragma unroll
           for (int e = 0; e < 4; ++e) acc[e] += red[q][e * 64 + lane];
+        // Raw dot products: k_dafps forms the cosines from them and the
+        // diagonal, which went through the same MFMA sequence.
         double* G = gram + cc.gram_off + (int64_t)f * P * P;
         const int col = tj * kGramTile + r16;
-        const double nc = col < P ? sqrt(nv[row0 + col]) : 0.0;
 #pragma unroll
         for (int e = 0; e < 4; ++e) {
           const int row = ti * kGramTile + 4 * e + g;
           if (row >= P || col >= P) continue;
-          const double nr = sqrt(nv[row0 + row]);
-          const double v = (nr == 0.0 || nc == 0.0) ? 0.0 : acc[e] / (nr * nc);
-          G[(int64_t)row * P + col] = v;
-          G[(int64_t)col * P + row] = v;
+          G[(int64_t)row * P + col] = acc[e];
+          G[(int64_t)col * P + row] = acc[e];
         }
       }
       __syncthreads();
@@ -1164,8 +1161,13 @@ __global__ __launch_bounds__(kGramWaves * 64) void k_spatial_gram(const ClipDev*
   }
 }
 
-// c_f = S_av / (sqrt(S_aa) sqrt(S_vv)) from the tile sums, in tile order.
-__global__ __launch_bounds__(kBlk) void k_spatial_reduce(int64_t n_frames, int tiles, const double* __restrict__ part,
+// c_f = S_av / (sqrt(S_aa) sqrt(S_vv)) from the tile sums, in tile order;
+// 0 when a side is degenerate: its centred Gram norm sqrt(S) at most
+// kCkaDegenerate of its raw trace (the sum of its tokens' squared norms).
+__global__ __launch_bounds__(kBlk) void k_spatial_reduce(const ClipDev* __restrict__ clips,
+                                                         const FrameDev* __restrict__ frames, int64_t n_frames,
+                                                         int tiles, const double* __restrict__ part,
+                                                         const double* __restrict__ nv, const double* __restrict__ na,
                                                          double* __restrict__ cka) {
   const int64_t f = (int64_t)blockIdx.x * kBlk + threadIdx.x;
   if (f >= n_frames) return;
@@ -1176,8 +1178,16 @@ __global__ __launch_bounds__(kBlk) void k_spatial_reduce(int64_t n_frames, int t
     s_av += q[1];
     s_vv += q[2];
   }
-  const double den = sqrt(s_aa) * sqrt(s_vv);
-  cka[f] = den == 0.0 ? 0.0 : s_av / den;
+  const FrameDev fr = frames[f];
+  const ClipDev c = clips[fr.clip];
+  const int64_t lo = ((int64_t)fr.f * c.n_audio) / c.n_frames;
+  const int64_t hi = (((int64_t)fr.f + 1) * c.n_audio + c.n_frames - 1) / c.n_frames;
+  double tr_a = 0.0, tr_v = 0.0;
+  for (int64_t r = lo; r < hi; ++r) tr_a += na[c.aud_off + r];
+  const int64_t row0 = c.vis_off + (int64_t)fr.f * c.per_frame;
+  for (int p = 0; p < c.per_frame; ++p) tr_v += nv[row0 + p];
+  const double sa = sqrt(s_aa), sv = sqrt(s_vv);
+  cka[f] = (sa <= kCkaDegenerate * tr_a || sv <= kCkaDegenerate * tr_v) ? 0.0 : s_av / (sa * sv);
 }
 
 // Lexicographic (value desc, index asc) argmax across a wave.
@@ -1195,14 +1205,15 @@ __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
 
 // Density of token i for DA-FPS: the mean of its dafps_k largest cosines to
 // the other tokens of the frame, and how many of those cosines reach the
-// coverage threshold.  The running top list lives in registers (static
+// coverage threshold.  Rows of S below R are cosines in LDS; later rows are
+// read from the raw Gram and turned into cosines with its diagonal dg.  The running top list lives in registers (static
 // indices only): each new value is carried down past the larger ones.  S is
 // exactly symmetric (entries (i, j) and (j, i) are the same products summed
 // in the same order), so thread i reads column i and a wave's loads for one
 // j are contiguous; loads are issued eight at a time.
 template <int KM>
-__device__ __forceinline__ double dafps_density(const double* S, const double* Sl, int R, int P, int i, int k,
-                                                double cover) {
+__device__ __forceinline__ double dafps_density(const double* S, const double* Sl, const double* dg, int R, int P,
+                                                int i, int k, double cover) {
   double top[KM];
 #pragma unroll
   for (int q = 0; q < KM; ++q) top[q] = -INFINITY;
@@ -1212,7 +1223,7 @@ __device__ __forceinline__ double dafps_density(const double* S, const double* S
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
       const int j = j0 + u;
-      vals[u] = j >= P ? 0.0 : j < R ? Sl[j * P + i] : S[(int64_t)j * P + i];
+      vals[u] = j >= P ? 0.0 : j < R ? Sl[j * P + i] : cos_from(S[(int64_t)j * P + i], dg[j], dg[i]);
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
@@ -1243,11 +1254,13 @@ __device__ __forceinline__ double dafps_density(const double* S, const double* S
 // ---------------------------------------------------------------------------
 // DA-FPS on an anchor frame: one workgroup, thread i owns token i.
 // ---------------------------------------------------------------------------
-// The anchor's first R rows of S (as many as fit) are copied to LDS; the
-// pick loop then runs in one wave, which holds up to four tokens per lane
+// The anchor's first R rows of its raw Gram (as many as fit) are copied to
+// LDS and turned into cosines there, S_ij = G_ij / sqrt(G_ii G_jj): the
+// diagonal went through the same MFMA sums as every entry, so a token and
+// a bitwise copy of it have cosine exactly 1.  The pick loop then runs in one wave, which holds up to four tokens per lane
 // and finds each pick with a shuffle argmax, so a pick costs one LDS row
 // read (a global one for the few rows past R) and no barrier.
-constexpr int kDafpsLdsDoubles = 20200;   // 161600 bytes of S rows; 160 KiB of LDS in all
+constexpr int kDafpsLdsDoubles = 19968;   // 159744 bytes of S rows; 160 KiB of LDS with rho and the diagonal
 
 __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restrict__ clips,
                                                         const FrameDev* __restrict__ frames,
@@ -1255,6 +1268,7 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
                                                         const double* __restrict__ gram, int32_t* __restrict__ kept) {
   __shared__ __attribute__((aligned(16))) double Sl[kDafpsLdsDoubles];
   __shared__ double rho_sh[kMaxPerFrame];
+  __shared__ double dg[kMaxPerFrame];
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
   const int64_t frame = c.frame_off + fr.f;
@@ -1264,6 +1278,7 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
   const int k = min(fp.budget, P);
   const double* S = gram + c.gram_off + (int64_t)fr.f * P * P;
   const int R = min(P, kDafpsLdsDoubles / P);
+  if (i < P) dg[i] = S[(int64_t)i * P + i];
   if (((uintptr_t)S & 15) == 0) {
     // Rows [0, R) of S into LDS with 16-byte direct-to-LDS loads, all in
     // flight together: wave load j fills bytes [1024 j, 1024 j + 1024), lane
@@ -1296,11 +1311,13 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
     }
   }
   __syncthreads();
+  for (int e = i; e < R * P; e += kMaxPerFrame) Sl[e] = cos_from(Sl[e], dg[e / P], dg[e % P]);
+  __syncthreads();
   // Density of every token (thread per token).
   if (i < P)
-    rho_sh[i] = prm.dafps_k <= 8    ? dafps_density<8>(S, Sl, R, P, i, prm.dafps_k, prm.cover)
-                : prm.dafps_k <= 16 ? dafps_density<16>(S, Sl, R, P, i, prm.dafps_k, prm.cover)
-                                    : dafps_density<32>(S, Sl, R, P, i, prm.dafps_k, prm.cover);
+    rho_sh[i] = prm.dafps_k <= 8    ? dafps_density<8>(S, Sl, dg, R, P, i, prm.dafps_k, prm.cover)
+                : prm.dafps_k <= 16 ? dafps_density<16>(S, Sl, dg, R, P, i, prm.dafps_k, prm.cover)
+                                    : dafps_density<32>(S, Sl, dg, R, P, i, prm.dafps_k, prm.cover);
   __syncthreads();
   if (i >= 64) return;
   // Wave 0: token t = lane + 64 u, u < 4.
@@ -1344,7 +1361,10 @@ __global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restric
       for (int u = 0; u < kU; ++u) sv[u] = lane + 64 * u < P ? Sl[pick * P + lane + 64 * u] : 0.0;
     } else {
 #pragma unroll
-      for (int u = 0; u < kU; ++u) sv[u] = lane + 64 * u < P ? S[(int64_t)pick * P + lane + 64 * u] : 0.0;
+      for (int u = 0; u < kU; ++u) {
+        const int t = lane + 64 * u;
+        sv[u] = t < P ? cos_from(S[(int64_t)pick * P + t], dg[pick], dg[t]) : 0.0;
+      }
     }
 #pragma unroll
     for (int u = 0; u < kU; ++u) {
@@ -1378,10 +1398,11 @@ template <class T>
 __global__ __launch_bounds__(kBlk) void k_dedup_sim(const ClipDev* __restrict__ clips,
                                                     const FrameDev* __restrict__ frames,
                                                     const FramePlanDev* __restrict__ plan, int dim,
-                                                    const T* __restrict__ xv, const double* __restrict__ nv,
-                                                    double* __restrict__ sim) {
+                                                    const T* __restrict__ xv, double* __restrict__ sim) {
   // One wave per position: cosine of token p of frame f with token p of its
-  // anchor, written to sim at the token's row.
+  // anchor, written to sim at the token's row.  The dot product and both
+  // squared norms are summed the same way, so a position that repeats the
+  // anchor's token has cosine exactly 1.
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
   const FramePlanDev fp = plan[c.frame_off + fr.f];
@@ -1393,19 +1414,22 @@ __global__ __launch_bounds__(kBlk) void k_dedup_sim(const ClipDev* __restrict__ 
   const int64_t rowf = c.vis_off + (int64_t)fr.f * P + p, rowa = c.vis_off + (int64_t)fp.anchor * P + p;
   const T* x = xv + rowf * dim;
   const T* y = xv + rowa * dim;
-  double acc = 0.0, o[8], q[8];
+  double xy = 0.0, xx = 0.0, yy = 0.0, o[8], q[8];
 #pragma unroll 4
   for (int d = lane * 8; d < dim; d += 64 * 8) {
     load8(x + d, o);
     load8(y + d, q);
 #pragma unroll
-    for (int e = 0; e < 8; ++e) acc += o[e] * q[e];
+    for (int e = 0; e < 8; ++e) {
+      xy = fma(o[e], q[e], xy);
+      xx = fma(o[e], o[e], xx);
+      yy = fma(q[e], q[e], yy);
+    }
   }
-  acc = wave_sum(acc);
-  if (lane == 0) {
-    const double nx = sqrt(nv[rowf]), ny = sqrt(nv[rowa]);
-    sim[rowf - c.vis_off + c.token_off] = (nx == 0.0 || ny == 0.0) ? 0.0 : acc / (nx * ny);
-  }
+  xy = wave_sum(xy);
+  xx = wave_sum(xx);
+  yy = wave_sum(yy);
+  if (lane == 0) sim[rowf - c.vis_off + c.token_off] = cos_from(xy, xx, yy);
 }
 
 __global__ __launch_bounds__(kBlk) void k_dedup_pick(const ClipDev* __restrict__ clips,
@@ -1466,24 +1490,24 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
                        dp.a, dp.q, dp.band_v, dp.band_a, dp.vq, dp.qq);
     if ((st = launch_status("k_band")) != APACK_OK) return st;
   }
+  if (n_vis + n_aud > 0) {
+    hipLaunchKernelGGL(k_norms, dim3((unsigned)((n_vis + n_aud + kBlk - 1) / kBlk)), dim3(kBlk), 0, s, n_vis, n_aud,
+                       (int)dchunks, dp.sqp, dp.nv, dp.na, dp.maxkey);
+    if ((st = launch_status("k_norms")) != APACK_OK) return st;
+  }
   if (prm.alignment == APACK_ALIGN_SPATIAL_CKA && nf > 0) {
     const unsigned gy = (unsigned)((pl.spatial_tiles + kGramWaves - 1) / kGramWaves);
     hipLaunchKernelGGL(k_spatial_gram<T>, dim3(nf, gy), dim3(kGramWaves * 64), 0, s, dp.clips, dp.frames, dim, xv,
                        xa, dp.v, dp.a, pl.spatial_tiles, dp.spatial);
     if ((st = launch_status("k_spatial_gram")) != APACK_OK) return st;
-    hipLaunchKernelGGL(k_spatial_reduce, dim3((unsigned)((nf + kBlk - 1) / kBlk)), dim3(kBlk), 0, s, (int64_t)nf,
-                       pl.spatial_tiles, dp.spatial, dp.cka);
+    hipLaunchKernelGGL(k_spatial_reduce, dim3((unsigned)((nf + kBlk - 1) / kBlk)), dim3(kBlk), 0, s, dp.clips,
+                       dp.frames, (int64_t)nf, pl.spatial_tiles, dp.spatial, dp.nv, dp.na, dp.cka);
     if ((st = launch_status("k_spatial_reduce")) != APACK_OK) return st;
   }
   auto cka = prm.window <= 2 ? k_cka<2> : prm.window <= 4 ? k_cka<4> : prm.window <= 8 ? k_cka<8> : k_cka<kMaxWindow>;
   hipLaunchKernelGGL(cka, dim3(nc), dim3(kBlk), 0, s, dp.clips, prm.window, prm.tau_gate, prm.alignment, dp.band_v,
                      dp.band_a, dp.cka, frame_cka, gate_fired);
   if ((st = launch_status("k_cka")) != APACK_OK) return st;
-  if (n_vis + n_aud > 0) {
-    hipLaunchKernelGGL(k_norms, dim3((unsigned)((n_vis + n_aud + kBlk - 1) / kBlk)), dim3(kBlk), 0, s, n_vis, n_aud,
-                       (int)dchunks, dp.sqp, dp.nv, dp.na, dp.maxkey);
-    if ((st = launch_status("k_norms")) != APACK_OK) return st;
-  }
   if (pl.gemm_tiles > 0) {
     if constexpr (std::is_same<T, bf16_t>::value) {
       if (pl.use256) {
@@ -1507,13 +1531,13 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
     if (pl.gram_items > 0) {
       const unsigned gb = (unsigned)std::min<int64_t>((pl.gram_items + 7) / 8 * 8, kGramBlocks);
       hipLaunchKernelGGL(k_gram<T>, dim3(gb), dim3(kGramSplit * 64), 0, s, dp.clips, nc, dp.anchors, dp.plan, dim,
-                         xv, dp.nv, dp.gram);
+                         xv, dp.gram);
     }
     if ((st = launch_status("k_gram")) != APACK_OK) return st;
     hipLaunchKernelGGL(k_dafps, dim3(nf), dim3(kMaxPerFrame), 0, s, dp.clips, dp.frames, dp.plan, prm, dp.gram, kept);
     if ((st = launch_status("k_dafps")) != APACK_OK) return st;
     hipLaunchKernelGGL(k_dedup_sim<T>, dim3(nf, (pl.max_per_frame + kBlk / 64 - 1) / (kBlk / 64)), dim3(kBlk), 0, s,
-                       dp.clips, dp.frames, dp.plan, dim, xv, dp.nv, dp.sim);
+                       dp.clips, dp.frames, dp.plan, dim, xv, dp.sim);
     if ((st = launch_status("k_dedup_sim")) != APACK_OK) return st;
     hipLaunchKernelGGL(k_dedup_pick, dim3(nf), dim3(kBlk), 0, s, dp.clips, dp.frames, dp.plan, dp.sim, kept);
     if ((st = launch_status("k_dedup_pick")) != APACK_OK) return st;

@@ -10,6 +10,18 @@ namespace apack {
 
 constexpr int kMaxWindow = 16;   // largest CKA window
 constexpr int kMaxPerFrame = 256;
+// A CKA input whose centred Gram has a Frobenius norm of at most this
+// fraction of its raw Gram's trace has no variation that fp64 resolves
+// through the Gram (repeated or zero frames): its c_f is 0.
+constexpr double kCkaDegenerate = 1e-8;
+
+// Cosine from a dot product and the two squared norms, each summed the same
+// way: dot / sqrt(nx ny), so a vector and a bitwise copy of it give exactly
+// 1 (the square root of a correctly rounded square is exact); 0 when a
+// norm is 0.
+__device__ __forceinline__ double cos_from(double dot, double nx, double ny) {
+  return (nx == 0.0 || ny == 0.0) ? 0.0 : dot / sqrt(nx * ny);
+}
 
 // Per-clip descriptor on the device.
 struct ClipDev {

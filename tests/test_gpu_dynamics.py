@@ -42,6 +42,7 @@ def _oracle(case, dtype="bf16"):
 def _certify(results):
     for r in results:
         m = r["margins"]
+        assert m["cka_degenerate"] > 1.0, m
         assert m["gate"] > 1e-9 and m["segment"] > 1e-9 and m["segment_budget"] > 1e-9, m
         assert m["dafps"] > 1e-9 and m["dedup"] > 1e-9, m
         assert m["frame_budget"] > (1e-4 if r["gate"] else 1e-9), m
@@ -236,3 +237,47 @@ def test_spatial_cka_ragged_batch_with_edge_shapes():
     _compare(case, got, want)
     f0 = sum(p.seqs[0].n_frames for p in parts[:1])
     assert np.all(got["cka"][f0:f0 + 10] == 0.0)   # one-token bins have no audio covariance
+
+
+# -- degenerate inputs: zero frame, static scene, duplicate and zero tokens --
+
+@pytest.mark.parametrize("alignment", ["gated_cka", "cka", "av_cosine", "spatial_cka"])
+@pytest.mark.parametrize("structure", ["shared", "offset"])
+def test_degenerate_inputs_parity(structure, alignment):
+    """A zero frame, a static scene (repeated frames and audio), duplicate
+    tokens in an anchor frame and zero tokens and audio rows: zero CKA on
+    degenerate windows, cosine exactly 1 between repeated tokens and 0 for
+    zero ones, so the ties these inputs create fall the same way (lower
+    index) on both sides."""
+    case = W.dynamics_edge(structure)
+    case.params = dict(case.params, alignment=alignment)
+    log(f"[dynamics] edge clip {structure}, {alignment}")
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+def test_degenerate_inputs_parity_fp32_and_wide_dim():
+    """The same degenerate clip at the 7B embedding width (the 256-tile gate
+    GEMM) and with fp32 inputs (the fp32 gate GEMM)."""
+    case = W.dynamics_edge("offset", dim=3584, frames=40, per_frame=24, audio=500)
+    log("[dynamics] edge clip, 3584-d, bf16")
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+    f32 = W.DynamicsCase("f32", case.dim, W.bf16_bits_to_f32(case.xv), W.bf16_bits_to_f32(case.xa),
+                         W.bf16_bits_to_f32(case.xq), case.seqs, case.params)
+    log("[dynamics] edge clip, 3584-d, fp32")
+    want = _oracle(f32, "f32")
+    _certify(want)
+    _compare(f32, _run(f32, "f32"), want, "f32")
+
+
+def test_scorer_is_deterministic():
+    """Two runs of the 60 s 7B-shape clip with the gate fired (atomic
+    maxima, split-K Grams, cross-workgroup sums) give the same bits."""
+    case = W.dynamics_cfg3("offset")
+    a, b = _run(case), _run(case)
+    for key in ("cka", "score", "budget", "segment", "gate", "kept"):
+        assert np.array_equal(a[key].view(np.uint8), b[key].view(np.uint8)), key
+    assert a["n_kept"] == b["n_kept"]

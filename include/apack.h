@@ -215,6 +215,23 @@ apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* src_rows, in
                                       int32_t* pos, int32_t pos_rows, int64_t pos_stride,
                                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* Reports whether the last apack_compact_kv_inplace call that moved rows
+ * with this workspace gave up one of its waits.  The ordering waits are
+ * bounded (see apack_set_inplace_wait_limit); a ticket whose wait gives up
+ * stores nothing, so no row that another output row still has to read is
+ * overwritten, but some of rows [0, n_out) keep their old contents and the
+ * result is unusable.  Only a stalled GPU reaches the default limit.
+ * Synchronises `stream`, then sets *gave_up (HOST) to 1 or 0. */
+apack_status apack_compact_kv_inplace_status(const void* workspace, size_t workspace_bytes,
+                                             int32_t* gave_up, void* stream);
+
+/* Bound on one ordering wait of apack_compact_kv_inplace, in polls of a few
+ * hundred nanoseconds each (default 2^22, a few seconds); returns the
+ * previous bound.  Applies to calls made after it returns, process-wide.
+ * A bound of 0 makes every wait that has earlier stripes to wait for give
+ * up at once, so the give-up report can be exercised without a stall. */
+uint32_t apack_set_inplace_wait_limit(uint32_t polls);
+
 /* ------------------------------------------------------------------------ */
 /* Prefill-FLOPs accounting (Appendix G)                                    */
 /* ------------------------------------------------------------------------ */

@@ -18,6 +18,7 @@ from ._lib import (  # noqa: F401
     DynParams,
     apack_compact_kv,
     apack_compact_kv_inplace,
+    apack_compact_kv_inplace_status,
     apack_compact_kv_inplace_workspace,
     apack_dyn_params_default,
     apack_keep_count,
@@ -28,6 +29,7 @@ from ._lib import (  # noqa: F401
     apack_schedule_lengths,
     apack_score_dynamics,
     apack_score_dynamics_query,
+    apack_set_inplace_wait_limit,
     apack_visual_budget,
     library,
     library_path,

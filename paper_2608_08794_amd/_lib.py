@@ -72,6 +72,8 @@ _SIGS = {
                                         ctypes.POINTER(_P), ctypes.POINTER(_P), _I32, _I32, ctypes.c_int,
                                         _I64, _I64, _P, _P, _I32, _P, _P, _I32, _I64, _I64, _P]),
     "apack_compact_kv_inplace_workspace": (_SZ, [_I64]),
+    "apack_compact_kv_inplace_status": (ctypes.c_int, [_P, _SZ, ctypes.POINTER(_I32), _P]),
+    "apack_set_inplace_wait_limit": (ctypes.c_uint32, [ctypes.c_uint32]),
     "apack_layer_flops": (ctypes.c_double, [_I64, _I64, _I64]),
     "apack_prefill_flops": (ctypes.c_int, [_I32, ctypes.POINTER(_I64), _I64, _I64, _I64,
                                            ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double)]),
@@ -133,6 +135,17 @@ def _stream(stream):
     if stream is not None:
         return ctypes.c_void_p(stream if isinstance(stream, int) else stream.cuda_stream)
     return ctypes.c_void_p(_torch().cuda.current_stream().cuda_stream)
+
+
+def _alloc_on(stream):
+    """Context for the tensors the binding allocates for a call enqueued on
+    `stream` (outputs, workspace): torch allocates and fills them on that
+    stream, so the caching allocator does not hand their memory out again
+    before the call's kernels are done, and any fill runs before them."""
+    torch = _torch()
+    if stream is None:
+        return torch.cuda.stream(None)
+    return torch.cuda.stream(torch.cuda.ExternalStream(stream) if isinstance(stream, int) else stream)
 
 
 def _dtype_code(t):
@@ -232,12 +245,13 @@ def apack_prune_layer(q, k, seqs, scores=None, kept_rows=None, workspace=None, s
     wsb = ctypes.c_size_t(0)
     _check(library().apack_prune_layer_query(n, arr, hq, hkv, d, n_kept, ctypes.byref(wsb)))
     total = sum(int(n_kept[i]) for i in range(n))
-    if scores is None:
-        scores = torch.zeros(k_rows, dtype=torch.float32, device=k.device)
-    if kept_rows is None:
-        kept_rows = torch.empty(max(total, 1), dtype=torch.int32, device=k.device)
-    if workspace is None:
-        workspace = _workspace(wsb.value, k.device)
+    with _alloc_on(stream):
+        if scores is None:
+            scores = torch.zeros(k_rows, dtype=torch.float32, device=k.device)
+        if kept_rows is None:
+            kept_rows = torch.empty(max(total, 1), dtype=torch.int32, device=k.device)
+        if workspace is None:
+            workspace = _workspace(wsb.value, k.device)
     _check(library().apack_prune_layer(
         n, arr, _dtype_code(q), hq, hkv, d, _ptr(q), qhs, q_rows, _ptr(k), khs, k_rows,
         _ptr(scores), _ptr(kept_rows), kept_rows.numel(), n_kept,
@@ -327,10 +341,25 @@ def apack_compact_kv_inplace(src_rows, n_in, k=(), v=(), hidden=None, pos=None, 
             raise ApackError(2, "position ids must have unit column stride")
     need = apack_compact_kv_inplace_workspace(n_out)
     if workspace is None:
-        workspace = _workspace(need, src_rows.device)
+        with _alloc_on(stream):
+            workspace = _workspace(need, src_rows.device)
     _check(library().apack_compact_kv_inplace(
         n_out, _ptr(src_rows), int(n_in), n_layers, tk, tv, hkv, d, code, hs,
         _ptr(hidden), hid, _ptr(pos), prow, ps, workspace.data_ptr(), workspace.numel(), _stream(stream)))
+
+
+def apack_compact_kv_inplace_status(workspace, stream=None):
+    """True if the last in-place compaction on `workspace` gave up a wait
+    (its result is unusable); synchronises the stream."""
+    flag = ctypes.c_int32(0)
+    _check(library().apack_compact_kv_inplace_status(_ptr(workspace), workspace.numel(), ctypes.byref(flag),
+                                                     _stream(stream)))
+    return bool(flag.value)
+
+
+def apack_set_inplace_wait_limit(polls):
+    """Sets the bound on one in-place ordering wait; returns the previous one."""
+    return int(library().apack_set_inplace_wait_limit(int(polls)))
 
 
 def apack_layer_flops(n, d_model, d_ffn):
@@ -412,16 +441,17 @@ def apack_score_dynamics(visual, audio, query, seqs, params=None, workspace=None
     total = sum(int(nk[i]) for i in range(n))
     frames = sum(int(arr[i].n_frames) for i in range(n))
     dev = visual.device
-    out = {
-        "cka": torch.empty(max(frames, 1), dtype=torch.float32, device=dev),
-        "score": torch.empty(max(frames, 1), dtype=torch.float32, device=dev),
-        "budget": torch.empty(max(frames, 1), dtype=torch.int32, device=dev),
-        "segment": torch.empty(max(frames, 1), dtype=torch.int32, device=dev),
-        "gate": torch.empty(max(n, 1), dtype=torch.uint8, device=dev),
-        "kept": torch.empty(max(total, 1), dtype=torch.int32, device=dev),
-    }
-    if workspace is None:
-        workspace = _workspace(wsb.value, dev)
+    with _alloc_on(stream):
+        out = {
+            "cka": torch.empty(max(frames, 1), dtype=torch.float32, device=dev),
+            "score": torch.empty(max(frames, 1), dtype=torch.float32, device=dev),
+            "budget": torch.empty(max(frames, 1), dtype=torch.int32, device=dev),
+            "segment": torch.empty(max(frames, 1), dtype=torch.int32, device=dev),
+            "gate": torch.empty(max(n, 1), dtype=torch.uint8, device=dev),
+            "kept": torch.empty(max(total, 1), dtype=torch.int32, device=dev),
+        }
+        if workspace is None:
+            workspace = _workspace(wsb.value, dev)
     for t, name in ((visual, "visual"), (audio, "audio"), (query, "query")):
         if t.dim() != 2 or t.stride(1) != 1 or t.stride(0) != dim:
             raise ApackError(2, f"{name} must be a contiguous [rows, dim] tensor")

@@ -24,7 +24,14 @@
 // were claimed by running workgroups.  By induction over stripes every
 // counter fills.  This holds for any src; only the row contents need src to
 // be strictly increasing.
+//
+// Each wait is still bounded (a defensive limit of ~seconds of polling, see
+// apack_set_inplace_wait_limit).  A wait that gives up sets the error word
+// in the workspace and its ticket stores nothing, so no source row that an
+// earlier stripe has yet to read is ever overwritten; the caller learns of
+// it from apack_compact_kv_inplace_status.
 #include <algorithm>
+#include <atomic>
 #include <cstring>
 #include <vector>
 
@@ -44,13 +51,14 @@ constexpr int kStripe = kThreads * kPerThread / kSlice;  // output rows per stri
 constexpr int kGroup = 2;                  // items per ticket, loaded together
 constexpr int kCounterPad = 16;            // one 64-byte line per stripe counter
 constexpr int kMaxPosRows = kThreads * kPerThread / kStripe;
-constexpr uint32_t kSpinCap = 1u << 22;    // defensive bound on one wait (seconds)
+constexpr uint32_t kDefaultWaitLimit = 1u << 22;  // polls per wait (~seconds)
 
 struct InplaceArgs {
   const int32_t* src;
   int64_t n_out, n_in;
   int64_t n_stripes, n_items;
   int32_t items_per_stripe;
+  uint32_t wait_limit;     // polls before a wait gives up; 0: every wait gives up at once
   // K/V planes: tensor t, head h at planes[t] + h * hs; rows of kv_row_units.
   int32_t kv_planes, heads, kv_slices;
   int64_t kv_row_units, hs;
@@ -93,19 +101,26 @@ __global__ __launch_bounds__(kThreads) void k_inplace_prep(const InplaceArgs a) 
     for (int64_t s = std::max<int64_t>(floor_div(cur, kStripe) + 1, 0); s <= a.n_stripes; ++s) fr[s] = (int32_t)a.n_out;
 }
 
-// Blocks until every stripe in [lo, hi] has all of its items read.
-__device__ void wait_stripes(const InplaceArgs& a, int64_t lo, int64_t hi) {
+// Blocks until every stripe in [lo, hi] has all of its items read; false
+// (with the workspace's error word set) if a wait gave up first.  A limit
+// of 0 gives up on any non-empty range without polling.
+__device__ bool wait_stripes(const InplaceArgs& a, int64_t lo, int64_t hi) {
+  if (a.wait_limit == 0 && lo <= hi) {
+    __hip_atomic_fetch_or(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return false;
+  }
   for (int64_t st = lo; st <= hi; ++st) {
     const uint32_t* c = a.done + st * kCounterPad;
     uint32_t spins = 0;
     while (ld_agent(c) < (uint32_t)a.items_per_stripe) {
-      if (++spins > kSpinCap) {
+      if (++spins > a.wait_limit) {
         __hip_atomic_fetch_or(a.err, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        break;
+        return false;
       }
       __builtin_amdgcn_s_sleep(2);
     }
   }
+  return true;
 }
 
 // Position ids move as 4-byte words inside a unit of either width.
@@ -228,7 +243,8 @@ __device__ __forceinline__ void reader_stripes(const InplaceArgs& a, int64_t t, 
 
 // A workgroup claims kGroup items with one ticket, loads them all, counts
 // them read in their stripes' counters, then waits for the readers of their
-// destination rows, then stores, and only then claims its next ticket.  So
+// destination rows, then stores (nothing, if a wait gave up), and only then
+// claims its next ticket.  So
 // a workgroup never waits while it holds a claimed item it has not counted:
 // a count waits on nothing but its own loads, and no chain of waits forms
 // between stripes.  Thread 0 reads the reader ranges before the data loads
@@ -237,6 +253,7 @@ __device__ __forceinline__ void reader_stripes(const InplaceArgs& a, int64_t t, 
 template <class U>
 __global__ __launch_bounds__(kThreads) void k_compact_inplace(const InplaceArgs a) {
   __shared__ uint32_t sh_ticket;
+  __shared__ uint32_t sh_ok;                   // the ticket's waits all completed
   __shared__ int32_t sidx[kGroup * kStripe];   // src of the ticket's output rows
   const int tid = threadIdx.x;
   int64_t waited = -1;  // latest stripe whose readers thread 0 has seen complete
@@ -283,19 +300,23 @@ __global__ __launch_bounds__(kThreads) void k_compact_inplace(const InplaceArgs 
       for (int64_t i = i0; i < i1; ++i)
         __hip_atomic_fetch_add(a.done + i / a.items_per_stripe * kCounterPad, 1u, __ATOMIC_RELAXED,
                                __HIP_MEMORY_SCOPE_AGENT);
-      if (pending)
+      bool ok = true;
+      if (pending || a.wait_limit == 0)
         for (int j = 0; j < kGroup; ++j)
           if (t0 + j <= sb) {
             int64_t lo, hi;
             reader_stripes(a, t0 + j, fr[j], fr[j + 1], lo, hi);
-            wait_stripes(a, lo, hi);
+            ok = ok && wait_stripes(a, lo, hi);
           }
-      waited = std::max(waited, sb);
+      if (ok) waited = std::max(waited, sb);
+      sh_ok = ok ? 1u : 0u;
     }
     __syncthreads();
+    if (sh_ok) {
 #pragma unroll
-    for (int p = 0; p < kGroup; ++p)
-      if (q[p].live) store_item<U>(a, i0 + p, q[p]);
+      for (int p = 0; p < kGroup; ++p)
+        if (q[p].live) store_item<U>(a, i0 + p, q[p]);
+    }
   }
 }
 
@@ -332,6 +353,8 @@ int resident_groups() {
   return n;
 }
 
+std::atomic<uint32_t> g_wait_limit{kDefaultWaitLimit};
+
 }  // namespace
 }  // namespace apack
 
@@ -339,6 +362,26 @@ using namespace apack;
 
 extern "C" size_t apack_compact_kv_inplace_workspace(int64_t n_out) {
   return n_out < 0 ? 0 : inplace_layout(n_out).bytes;
+}
+
+extern "C" uint32_t apack_set_inplace_wait_limit(uint32_t polls) { return g_wait_limit.exchange(polls); }
+
+extern "C" apack_status apack_compact_kv_inplace_status(const void* workspace, size_t workspace_bytes,
+                                                        int32_t* gave_up, void* stream) {
+  clear_error();
+  APACK_CHECK(gave_up, APACK_E_ARG, "gave_up is NULL");
+  APACK_CHECK(workspace && ((uintptr_t)workspace % kAlign) == 0, APACK_E_WORKSPACE,
+              "workspace must be non-NULL and %zu-byte aligned", kAlign);
+  const InplaceLayout lay = inplace_layout(0);
+  APACK_CHECK(workspace_bytes >= lay.off_ticket + 2 * sizeof(uint32_t), APACK_E_WORKSPACE,
+              "workspace of %zu bytes holds no status word", workspace_bytes);
+  uint32_t err = 0;
+  hipStream_t hs = static_cast<hipStream_t>(stream);
+  APACK_HIP(hipMemcpyAsync(&err, static_cast<const char*>(workspace) + lay.off_ticket + sizeof(uint32_t),
+                           sizeof err, hipMemcpyDeviceToHost, hs));
+  APACK_HIP(hipStreamSynchronize(hs));
+  *gave_up = err != 0 ? 1 : 0;
+  return APACK_OK;
 }
 
 extern "C" apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* src_rows, int64_t n_in,
@@ -459,6 +502,7 @@ extern "C" apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* s
   APACK_CHECK(ips * a.n_stripes < (int64_t(1) << 31) * kGroup, APACK_E_UNSUPPORTED, "too many work items");
   a.items_per_stripe = (int32_t)ips;
   a.n_items = ips * a.n_stripes;
+  a.wait_limit = g_wait_limit.load();
   char* ws = static_cast<char*>(workspace);
   a.ticket = reinterpret_cast<uint32_t*>(ws + lay.off_ticket);
   a.err = a.ticket + 1;

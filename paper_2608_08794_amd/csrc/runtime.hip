@@ -31,8 +31,12 @@ apack_status launch_status(const char* what) {
 
 // ---------------------------------------------------------------------------
 // Pinned staging pool.  Blocks are reused once the event recorded after their
-// last upload has completed; a busy pool grows instead of waiting.
+// last upload has completed; a busy pool grows instead of waiting, up to
+// kMaxStaging blocks per device.  Past that, a call waits for the oldest
+// block's upload and takes it (growing it if it is too small), so a caller
+// that queues many calls ahead holds at most that many pinned blocks.
 // ---------------------------------------------------------------------------
+constexpr int kMaxStaging = 32;
 struct Staging {
   void* host = nullptr;
   void* mapped = nullptr;  // device address of `host`
@@ -40,17 +44,50 @@ struct Staging {
   int device = -1;
   hipEvent_t done = nullptr;
   bool busy = false;
+  uint64_t stamp = 0;      // acquisition order, for the wait at the cap
 };
 
 static std::mutex g_pool_mu;
 static std::vector<Staging*> g_pool;
+static uint64_t g_stamp = 0;
+
+// Pinned memory of `cap` bytes, its device address, and the block's event
+// (created once per block).
+static apack_status staging_alloc(Staging* s, size_t cap) {
+  s->cap = cap;
+  hipError_t e = hipHostMalloc(&s->host, s->cap, hipHostMallocDefault);
+  if (e != hipSuccess) {
+    s->host = nullptr;
+    s->cap = 0;
+    return fail(APACK_E_HIP, "hipHostMalloc(%zu): %s", cap, hipGetErrorString(e));
+  }
+  e = hipHostGetDevicePointer(&s->mapped, s->host, 0);
+  // The event only tells the host that the upload kernel has finished reading
+  // the block; no device write has to become visible to the host, so it skips
+  // the system-scope release (an L2 writeback that stalled the stream ~5 us).
+  if (e == hipSuccess && !s->done)
+    e = hipEventCreateWithFlags(&s->done, hipEventDisableTiming | hipEventDisableSystemFence);
+  if (e != hipSuccess) {
+    (void)hipHostFree(s->host);
+    s->host = nullptr;
+    s->cap = 0;
+    return fail(APACK_E_HIP, "staging block set-up: %s", hipGetErrorString(e));
+  }
+  return APACK_OK;
+}
 
 apack_status staging_acquire(size_t bytes, Staging** blk, void** host) {
   int dev = 0;
   APACK_HIP(hipGetDevice(&dev));
+  const size_t want = align_up(bytes < 65536 ? 65536 : bytes, 65536);
   std::lock_guard<std::mutex> lk(g_pool_mu);
+  int on_dev = 0;
+  Staging* oldest = nullptr;
   for (Staging* s : g_pool) {
-    if (s->device != dev || s->cap < bytes) continue;
+    if (s->device != dev) continue;
+    ++on_dev;
+    if (!oldest || s->stamp < oldest->stamp) oldest = s;
+    if (s->cap < bytes) continue;
     if (s->busy) {
       hipError_t q = hipEventQuery(s->done);
       if (q == hipErrorNotReady) continue;
@@ -58,29 +95,40 @@ apack_status staging_acquire(size_t bytes, Staging** blk, void** host) {
       s->busy = false;
     }
     s->busy = true;
+    s->stamp = ++g_stamp;
+    *blk = s;
+    *host = s->host;
+    return APACK_OK;
+  }
+  if (on_dev >= kMaxStaging) {
+    // At the cap: wait until the oldest block's upload has been read, then
+    // reuse it, reallocated if it is too small.
+    Staging* s = oldest;
+    if (s->busy) APACK_HIP(hipEventSynchronize(s->done));
+    s->busy = false;
+    if (s->cap < bytes) {
+      APACK_HIP(hipHostFree(s->host));
+      s->host = nullptr;
+      s->cap = 0;
+      apack_status st = staging_alloc(s, want);
+      if (st != APACK_OK) return st;   // the block stays idle, with no memory, until re-sized
+    }
+    s->busy = true;
+    s->stamp = ++g_stamp;
     *blk = s;
     *host = s->host;
     return APACK_OK;
   }
   auto* s = new Staging();
-  s->cap = align_up(bytes < 65536 ? 65536 : bytes, 65536);
   s->device = dev;
-  hipError_t e = hipHostMalloc(&s->host, s->cap, hipHostMallocDefault);
-  if (e != hipSuccess) {
+  apack_status st = staging_alloc(s, want);
+  if (st != APACK_OK) {
+    if (s->done) (void)hipEventDestroy(s->done);
     delete s;
-    return fail(APACK_E_HIP, "hipHostMalloc(%zu): %s", bytes, hipGetErrorString(e));
-  }
-  e = hipHostGetDevicePointer(&s->mapped, s->host, 0);
-  // The event only tells the host that the upload kernel has finished reading
-  // the block; no device write has to become visible to the host, so it skips
-  // the system-scope release (an L2 writeback that stalled the stream ~5 us).
-  if (e == hipSuccess) e = hipEventCreateWithFlags(&s->done, hipEventDisableTiming | hipEventDisableSystemFence);
-  if (e != hipSuccess) {
-    (void)hipHostFree(s->host);
-    delete s;
-    return fail(APACK_E_HIP, "staging block set-up: %s", hipGetErrorString(e));
+    return st;
   }
   s->busy = true;
+  s->stamp = ++g_stamp;
   g_pool.push_back(s);
   *blk = s;
   *host = s->host;

@@ -309,6 +309,25 @@ def test_inplace_with_nothing_to_move_is_ok_without_device():
     assert _inplace(n_out=0, layers=0, v=False, ws=None)[0] == 0
 
 
+def test_inplace_status_validation_without_device():
+    lib = A.library()
+    flag = ctypes.c_int32(7)
+    assert lib.apack_compact_kv_inplace_status(FAKE, 1024, None, None) == 1
+    assert lib.apack_compact_kv_inplace_status(None, 1024, ctypes.byref(flag), None) == 4
+    assert lib.apack_compact_kv_inplace_status(FAKE + 8, 1024, ctypes.byref(flag), None) == 4
+    assert lib.apack_compact_kv_inplace_status(FAKE, 4, ctypes.byref(flag), None) == 4
+    assert flag.value == 7   # untouched on error
+
+
+def test_inplace_wait_limit_round_trips():
+    prev = A.apack_set_inplace_wait_limit(12345)
+    try:
+        assert prev == 1 << 22
+        assert A.apack_set_inplace_wait_limit(0) == 12345
+    finally:
+        A.apack_set_inplace_wait_limit(prev)
+
+
 # -- scorer validation (fake device addresses, never dereferenced) ----------
 
 def _av(n_frames=8, per_frame=16, n_audio=100, n_query=4, vis_off=0, aud_off=0, qry_off=0):

@@ -219,12 +219,16 @@ def test_inplace_compaction_matches_gather(dtype, d, hid, prows, layers, n_in, k
 # -- edge cases ---------------------------------------------------------------
 
 
-def _synthetic(dtype, hq, hkv, d, seq_specs, seed, zero_keys=False, dup=None, lift=True):
-    """Small packed batch.  seq_specs: list of (spans, n_tokens, q_len, keep)."""
+def _synthetic(dtype, hq, hkv, d, seq_specs, seed, zero_keys=False, dup=None, lift=True, joint=(), bases=None):
+    """Small packed batch.  seq_specs: list of (spans, n_tokens, q_len, keep);
+    sequences listed in ``joint`` rank S jointly with keep[0], and ``bases``
+    maps a sequence to its keep basis.  With ``lift`` each sequence's top set
+    (per modality, or joint) is planted with a certified gap."""
     rng = np.random.default_rng(seed)
     seqs, tok, qrow = [], 0, 0
-    for spans, n, ql, keep in seq_specs:
-        seqs.append(W.PruneSeq(tok, n, spans, qrow, ql, keep))
+    for i, (spans, n, ql, keep) in enumerate(seq_specs):
+        basis = (bases or {}).get(i, (0, 0))
+        seqs.append(W.PruneSeq(tok, n, spans, qrow, ql, keep, basis, i in joint))
         tok += n
         qrow += ql
     scale = 1.0 if dtype == "f32" else 1.0 / math.sqrt(d)
@@ -234,12 +238,18 @@ def _synthetic(dtype, hq, hkv, d, seq_specs, seed, zero_keys=False, dup=None, li
     if lift and not zero_keys:
         qv = W.bf16_bits_to_f32(W.to_bf16_bits(qf)) if dtype == "bf16" else qf
         for i, s in enumerate(seqs):
-            topi = W._planted_sets(rng, s.tags(), s.keep, s.keep_basis)
+            if s.joint:
+                cand = np.flatnonzero(s.tags() != 0)
+                n = s.keep_basis[0] or cand.size
+                topi = {"joint": np.sort(rng.choice(cand, size=OP.keep_count(s.keep[0], n), replace=False))}
+                rows = topi["joint"]
+            else:
+                topi = W._planted_sets(rng, s.tags(), s.keep, s.keep_basis)
+                rows = np.concatenate([topi[1], topi[2]]).astype(np.int64)
             top[i] = topi
             if s.q_len == 0:
                 continue
             dirs = W._group_unit_dirs(qv[:, s.q_off:s.q_off + s.q_len], hkv)
-            rows = np.concatenate([topi[1], topi[2]]).astype(np.int64)
             if dtype == "f32":
                 n_rep = hq // hkv
                 for g in range(hkv):
@@ -313,14 +323,15 @@ def test_keep_zero_and_keep_all():
 
 
 def test_cumulative_keep_basis():
-    case = _synthetic("bf16", 8, 2, 128, [([(0, 300, A_), (300, 500, V_)], 830, 20, (0.5, 0.5))], seed=15,
-                      lift=False)
-    s = case.seqs[0]
-    seqs = [W.PruneSeq(s.tok_off, s.n_tokens, s.spans, s.q_off, s.q_len, (0.3, 0.3), (400, 700))]
-    w_scores, w_kept, w_n, _ = _oracle(case, seqs)
-    g_scores, g_kept, g_n = _run_prune(case, seqs)
-    assert g_n == w_n == [30 + 120 + 210]
-    _check_scores(g_scores, w_scores, seqs, "bf16")
+    """Counts against the original modality lengths (400 audio, 700 visual
+    rows before an earlier prune): 120 of the 300 audio and 210 of the 500
+    visual rows are kept, planted with a certified gap."""
+    case = _synthetic("bf16", 8, 2, 128, [([(0, 300, A_), (300, 500, V_)], 830, 20, (0.3, 0.3))], seed=15,
+                      bases={0: (400, 700)})
+    kept = _parity(case)
+    assert kept.size == 30 + 120 + 210
+    want = np.sort(np.concatenate([case.planted[0][A_], case.planted[0][V_], np.arange(800, 830)]))
+    np.testing.assert_array_equal(kept, want)
 
 
 def test_long_sequence_beyond_register_resident_select():
@@ -358,13 +369,16 @@ def test_joint_ranking_last_query_7b_layer():
 
 def test_joint_and_per_modality_sequences_in_one_batch():
     # A jointly ranked sequence next to a per-modality one, interleaved spans.
+    # Both sequences carry a planted top set (joint for the first), so the
+    # kept sets are certified by a gap >= 1e-2.
     specs = [([(0, 60, V_), (60, 40, A_), (100, 90, V_)], 230, 1, (0.85, 0.0)),
              ([(0, 300, A_), (300, 500, V_)], 900, 3, (0.6, 0.25))]
-    case = _synthetic("bf16", 28, 4, 128, specs, seed=41, lift=False)
-    seqs = list(case.seqs)
-    seqs[0] = W.PruneSeq(seqs[0].tok_off, seqs[0].n_tokens, seqs[0].spans, seqs[0].q_off, seqs[0].q_len,
-                         (0.85, 0.0), (0, 0), True)
-    _parity(case, seqs, min_margin=0)
+    case = _synthetic("bf16", 28, 4, 128, specs, seed=41, joint=(0,))
+    kept = _parity(case)
+    s0, s1 = case.seqs
+    want0 = np.sort(np.concatenate([case.planted[0]["joint"], np.arange(190, 230)]))
+    want1 = s1.tok_off + np.sort(np.concatenate([case.planted[1][A_], case.planted[1][V_], np.arange(800, 900)]))
+    np.testing.assert_array_equal(kept, np.concatenate([want0, want1]))
 
 
 def test_paper_schedule_every_layer_from_l_mid():
@@ -425,3 +439,103 @@ def test_paper_schedule_every_layer_from_l_mid():
     assert lengths == OF.step_schedule(T, n, list(pc.prune_layers), oracle_kept)
     _, ratio = A.apack_prefill_flops(lengths, n, d, m)
     assert ratio == pytest.approx(float(OF.flops_ratio(lengths, n, d, m)), rel=1e-13)
+
+
+def test_prune_and_compaction_are_deterministic():
+    """Two runs of the 7B post-scorer layer (cross-workgroup partial sums,
+    arrival counters, radix histograms) give bit-identical scores, kept rows
+    and compacted tensors."""
+    import paper_2608_08794_amd as A
+    case = W.prune_cfg3()
+    cache = W.cfg_cache(3, case)
+    q, k = to_dev(case.q, "bf16"), to_dev(case.k, "bf16")
+    v = to_dev(cache.v_layers[0], "bf16")
+    h = to_dev(cache.hidden, "bf16")
+    runs = []
+    for _ in range(2):
+        scores, kept, n_kept = A.apack_prune_layer(q, k, case.seqs)
+        m = n_kept[0]
+        ko, vo = (torch.empty((case.hkv, m, case.d), dtype=torch.bfloat16, device="cuda") for _ in range(2))
+        ho = torch.empty((m, h.shape[1]), dtype=torch.bfloat16, device="cuda")
+        A.apack_compact_kv(kept, case.k.shape[1], [k], [v], [ko], [vo], h, ho)
+        torch.cuda.synchronize()
+        runs.append([bits(t) for t in (scores, kept, ko, vo, ho)])
+    for name, a, b in zip(("scores", "kept", "k", "v", "hidden"), *runs):
+        assert np.array_equal(a, b), name
+
+
+def test_inplace_give_up_is_reported_and_stores_nothing():
+    """With the wait bound at 0 every ordering wait gives up at once (no
+    kernel spins): the status call reports it, and no ticket that gave up
+    stored anything, so rows whose readers sat in earlier stripes keep their
+    old contents.  Back at the default bound the same call is exact and the
+    status is clear."""
+    import paper_2608_08794_amd as A
+    rng = np.random.default_rng(77)
+    n_in, hkv, d = 5000, 3, 128
+    plane = W.payload_bits(rng, (hkv, n_in, d), "bf16")
+    src = np.sort(rng.choice(n_in, 1500, replace=False))
+    ws = torch.empty(A.apack_compact_kv_inplace_workspace(src.size), dtype=torch.uint8, device="cuda")
+    idx = torch.from_numpy(src.astype(np.int32)).cuda()
+    prev = A.apack_set_inplace_wait_limit(0)
+    try:
+        x = to_dev(plane, "bf16")
+        A.apack_compact_kv_inplace(idx, n_in, [x], workspace=ws)
+        assert A.apack_compact_kv_inplace_status(ws)
+    finally:
+        assert A.apack_set_inplace_wait_limit(prev) == 0
+    got = bits(x)
+    moved = OP.compact_rows(plane, src, axis=1)
+    # Each output row of each head plane (one work item's unit here) is
+    # either moved or untouched, never anything else.
+    for h in range(hkv):
+        for r in range(src.size):
+            assert np.array_equal(got[h, r], moved[h, r]) or np.array_equal(got[h, r], plane[h, r]), (h, r)
+    assert not np.array_equal(got[:, :src.size], moved)
+    assert np.array_equal(got[:, src.size:], plane[:, src.size:])
+    x = to_dev(plane, "bf16")
+    A.apack_compact_kv_inplace(idx, n_in, [x], workspace=ws)
+    assert not A.apack_compact_kv_inplace_status(ws)
+    assert np.array_equal(bits(x)[:, :src.size], moved)
+
+
+def test_entry_points_on_a_side_stream():
+    """Every entry point enqueued on a stream other than torch's current one,
+    with the binding allocating outputs and workspaces: results match the
+    oracle (the allocations are made on that stream, so their memory is not
+    handed out again while the call runs)."""
+    import paper_2608_08794_amd as A
+    side = torch.cuda.Stream()
+    case = W.prune_cfg2()
+    cache = W.cfg_cache(2, case)
+    w_scores, w_kept, w_n, _ = _oracle(case)
+    q, k = to_dev(case.q, "bf16"), to_dev(case.k, "bf16")
+    v = to_dev(cache.v_layers[0], "bf16")
+    torch.cuda.synchronize()
+    with torch.cuda.stream(torch.cuda.Stream()):   # the current stream is yet another one
+        scores, kept, n_kept = A.apack_prune_layer(q, k, case.seqs, stream=side)
+        side.synchronize()
+        junk = [torch.full((1 << 20,), 7, dtype=torch.int32, device="cuda") for _ in range(8)]
+        m = n_kept[0]
+        vo = torch.empty((case.hkv, m, case.d), dtype=torch.bfloat16, device="cuda")
+        A.apack_compact_kv(kept, case.k.shape[1], [v], (), [vo], (), stream=side)
+        xi = v.clone()
+        torch.cuda.current_stream().synchronize()
+        A.apack_compact_kv_inplace(kept, case.k.shape[1], [xi], stream=side)
+        dyn = W.dynamics_small("offset")
+        xv, xa, xq = (to_dev(x, "bf16") for x in (dyn.xv, dyn.xa, dyn.xq))
+        torch.cuda.current_stream().synchronize()
+        got = A.apack_score_dynamics(xv, xa, xq, dyn.seqs, dyn.params, stream=side)
+        side.synchronize()
+        del junk
+    assert n_kept == w_n
+    np.testing.assert_array_equal(kept.cpu().numpy().astype(np.int64), w_kept)
+    _check_scores(scores.cpu().numpy(), w_scores, case.seqs, "bf16")
+    np.testing.assert_array_equal(bits(vo), raw_bits(cache.v_layers[0], "bf16")[:, w_kept])
+    np.testing.assert_array_equal(bits(xi)[:, :m], raw_bits(cache.v_layers[0], "bf16")[:, w_kept])
+    from oracle import dynamics as OD
+    s = dyn.seqs[0]
+    r = OD.score_sequence(widen(dyn.xv, "bf16"), widen(dyn.xa, "bf16"), widen(dyn.xq, "bf16"), s.n_frames,
+                          s.per_frame, dyn.params)
+    np.testing.assert_array_equal(got["kept"].cpu().numpy().astype(np.int64), r["kept"])
+    np.testing.assert_array_equal(got["budget"].cpu().numpy(), r["frame_budget"])

@@ -215,6 +215,28 @@ apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* src_rows, in
                                       int32_t* pos, int32_t pos_rows, int64_t pos_stride,
                                       void* workspace, size_t workspace_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * in-place compaction as apack_compact_kv_inplace, with the same arguments
+ * and results, whose per-call counters live in a library-owned static device
+ * array instead of a caller workspace.  The call allocates nothing, on the
+ * device or the host.  Limit: n_out <= 2^20 kept rows (about 545 KiB of
+ * scratch per GPU, held until the process ends); a larger n_out returns
+ * APACK_E_UNSUPPORTED before anything is launched.  Every call on one GPU
+ * shares that GPU's array, so calls on one GPU that overlap in time (on
+ * different streams, or from different threads) race and must be ordered
+ * by the caller.  The first call on a device looks up that device's copy of
+ * the array; make it outside any graph capture.  A give-up of an ordering
+ * wait (see apack_set_inplace_wait_limit) is not reported for this variant:
+ * apack_compact_kv_inplace_status needs a caller workspace. */
+apack_status apack_compact_kv_inplace_static(int64_t n_out, const int32_t* src_rows, int64_t n_in,
+                                             int32_t n_layers, void* const* k, void* const* v,
+                                             int32_t hkv, int32_t d, apack_dtype dtype,
+                                             int64_t head_stride,
+                                             void* hidden, int32_t hidden_dim,
+                                             int32_t* pos, int32_t pos_rows, int64_t pos_stride,
+                                             void* stream);
+
 /* Reports whether the last apack_compact_kv_inplace call that moved rows
  * with this workspace gave up one of its waits.  The ordering waits are
  * bounded (see apack_set_inplace_wait_limit); a ticket whose wait gives up

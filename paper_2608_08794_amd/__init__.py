@@ -18,6 +18,7 @@ from ._lib import (  # noqa: F401
     DynParams,
     apack_compact_kv,
     apack_compact_kv_inplace,
+    apack_compact_kv_inplace_static,
     apack_compact_kv_inplace_status,
     apack_compact_kv_inplace_workspace,
     apack_dyn_params_default,

@@ -72,6 +72,9 @@ _SIGS = {
                                         ctypes.POINTER(_P), ctypes.POINTER(_P), _I32, _I32, ctypes.c_int,
                                         _I64, _I64, _P, _P, _I32, _P, _P, _I32, _I64, _I64, _P]),
     "apack_compact_kv_inplace_workspace": (_SZ, [_I64]),
+    "apack_compact_kv_inplace_static": (ctypes.c_int, [_I64, _P, _I64, _I32, ctypes.POINTER(_P),
+                                                       ctypes.POINTER(_P), _I32, _I32, ctypes.c_int, _I64, _P,
+                                                       _I32, _P, _I32, _I64, _P]),
     "apack_compact_kv_inplace_status": (ctypes.c_int, [_P, _SZ, ctypes.POINTER(_I32), _P]),
     "apack_set_inplace_wait_limit": (ctypes.c_uint32, [ctypes.c_uint32]),
     "apack_layer_flops": (ctypes.c_double, [_I64, _I64, _I64]),
@@ -306,11 +309,9 @@ def apack_compact_kv_inplace_workspace(n_out):
     return int(library().apack_compact_kv_inplace_workspace(int(n_out)))
 
 
-def apack_compact_kv_inplace(src_rows, n_in, k=(), v=(), hidden=None, pos=None, workspace=None, stream=None):
-    """x[i] = x[src_rows[i]] in place for every K/V layer tensor [Hkv, rows, D]
-    (v may be empty: K planes only), the hidden states [rows, H] and the
-    position ids [P, rows]; src_rows must be strictly increasing.  Rows
-    [0, n_out) hold the result, later rows keep their contents."""
+def _inplace_args(src_rows, k, v, hidden, pos):
+    """(n_out, K table, V table, hkv, d, dtype code, head stride, hidden
+    width, position rows, position stride) of an in-place compaction."""
     n_out = int(src_rows.numel())
     n_layers = len(k)
     if len(v) not in (0, n_layers):
@@ -339,13 +340,31 @@ def apack_compact_kv_inplace(src_rows, n_in, k=(), v=(), hidden=None, pos=None, 
         prow, ps = pos.shape[0], pos.stride(0)
         if pos.stride(1) != 1:
             raise ApackError(2, "position ids must have unit column stride")
+    return n_out, tk, tv, hkv, d, code, hs, hid, prow, ps
+
+
+def apack_compact_kv_inplace(src_rows, n_in, k=(), v=(), hidden=None, pos=None, workspace=None, stream=None):
+    """x[i] = x[src_rows[i]] in place for every K/V layer tensor [Hkv, rows, D]
+    (v may be empty: K planes only), the hidden states [rows, H] and the
+    position ids [P, rows]; src_rows must be strictly increasing.  Rows
+    [0, n_out) hold the result, later rows keep their contents."""
+    n_out, tk, tv, hkv, d, code, hs, hid, prow, ps = _inplace_args(src_rows, k, v, hidden, pos)
     need = apack_compact_kv_inplace_workspace(n_out)
     if workspace is None:
         with _alloc_on(stream):
             workspace = _workspace(need, src_rows.device)
     _check(library().apack_compact_kv_inplace(
-        n_out, _ptr(src_rows), int(n_in), n_layers, tk, tv, hkv, d, code, hs,
+        n_out, _ptr(src_rows), int(n_in), len(k), tk, tv, hkv, d, code, hs,
         _ptr(hidden), hid, _ptr(pos), prow, ps, workspace.data_ptr(), workspace.numel(), _stream(stream)))
+
+
+def apack_compact_kv_inplace_static(src_rows, n_in, k=(), v=(), hidden=None, pos=None, stream=None):
+    """apack_compact_kv_inplace with the library's static scratch instead of a
+    workspace: allocates nothing (n_out <= 2^20)."""
+    n_out, tk, tv, hkv, d, code, hs, hid, prow, ps = _inplace_args(src_rows, k, v, hidden, pos)
+    _check(library().apack_compact_kv_inplace_static(
+        n_out, _ptr(src_rows), int(n_in), len(k), tk, tv, hkv, d, code, hs,
+        _ptr(hidden), hid, _ptr(pos), prow, ps, _stream(stream)))
 
 
 def apack_compact_kv_inplace_status(workspace, stream=None):

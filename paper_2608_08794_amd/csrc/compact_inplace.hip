@@ -31,9 +31,10 @@
 // earlier stripe has yet to read is ever overwritten; the caller learns of
 // it from apack_compact_kv_inplace_status.
 #include <algorithm>
+#include <array>
 #include <atomic>
 #include <cstring>
-#include <vector>
+#include <mutex>
 
 #include "common.hpp"
 #include "sync.hpp"
@@ -356,6 +357,50 @@ int resident_groups() {
 std::atomic<uint32_t> g_wait_limit{kDefaultWaitLimit};
 
 }  // namespace
+
+// Library-owned scratch of apack_compact_kv_inplace_static: the workspace of
+// a compaction of up to kStaticRows kept rows (ticket, status word, one
+// counter line per stripe and the stripes' first readers), one copy per
+// GPU, held until the process ends.  Host code never uses this name as an
+// address: each device's copy is reached through the pointer that
+// hipGetSymbolAddress returns on that device.
+constexpr int64_t kStaticRows = int64_t(1) << 20;
+constexpr int64_t kStaticStripes = kStaticRows / kStripe;
+constexpr size_t kStaticBytes = 256 + (size_t)kStaticStripes * kCounterPad * 4 +
+                                ((size_t)(kStaticStripes + 1) * 4 + 255) / 256 * 256;
+static __device__ __align__(256) uint8_t scratch[kStaticBytes];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+std::array<void*, kMaxDevices> g_scratch{};   // device address of scratch, per device
+
+// The address of the current device's copy of `scratch`, looked up once per
+// device with that device current.
+apack_status static_scratch(void** ptr) {
+  int dev = 0;
+  APACK_HIP(hipGetDevice(&dev));
+  APACK_CHECK(dev >= 0 && dev < kMaxDevices, APACK_E_UNSUPPORTED, "device %d beyond the %d this build tracks", dev,
+              kMaxDevices);
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    APACK_CHECK(e == hipSuccess && p, APACK_E_HIP, "hipGetSymbolAddress(scratch) on device %d: %s", dev,
+                hipGetErrorString(e));
+    g_scratch[dev] = p;
+  }
+  *ptr = g_scratch[dev];
+  return APACK_OK;
+}
+
+apack_status compact_inplace(int64_t n_out, const int32_t* src_rows, int64_t n_in, int32_t n_layers,
+                             void* const* k, void* const* v, int32_t hkv, int32_t d, apack_dtype dtype,
+                             int64_t head_stride, void* hidden, int32_t hidden_dim, int32_t* pos, int32_t pos_rows,
+                             int64_t pos_stride, void* workspace, size_t workspace_bytes, void* stream);
+
+}  // namespace
 }  // namespace apack
 
 using namespace apack;
@@ -391,6 +436,37 @@ extern "C" apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* s
                                                  int64_t pos_stride, void* workspace, size_t workspace_bytes,
                                                  void* stream) {
   clear_error();
+  return compact_inplace(n_out, src_rows, n_in, n_layers, k, v, hkv, d, dtype, head_stride, hidden, hidden_dim, pos,
+                         pos_rows, pos_stride, workspace, workspace_bytes, stream);
+}
+
+extern "C" apack_status apack_compact_kv_inplace_static(int64_t n_out, const int32_t* src_rows, int64_t n_in,
+                                                        int32_t n_layers, void* const* k, void* const* v,
+                                                        int32_t hkv, int32_t d, apack_dtype dtype,
+                                                        int64_t head_stride, void* hidden, int32_t hidden_dim,
+                                                        int32_t* pos, int32_t pos_rows, int64_t pos_stride,
+                                                        void* stream) {
+  clear_error();
+  APACK_CHECK(n_out <= kStaticRows, APACK_E_UNSUPPORTED,
+              "n_out (%lld) exceeds the %lld kept rows the static scratch holds", (long long)n_out,
+              (long long)kStaticRows);
+  void* ws = nullptr;
+  if (n_out > 0) {
+    const apack_status st = static_scratch(&ws);
+    if (st != APACK_OK) return st;
+  }
+  return compact_inplace(n_out, src_rows, n_in, n_layers, k, v, hkv, d, dtype, head_stride, hidden, hidden_dim, pos,
+                         pos_rows, pos_stride, ws, kStaticBytes, stream);
+}
+
+namespace apack {
+namespace {
+
+// Validation and launch of one in-place compaction (both entry points).
+apack_status compact_inplace(int64_t n_out, const int32_t* src_rows, int64_t n_in, int32_t n_layers,
+                             void* const* k, void* const* v, int32_t hkv, int32_t d, apack_dtype dtype,
+                             int64_t head_stride, void* hidden, int32_t hidden_dim, int32_t* pos, int32_t pos_rows,
+                             int64_t pos_stride, void* workspace, size_t workspace_bytes, void* stream) {
   APACK_CHECK(dtype_ok(dtype), APACK_E_DTYPE, "unknown dtype %d", (int)dtype);
   APACK_CHECK(n_out >= 0 && n_in >= 0, APACK_E_SHAPE, "negative row count");
   APACK_CHECK(n_out <= n_in, APACK_E_SHAPE, "n_out (%lld) exceeds n_in (%lld)", (long long)n_out,
@@ -416,18 +492,24 @@ extern "C" apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* s
     APACK_CHECK(pos_stride >= n_in, APACK_E_SHAPE, "position row stride must be >= rows");
   }
   // Every plane is distinct; src_rows and the workspace touch none of them.
-  std::vector<std::pair<const void*, size_t>> bufs;
+  // (A fixed table: this path allocates nothing, on the host or the device.)
+  struct Buf {
+    const void* p;
+    size_t bytes;
+  };
+  Buf bufs[kMaxTensors + 2];
+  int n_bufs = 0;
   const size_t kv_bytes = n_layers ? (size_t)((hkv - 1) * head_stride + n_in * d) * es : 0;
   for (int l = 0; l < n_layers; ++l) {
     APACK_CHECK(k[l] && (!has_v || v[l]), APACK_E_ARG, "layer %d: NULL K/V pointer", l);
-    bufs.emplace_back(k[l], kv_bytes);
-    if (has_v) bufs.emplace_back(v[l], kv_bytes);
+    bufs[n_bufs++] = Buf{k[l], kv_bytes};
+    if (has_v) bufs[n_bufs++] = Buf{v[l], kv_bytes};
   }
-  if (has_h) bufs.emplace_back(hidden, (size_t)n_in * hidden_dim * es);
-  if (has_p) bufs.emplace_back(pos, (size_t)((pos_rows - 1) * pos_stride + n_in) * 4);
-  for (size_t i = 0; i < bufs.size(); ++i)
-    for (size_t j = i + 1; j < bufs.size(); ++j)
-      APACK_CHECK(!overlaps(bufs[i].first, bufs[i].second, bufs[j].first, bufs[j].second), APACK_E_ALIAS,
+  if (has_h) bufs[n_bufs++] = Buf{hidden, (size_t)n_in * hidden_dim * es};
+  if (has_p) bufs[n_bufs++] = Buf{pos, (size_t)((pos_rows - 1) * pos_stride + n_in) * 4};
+  for (int i = 0; i < n_bufs; ++i)
+    for (int j = i + 1; j < n_bufs; ++j)
+      APACK_CHECK(!overlaps(bufs[i].p, bufs[i].bytes, bufs[j].p, bufs[j].bytes), APACK_E_ALIAS,
                   "two compacted tensors overlap");
   const InplaceLayout lay = inplace_layout(n_out);
   if (n_out > 0) {
@@ -435,10 +517,10 @@ extern "C" apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* s
                 "workspace must be non-NULL and %zu-byte aligned", kAlign);
     APACK_CHECK(workspace_bytes >= lay.bytes, APACK_E_WORKSPACE, "workspace of %zu bytes < %zu needed",
                 workspace_bytes, lay.bytes);
-    for (auto& b : bufs) {
-      APACK_CHECK(!overlaps(b.first, b.second, src_rows, (size_t)n_out * 4), APACK_E_ALIAS,
+    for (int i = 0; i < n_bufs; ++i) {
+      APACK_CHECK(!overlaps(bufs[i].p, bufs[i].bytes, src_rows, (size_t)n_out * 4), APACK_E_ALIAS,
                   "src_rows overlaps a compacted tensor");
-      APACK_CHECK(!overlaps(b.first, b.second, workspace, lay.bytes), APACK_E_ALIAS,
+      APACK_CHECK(!overlaps(bufs[i].p, bufs[i].bytes, workspace, lay.bytes), APACK_E_ALIAS,
                   "the workspace overlaps a compacted tensor");
     }
     APACK_CHECK(!overlaps(src_rows, (size_t)n_out * 4, workspace, lay.bytes), APACK_E_ALIAS,
@@ -523,3 +605,6 @@ extern "C" apack_status apack_compact_kv_inplace(int64_t n_out, const int32_t* s
     hipLaunchKernelGGL(k_compact_inplace<uint32_t>, dim3(grid), dim3(kThreads), 0, hs, a);
   return launch_status("k_compact_inplace");
 }
+
+}  // namespace
+}  // namespace apack

@@ -319,6 +319,16 @@ def test_inplace_status_validation_without_device():
     assert flag.value == 7   # untouched on error
 
 
+def test_inplace_static_rejects_more_rows_than_its_scratch_without_device():
+    lib = A.library()
+    tk = (ctypes.c_void_p * 1)(FAKE + (1 << 34))
+    st = lib.apack_compact_kv_inplace_static((1 << 20) + 1, FAKE, (1 << 20) + 2, 1, tk, None, 1, 8, 0,
+                                             (1 << 20) + 2 << 3, None, 0, None, 0, 0, None)
+    assert st == 7 and "static scratch" in lib.apack_last_error().decode()
+    # Nothing to move: returns before touching the device.
+    assert lib.apack_compact_kv_inplace_static(0, None, 10, 0, None, None, 0, 0, 0, 0, None, 0, None, 0, 0, None) == 0
+
+
 def test_inplace_wait_limit_round_trips():
     prev = A.apack_set_inplace_wait_limit(12345)
     try:

@@ -59,7 +59,15 @@ typedef enum apack_status {
   APACK_E_UNSUPPORTED = 7 /* valid but outside what this build implements  */
 } apack_status;
 
-typedef enum apack_dtype { APACK_BF16 = 0, APACK_F32 = 1 } apack_dtype;
+/* The two bounding enumerators make every int32 value a valid apack_dtype,
+ * so a wrong value passed by a caller is rejected (APACK_E_DTYPE) rather
+ * than being undefined behaviour in the library. */
+typedef enum apack_dtype {
+  APACK_BF16 = 0,
+  APACK_F32 = 1,
+  APACK_DTYPE_MIN_ENUM_ = -0x7FFFFFFF - 1,
+  APACK_DTYPE_MAX_ENUM_ = 0x7FFFFFFF
+} apack_dtype;
 
 typedef enum apack_modality {
   APACK_OTHER = 0,  /* text, system and any row not covered by a span */

@@ -56,5 +56,54 @@ def build(verbose=False):
     return LIB
 
 
+ASAN_BUILD = os.path.join(HERE, "_build_asan")
+ASAN_LIB = os.path.join(ASAN_BUILD, "libapack_asan.so")
+# Host code only: every -fsanitize= follows -Xarch_host, so the device code
+# is compiled exactly as in the product build.
+ASAN_FLAGS = ["-Xarch_host", "-fsanitize=address", "-Xarch_host", "-fsanitize=undefined",
+              "-Xarch_host", "-fno-sanitize-recover=undefined", "-Xarch_host", "-fno-omit-frame-pointer",
+              "-Xarch_host", "-g", "-shared-libasan"]
+
+
+def asan_runtime():
+    """The shared AddressSanitizer runtime the sanitized library needs
+    preloaded into a host process that was not built with it."""
+    out = subprocess.run([HIPCC, "-print-file-name=libclang_rt.asan-x86_64.so"], capture_output=True, text=True)
+    path = out.stdout.strip()
+    if os.path.isabs(path) and os.path.exists(path):
+        return path
+    cands = sorted(glob.glob(os.path.join(os.path.dirname(os.path.realpath(HIPCC)), "..", "llvm", "lib", "clang",
+                                          "*", "lib", "linux", "libclang_rt.asan-x86_64.so")))
+    if not cands:
+        raise RuntimeError("libclang_rt.asan-x86_64.so not found")
+    return os.path.realpath(cands[-1])
+
+
+def build_sanitized(verbose=False):
+    """libapack with its host code (validation, planning, staging, launch
+    set-up) built with AddressSanitizer and UndefinedBehaviorSanitizer, for
+    CPU-only runs of the ABI tests; the device code is unchanged."""
+    os.makedirs(ASAN_BUILD, exist_ok=True)
+    srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
+
+    def comp(src):
+        obj = os.path.join(ASAN_BUILD, os.path.basename(src) + ".o")
+        r = subprocess.run([HIPCC, *FLAGS, *ASAN_FLAGS, "-c", src, "-o", obj], capture_output=True, text=True)
+        if r.returncode != 0:
+            raise RuntimeError(f"hipcc (sanitized) failed on {src}:\n{r.stdout}{r.stderr}")
+        return obj
+
+    with concurrent.futures.ThreadPoolExecutor(max_workers=min(8, len(srcs))) as ex:
+        objs = list(ex.map(comp, srcs))
+    r = subprocess.run([HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *ASAN_FLAGS, "-o", ASAN_LIB, *objs],
+                       capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("sanitized link failed:\n" + r.stdout + r.stderr)
+    return ASAN_LIB
+
+
 if __name__ == "__main__":
-    print(build(verbose=True))
+    if len(sys.argv) > 1 and sys.argv[1] == "asan":
+        print(build_sanitized(verbose=True))
+    else:
+        print(build(verbose=True))

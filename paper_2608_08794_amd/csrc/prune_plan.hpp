@@ -21,7 +21,10 @@ constexpr int kKeyTile = APACK_KEY_TILE;       // keys per LDS stage of the scor
 constexpr int kRB = APACK_ROW_BLOCKS;          // 32-row query blocks held by one wave
 constexpr int kRowsPerWave = 32 * kRB;
 constexpr int kMaxWaves = 8;                   // waves per score workgroup
-constexpr int kMaxChunk = 4096;               // keys per score workgroup, at most
+#ifndef APACK_MAX_CHUNK
+#define APACK_MAX_CHUNK 4096
+#endif
+constexpr int kMaxChunk = APACK_MAX_CHUNK;    // keys per score workgroup, at most
 constexpr int kRowTile = 1024;   // rows per workgroup of the select and compaction kernels
 
 // Per-sequence descriptor on the device (uploaded once per call).  The

@@ -1203,44 +1203,156 @@ __device__ __forceinline__ void wave_argmax(double& v, int& idx) {
   }
 }
 
-// Density of token i for DA-FPS: the mean of its dafps_k largest cosines to
-// the other tokens of the frame, and how many of those cosines reach the
-// coverage threshold.  Rows of S below R are cosines in LDS; later rows are
-// read from the raw Gram and turned into cosines with its diagonal dg.  The running top list lives in registers (static
-// indices only): each new value is carried down past the larger ones.  S is
-// exactly symmetric (entries (i, j) and (j, i) are the same products summed
-// in the same order), so thread i reads column i and a wave's loads for one
-// j are contiguous; loads are issued eight at a time.
+// v_max_f64 / v_min_f64 as single instructions.  In IEEE mode the
+// compiler quiets possible signalling NaNs before fmax / fmin with an extra
+// max of each operand with itself; no value here is a signalling NaN
+// (every one comes from arithmetic or from the Gram), and a quiet NaN
+// operand gives the other one, as fmax / fmin do.
+__device__ __forceinline__ double max_f64(double a, double b) {
+  double r;
+  asm("v_max_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+__device__ __forceinline__ double min_f64(double a, double b) {
+  double r;
+  asm("v_min_f64 %0, %1, %2" : "=v"(r) : "v"(a), "v"(b));
+  return r;
+}
+
+// Unsigned key with the numeric order of doubles: positive values (sign bit
+// clear) get the sign bit set, negative ones are negated as 64-bit integers,
+// so the larger magnitude gives the smaller key and -0 gets the key of +0.
+// Equal values have equal keys; every key is above 0 except those of
+// negative NaNs.
+__device__ __forceinline__ uint64_t order_key(double v) {
+  const uint64_t b = (uint64_t)__double_as_longlong(v);
+  return (b >> 63) ? (uint64_t)0 - b : (b | 0x8000000000000000ull);
+}
+
+// Maximum of a 32-bit value over the 64 lanes, in every lane: DPP within
+// 16-lane rows, then the row-pair and half swaps.  All lanes active.
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t v) {
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0xB1, 0xF, 0xF, true));   // quad_perm [1,0,3,2]
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x4E, 0xF, 0xF, true));   // quad_perm [2,3,0,1]
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x141, 0xF, 0xF, true));  // row_half_mirror
+  v = max(v, (uint32_t)__builtin_amdgcn_update_dpp(0, (int)v, 0x140, 0xF, 0xF, true));  // row_mirror
+  const auto r = __builtin_amdgcn_permlane16_swap(v, v, false, false);
+  v = max((uint32_t)r[0], (uint32_t)r[1]);
+  const auto h = __builtin_amdgcn_permlane32_swap(v, v, false, false);
+  return max((uint32_t)h[0], (uint32_t)h[1]);
+}
+
+// Cosine of tokens i and j of an anchor frame from their Gram entry g, the
+// Gram's diagonal entries d (squared norms, summed like every entry) and
+// r = 1 / sqrt(d): exactly 1 when g equals both diagonal entries and is not
+// 0, which is also exactly what g / sqrt(d_i d_j) gives there (a token and a
+// bitwise copy of it); otherwise g (r_i r_j), within a few ulps of that
+// quotient and symmetric in i and j; 0 for a zero-norm token (r = 0).  The
+// three tests are combined without branches.
+__device__ __forceinline__ double cos_gram(double g, double di, double ri, double dj, double rj) {
+  const double c = g * (ri * rj);
+  const bool one = (g == di) & (g == dj) & (g != 0.0);
+  return one ? 1.0 : c;
+}
+
+// Running list of the KM largest values, sorted descending: a new value is
+// carried down past the larger entries (static indices, all in registers).
 template <int KM>
-__device__ __forceinline__ double dafps_density(const double* S, const double* Sl, const double* dg, int R, int P,
-                                                int i, int k, double cover) {
+__device__ __forceinline__ void top_insert(double (&top)[KM], double v) {
+#pragma unroll
+  for (int q = 0; q < KM; ++q) {
+    const double hi = max_f64(top[q], v);
+    v = min_f64(top[q], v);
+    top[q] = hi;
+  }
+}
+
+// LDS of k_dafps, in doubles (160 KiB).
+constexpr int kDafpsLds = 20480;
+
+struct DafpsLds {
+  double* rows;    // rows [0, R) of the frame's cosine matrix, P apart
+  double* corner;  // entries (j, t), j and t in [R, P): (P - R)^2 of them
+  double2* nrm;    // (d, r) per token
+  double* rho;     // densities
+  int R;
+  bool has_corner;
+};
+
+// Density of token i: the mean of its dafps_k largest cosines to the other
+// tokens of the frame, times one plus the number of those cosines at or
+// above the coverage threshold.  Two lanes of a wave (2i and 2i + 1) share
+// token i, each walking its own rows [lo, hi) of column i of the Gram (S is
+// exactly symmetric: entries (i, j) and (j, i) are the same products summed
+// in the same order); each entry becomes a cosine, written back over the
+// Gram entry in LDS (rows below R) or into the corner block (rows and token
+// at or past R), so that the pick loop reads cosines.  Rows at or past R
+// come from the Gram in global memory, the first eight of a lane's share
+// prefetched into `pre` before the rows were staged.  Reads are issued
+// eight rows at a time; ns and ng bound, for every lane of the wave, the
+// staged and global row counts.  The two halves' lists and counts are then
+// merged across the lane pair.  KM >= min(dafps_k, P - 1): only the first
+// min(dafps_k, P - 1) entries of the merged list enter the mean.  Every
+// lane of the wave must take part (lanes of tokens past P with empty
+// ranges).
+template <int KM>
+__device__ __forceinline__ double dafps_density(const DafpsLds& L, const double* __restrict__ S, int P, int i,
+                                                int lo, int hi, int ns, int ng, const double (&pre)[8], double di,
+                                                double ri, int k, double cover) {
   double top[KM];
 #pragma unroll
   for (int q = 0; q < KM; ++q) top[q] = -INFINITY;
   int cov = 0;
-  for (int j0 = 0; j0 < P; j0 += 8) {
-    double vals[8];
+  const int R = L.R, ic = min(i, P - 1);
+  const int s_end = min(hi, R), g_lo = max(lo, R);
+  auto take = [&](bool valid, int j, double c) {
+    const bool use = valid & (j != i);
+    cov += (int)(use & (c >= cover));
+    top_insert(top, use ? c : -INFINITY);
+  };
+  for (int jj = 0; jj < ns; jj += 8) {
+    double g[8];
+    double2 nj[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int j = j0 + u;
-      vals[u] = j >= P ? 0.0 : j < R ? Sl[j * P + i] : cos_from(S[(int64_t)j * P + i], dg[j], dg[i]);
+      const int j = min(lo + jj + u, R - 1);
+      g[u] = L.rows[j * P + ic];
+      nj[u] = L.nrm[j];
     }
 #pragma unroll
     for (int u = 0; u < 8; ++u) {
-      const int j = j0 + u;
-      if (j >= P || j == i) continue;
-      double v = vals[u];
-      if (v >= cover) ++cov;
-#pragma unroll
-      for (int q = 0; q < KM; ++q) {
-        if (q < k) {
-          const double hi = fmax(top[q], v);
-          v = fmin(top[q], v);
-          top[q] = hi;
-        }
-      }
+      const int j = lo + jj + u;
+      const bool valid = j < s_end;
+      const double c = cos_gram(g[u], di, ri, nj[u].x, nj[u].y);
+      if (valid) L.rows[j * P + i] = c;
+      take(valid, j, c);
     }
   }
+  auto tail = [&](int j0, const double (&g)[8]) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      const int j = j0 + u;
+      const bool valid = j < hi;
+      const double2 nj = L.nrm[min(j, P - 1)];
+      const double c = cos_gram(g[u], di, ri, nj.x, nj.y);
+      if (valid && L.has_corner && i >= R) L.corner[(j - R) * (P - R) + (i - R)] = c;
+      take(valid, j, c);
+    }
+  };
+  if (ng > 0) tail(g_lo, pre);
+  for (int jj = 8; jj < ng; jj += 8) {
+    double g[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) g[u] = S[(int64_t)min(g_lo + jj + u, P - 1) * P + ic];
+    tail(g_lo + jj, g);
+  }
+  // Merge with the partner lane's list and count.
+  double o[KM];
+#pragma unroll
+  for (int q = 0; q < KM; ++q) o[q] = dpp_f64<0xB1>(top[q]);
+#pragma unroll
+  for (int q = 0; q < KM; ++q) top_insert(top, o[q]);
+  cov += __builtin_amdgcn_update_dpp(cov, cov, 0xB1, 0xF, 0xF, false);
   const int nt = min(k, P - 1);
   double knn = 0.0;
 #pragma unroll
@@ -1250,144 +1362,238 @@ __device__ __forceinline__ double dafps_density(const double* S, const double* S
   return fmax(knn, 0.0) * (1.0 + cov);
 }
 
+// DA-FPS picks in one wave: token t = lane + 64 u, u < KU; tc is t clamped
+// into the frame (addresses of lanes past the end stay in bounds; those
+// tokens count as taken).  The first pick is the densest token, each later
+// one the token farthest from the picked set, weighted by density:
+// argmax of (1 - max cosine to the picked set) rho^power.  The argmax is
+// lexicographic (value desc, token asc): the wave's largest order key, then
+// the lowest token holding it -- tokens 64u + lane ascend with u and then
+// with the lane, so the first non-empty ballot in u order names it.  Taken
+// tokens have key 0, below every value's key except a negative NaN's; should
+// no untaken token reach the maximum key (negative NaNs only), the lowest
+// untaken token is taken, so a pick is always valid.  The picked positions
+// go to kept[out...] in ascending order, as rows base + t.
+template <int KU>
+__device__ __forceinline__ void dafps_pick(const DafpsLds& L, const double* __restrict__ S, int P, int k,
+                                           double power, int lane, int32_t* __restrict__ kept, int64_t out,
+                                           int64_t base) {
+  const int R = L.R;
+  double wgt[KU], smax[KU], dt[KU], rt[KU];
+  uint64_t key[KU];
+  bool taken[KU];
+  int tc[KU];
+#pragma unroll
+  for (int u = 0; u < KU; ++u) {
+    const int t = lane + 64 * u;
+    taken[u] = t >= P;
+    tc[u] = min(t, P - 1);
+    const double rho = L.rho[tc[u]];
+    wgt[u] = taken[u] ? 0.0 : pow(rho, power);
+    key[u] = taken[u] ? 0 : order_key(rho);
+    smax[u] = -INFINITY;
+    const double2 n = L.nrm[tc[u]];
+    dt[u] = n.x;
+    rt[u] = n.y;
+  }
+  auto pick_of = [&]() {
+    uint64_t kb = key[0];
+#pragma unroll
+    for (int u = 1; u < KU; ++u) kb = key[u] > kb ? key[u] : kb;
+    const uint32_t mh = wave_max_u32((uint32_t)(kb >> 32));
+    const uint32_t ml = wave_max_u32((uint32_t)(kb >> 32) == mh ? (uint32_t)kb : 0u);
+    const uint64_t mk = ((uint64_t)__builtin_amdgcn_readfirstlane(mh) << 32) | (uint32_t)__builtin_amdgcn_readfirstlane(ml);
+    int best = 0x7FFFFFFF;
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+      const uint64_t b = __ballot(!taken[u] && key[u] == mk);
+      if (b && best == 0x7FFFFFFF) best = 64 * u + (int)__builtin_ctzll(b);
+    }
+    if (best == 0x7FFFFFFF) {
+#pragma unroll
+      for (int u = 0; u < KU; ++u) {
+        const uint64_t b = __ballot(!taken[u]);
+        if (b && best == 0x7FFFFFFF) best = 64 * u + (int)__builtin_ctzll(b);
+      }
+    }
+    return best;
+  };
+  int pick = pick_of();
+  for (int n = 0;; ++n) {
+    double sv[KU];
+    if (pick < R) {  // the same branch for the whole wave
+#pragma unroll
+      for (int u = 0; u < KU; ++u) sv[u] = L.rows[pick * P + tc[u]];
+    } else {
+      const double2 np = L.nrm[pick];
+#pragma unroll
+      for (int u = 0; u < KU; ++u) {
+        if (tc[u] < R)
+          sv[u] = L.rows[tc[u] * P + pick];
+        else if (L.has_corner)
+          sv[u] = L.corner[(pick - R) * (P - R) + (tc[u] - R)];
+        else
+          sv[u] = cos_gram(S[(int64_t)pick * P + tc[u]], np.x, np.y, dt[u], rt[u]);
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < KU; ++u) {
+      if (lane + 64 * u == pick) taken[u] = true;
+      smax[u] = max_f64(smax[u], sv[u]);
+    }
+    if (n + 1 >= k) break;
+#pragma unroll
+    for (int u = 0; u < KU; ++u) key[u] = taken[u] ? 0 : order_key((1.0 - smax[u]) * wgt[u]);
+    pick = pick_of();
+  }
+  // Ascending output of the picked positions.
+#pragma unroll
+  for (int u = 0; u < KU; ++u) {
+    const int t = lane + 64 * u;
+    const bool kp = t < P && taken[u];
+    const uint64_t bal = __ballot(kp);
+    if (kp) kept[out + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(base + t);
+    out += __popcll(bal);
+  }
+}
 
 // ---------------------------------------------------------------------------
-// DA-FPS on an anchor frame: one workgroup, thread i owns token i.
+// DA-FPS on an anchor frame: one workgroup, two threads per token.
 // ---------------------------------------------------------------------------
-// The anchor's first R rows of its raw Gram (as many as fit) are copied to
-// LDS and turned into cosines there, S_ij = G_ij / sqrt(G_ii G_jj): the
-// diagonal went through the same MFMA sums as every entry, so a token and
-// a bitwise copy of it have cosine exactly 1.  The pick loop then runs in one wave, which holds up to four tokens per lane
-// and finds each pick with a shuffle argmax, so a pick costs one LDS row
-// read (a global one for the few rows past R) and no barrier.
-constexpr int kDafpsLdsDoubles = 19968;   // 159744 bytes of S rows; 160 KiB of LDS with rho and the diagonal
+// The frame's raw Gram rows [0, R) go to LDS by direct loads; R is the
+// largest row count for which those rows, the (P - R) x (P - R) corner block
+// and the per-token arrays fit in 160 KiB (R = P up to P = 141, 139 rows of
+// 144), else as many rows as fit without the corner.  The density pass
+// (threads 2i and 2i + 1 on token i, rows split at (P + 1) / 2) turns every
+// entry into a cosine (cos_gram).  The pick loop then runs in one wave,
+// which holds up to four tokens per lane and finds each pick from order
+// keys reduced by DPP (dafps_pick); a pick reads one cosine row from LDS:
+// row `pick` itself when pick < R, else column `pick` of the staged rows
+// (the same values, by symmetry) and the corner block -- or, when the
+// corner did not fit, the Gram row in global memory, turned into cosines as
+// it is read.
+constexpr int kDafpsThreads = 2 * kMaxPerFrame;
 
-__global__ __launch_bounds__(kMaxPerFrame) void k_dafps(const ClipDev* __restrict__ clips,
-                                                        const FrameDev* __restrict__ frames,
-                                                        const FramePlanDev* __restrict__ plan, DynParamsDev prm,
-                                                        const double* __restrict__ gram, int32_t* __restrict__ kept) {
-  __shared__ __attribute__((aligned(16))) double Sl[kDafpsLdsDoubles];
-  __shared__ double rho_sh[kMaxPerFrame];
-  __shared__ double dg[kMaxPerFrame];
+__global__ __launch_bounds__(kDafpsThreads) void k_dafps(const ClipDev* __restrict__ clips,
+                                                         const FrameDev* __restrict__ frames,
+                                                         const FramePlanDev* __restrict__ plan, DynParamsDev prm,
+                                                         const double* __restrict__ gram, int32_t* __restrict__ kept) {
+  __shared__ __attribute__((aligned(16))) double lds[kDafpsLds];
   const FrameDev fr = frames[blockIdx.x];
   const ClipDev c = clips[fr.clip];
   const int64_t frame = c.frame_off + fr.f;
   const FramePlanDev fp = plan[frame];
   if (!fp.is_anchor || fp.budget == 0) return;
-  const int P = c.per_frame, i = threadIdx.x;
+  const int P = c.per_frame, tid = threadIdx.x, i = tid >> 1, h = tid & 1;
   const int k = min(fp.budget, P);
   const double* S = gram + c.gram_off + (int64_t)fr.f * P * P;
-  const int R = min(P, kDafpsLdsDoubles / P);
-  if (i < P) dg[i] = S[(int64_t)i * P + i];
-  if (((uintptr_t)S & 15) == 0) {
-    // Rows [0, R) of S into LDS with 16-byte direct-to-LDS loads, all in
-    // flight together: wave load j fills bytes [1024 j, 1024 j + 1024), lane
-    // l the 16 bytes at 1024 j + 16 l (lanes past the end stay idle).
+
+  // LDS layout: the per-token arrays take 3 P doubles plus one of padding
+  // (the (d, r) pairs are 16-byte aligned).
+  const int fixed = 3 * P + 2;
+  int R = P;
+  while (R > P / 2 && R * P + (P - R) * (P - R) + fixed > kDafpsLds) --R;
+  const bool has_corner = R * P + (P - R) * (P - R) + fixed <= kDafpsLds;
+  if (!has_corner) R = min(P, (kDafpsLds - fixed) / P);
+  DafpsLds L;
+  L.R = R;
+  L.rows = lds;
+  L.has_corner = has_corner;
+  L.corner = lds + R * P;
+  const int nrm_off = (R * P + (has_corner ? (P - R) * (P - R) : 0) + 1) & ~1;
+  L.nrm = reinterpret_cast<double2*>(lds + nrm_off);
+  L.rho = lds + nrm_off + 2 * P;
+
+  // Each thread's rows of column i: [0, Hs) or [Hs, P); ns and ng bound the
+  // staged and global counts of either half (the same for every wave).
+  const int Hs = (P + 1) / 2;
+  const int lo = i < P ? (h ? Hs : 0) : 0, hi = i < P ? (h ? P : Hs) : 0;
+  const int ns = max(min(Hs, R), max(min(P, R) - Hs, 0));
+  const int ng = max(Hs - min(Hs, R), P - max(Hs, R));
+
+  // Global reads first (diagonal entry, the first eight global rows of the
+  // thread's share of column i), then the staged rows; all in flight
+  // together.
+  double di = 0.0, pre[8];
+#pragma unroll
+  for (int u = 0; u < 8; ++u) pre[u] = 0.0;
+  if (i < P) {
+    di = S[(int64_t)i * P + i];
+    const int g_lo = max(lo, R);
+    if (g_lo < hi) {
+#pragma unroll
+      for (int u = 0; u < 8; ++u) pre[u] = S[(int64_t)min(g_lo + u, P - 1) * P + i];
+    }
+  }
+  if (((uintptr_t)S & 15) == 0 && (R * P) % 2 == 0) {
+    // 16-byte direct-to-LDS loads: wave load j fills bytes [1024 j, 1024 j +
+    // 1024), lane l the 16 bytes at 1024 j + 16 l (lanes past the end stay
+    // idle; the byte count is a multiple of 16).
     typedef __attribute__((address_space(3))) void* lds_ptr_t;
     typedef __attribute__((address_space(1))) void* glb_ptr_t;
     const int bytes = R * P * 8;
-    const int lane = i & 63, wave = i >> 6;
-    for (int j = wave; j * 1024 < bytes; j += kMaxPerFrame / 64) {
+    const int lane = tid & 63, wave = tid >> 6;
+    for (int j = wave; j * 1024 < bytes; j += kDafpsThreads / 64) {
       const int off = j * 1024 + lane * 16;
       if (off < bytes)
         __builtin_amdgcn_global_load_lds((glb_ptr_t)(reinterpret_cast<const char*>(S) + off),
-                                         (lds_ptr_t)(reinterpret_cast<char*>(Sl) + j * 1024), 16, 0, 0);
+                                         (lds_ptr_t)(reinterpret_cast<char*>(lds) + j * 1024), 16, 0, 0);
     }
     asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
   } else {
-    // Odd P * P: S is only 8-byte aligned; eight loads in flight per thread.
-    for (int e0 = i; e0 < R * P; e0 += 8 * kMaxPerFrame) {
+    // S only 8-byte aligned (odd P * P before it) or an odd element count:
+    // eight loads in flight per thread.
+    for (int e0 = tid; e0 < R * P; e0 += 8 * kDafpsThreads) {
       double v[8];
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int e = e0 + u * kMaxPerFrame;
+        const int e = e0 + u * kDafpsThreads;
         v[u] = e < R * P ? S[e] : 0.0;
       }
 #pragma unroll
       for (int u = 0; u < 8; ++u) {
-        const int e = e0 + u * kMaxPerFrame;
-        if (e < R * P) Sl[e] = v[u];
+        const int e = e0 + u * kDafpsThreads;
+        if (e < R * P) lds[e] = v[u];
       }
     }
   }
+  const double ri = di > 0.0 ? 1.0 / sqrt(di) : 0.0;
+  if (i < P && h == 0) L.nrm[i] = make_double2(di, ri);
   __syncthreads();
-  for (int e = i; e < R * P; e += kMaxPerFrame) Sl[e] = cos_from(Sl[e], dg[e / P], dg[e % P]);
+
+  // Density of every token; the list length is the exact dafps_k up to 8.
+  // Waves whose tokens all lie past P skip it (the test is the same for the
+  // whole wave, so every lane of a working wave takes part).
+  if (32 * (tid >> 6) < P) {
+    const int dk = prm.dafps_k;
+    const double cv = prm.cover;
+    double rho;
+    switch (dk) {
+      case 1: rho = dafps_density<1>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv); break;
+      case 2: rho = dafps_density<2>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv); break;
+      case 3: rho = dafps_density<3>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv); break;
+      case 4: rho = dafps_density<4>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv); break;
+      case 5: rho = dafps_density<5>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv); break;
+      case 6: rho = dafps_density<6>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv); break;
+      case 7: rho = dafps_density<7>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv); break;
+      case 8: rho = dafps_density<8>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv); break;
+      default:
+        rho = dk <= 16 ? dafps_density<16>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv)
+                       : dafps_density<32>(L, S, P, i, lo, hi, ns, ng, pre, di, ri, dk, cv);
+    }
+    if (i < P && h == 0) L.rho[i] = rho;
+  }
   __syncthreads();
-  // Density of every token (thread per token).
-  if (i < P)
-    rho_sh[i] = prm.dafps_k <= 8    ? dafps_density<8>(S, Sl, dg, R, P, i, prm.dafps_k, prm.cover)
-                : prm.dafps_k <= 16 ? dafps_density<16>(S, Sl, dg, R, P, i, prm.dafps_k, prm.cover)
-                                    : dafps_density<32>(S, Sl, dg, R, P, i, prm.dafps_k, prm.cover);
-  __syncthreads();
-  if (i >= 64) return;
-  // Wave 0: token t = lane + 64 u, u < 4.
-  constexpr int kU = kMaxPerFrame / 64;
-  const int lane = i;
-  double wgt[kU], smax[kU], rho[kU];
-  bool taken[kU];
-#pragma unroll
-  for (int u = 0; u < kU; ++u) {
-    const int t = lane + 64 * u;
-    taken[u] = t >= P;
-    rho[u] = taken[u] ? -INFINITY : rho_sh[t];
-    wgt[u] = taken[u] ? 0.0 : pow(rho[u], prm.power);
-    smax[u] = 0.0;
-  }
-  // Lexicographic (value desc, token asc) argmax: the wave's largest value
-  // first, then the lowest token holding it -- tokens 64u + lane ascend
-  // with u and then with the lane, so the first non-empty ballot in u order
-  // names it.
-  auto pick_of = [&](const double (&v)[kU]) {
-    double m = -INFINITY;
-#pragma unroll
-    for (int u = 0; u < kU; ++u)
-      if (!taken[u]) m = fmax(m, v[u]);
-    m = wave_max_f64(m);
-    int best = 0x7FFFFFFF;
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const uint64_t b = __ballot(!taken[u] && v[u] == m);
-      if (b && best == 0x7FFFFFFF) best = 64 * u + (int)__builtin_ctzll(b);
-    }
-    return best;
-  };
-  // First pick: the densest token; then the farthest from the picked set,
-  // weighted by density.
-  int pick = pick_of(rho);
-  for (int n = 0;; ++n) {
-    double sv[kU];
-    if (pick < R) {  // the same branch for the whole wave
-#pragma unroll
-      for (int u = 0; u < kU; ++u) sv[u] = lane + 64 * u < P ? Sl[pick * P + lane + 64 * u] : 0.0;
-    } else {
-#pragma unroll
-      for (int u = 0; u < kU; ++u) {
-        const int t = lane + 64 * u;
-        sv[u] = t < P ? cos_from(S[(int64_t)pick * P + t], dg[pick], dg[t]) : 0.0;
-      }
-    }
-#pragma unroll
-    for (int u = 0; u < kU; ++u) {
-      const int t = lane + 64 * u;
-      if (t == pick) taken[u] = true;
-      if (t < P) smax[u] = n == 0 ? sv[u] : fmax(smax[u], sv[u]);
-    }
-    if (n + 1 >= k) break;
-    double val[kU];
-#pragma unroll
-    for (int u = 0; u < kU; ++u) val[u] = (1.0 - smax[u]) * wgt[u];
-    pick = pick_of(val);
-  }
-  // Ascending output of the picked positions.
-  int64_t pos = fp.out_off;
-#pragma unroll
-  for (int u = 0; u < kU; ++u) {
-    const int t = lane + 64 * u;
-    const bool kp = t < P && taken[u];
-    const uint64_t bal = __ballot(kp);
-    if (kp) kept[pos + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(c.vis_off + (int64_t)fr.f * P + t);
-    pos += __popcll(bal);
-  }
+  if (tid >= 64) return;
+
+  // Wave 0 picks; lanes hold ceil(P / 64) tokens each.
+  const int nu = (P + 63) / 64;
+  int64_t out = fp.out_off;
+  const int64_t base = c.vis_off + (int64_t)fr.f * P;
+  if (nu == 1) dafps_pick<1>(L, S, P, k, prm.power, tid, kept, out, base);
+  else if (nu == 2) dafps_pick<2>(L, S, P, k, prm.power, tid, kept, out, base);
+  else if (nu == 3) dafps_pick<3>(L, S, P, k, prm.power, tid, kept, out, base);
+  else dafps_pick<4>(L, S, P, k, prm.power, tid, kept, out, base);
 }
 
 // ---------------------------------------------------------------------------
@@ -1534,7 +1740,7 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
                          xv, dp.gram);
     }
     if ((st = launch_status("k_gram")) != APACK_OK) return st;
-    hipLaunchKernelGGL(k_dafps, dim3(nf), dim3(kMaxPerFrame), 0, s, dp.clips, dp.frames, dp.plan, prm, dp.gram, kept);
+    hipLaunchKernelGGL(k_dafps, dim3(nf), dim3(kDafpsThreads), 0, s, dp.clips, dp.frames, dp.plan, prm, dp.gram, kept);
     if ((st = launch_status("k_dafps")) != APACK_OK) return st;
     hipLaunchKernelGGL(k_dedup_sim<T>, dim3(nf, (pl.max_per_frame + kBlk / 64 - 1) / (kBlk / 64)), dim3(kBlk), 0, s,
                        dp.clips, dp.frames, dp.plan, dim, xv, dp.sim);

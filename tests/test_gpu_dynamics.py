@@ -142,6 +142,8 @@ def test_ragged_batch_of_clips_with_edge_shapes():
         W.dynamics_small("shared", seed=23, frames=1, per_frame=5, audio=9),       # one frame
         W.dynamics_small("offset", seed=24, frames=20, per_frame=70, audio=250),   # P not a multiple of 64
         W.dynamics_small("shared", seed=25, frames=12, per_frame=256, audio=150),  # largest P
+        W.dynamics_small("offset", seed=27, frames=8, per_frame=160, audio=80),    # DA-FPS rows past LDS
+        W.dynamics_small("shared", seed=28, frames=7, per_frame=151, audio=70),    # odd P * P, rows past LDS
     ]
     case = _packed(parts, {"window": 3, "r_pre": 0.5})
     want = _oracle(case)

@@ -43,9 +43,6 @@ typedef float f32x16 __attribute__((ext_vector_type(16)));
 
 constexpr int kBlk = 256;
 
-__device__ __forceinline__ double widen(bf16_t x) { return (double)__uint_as_float((uint32_t)x << 16); }
-__device__ __forceinline__ double widen(float x) { return (double)x; }
-
 // 8 consecutive elements as doubles (16- or 32-byte aligned loads).
 __device__ __forceinline__ void load8(const bf16_t* p, double (&o)[8]) {
   const uint4 u = *reinterpret_cast<const uint4*>(p);
@@ -167,6 +164,42 @@ __device__ double block_max(double v, double* sh) {
 template <int NT = kBlk>
 __device__ double block_min(double v, double* sh) { return -block_max<NT>(-v, sh); }
 
+// Eight consecutive elements of a row as raw bits, widened to doubles when
+// used (so that many rows' loads can be in flight in few registers).
+template <class T>
+struct Raw8;
+template <>
+struct Raw8<bf16_t> {
+  uint4 u;
+  // Always loads (from the row's last 8 elements when k is past dim - 8), so
+  // the loads carry no branch; get() zeroes a step past the limit.
+  __device__ __forceinline__ void load(const bf16_t* row, int k, int dim) {
+    u = *reinterpret_cast<const uint4*>(row + min(k, dim - 8));
+  }
+  __device__ __forceinline__ void get(double (&o)[8], bool valid) const {
+    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      o[2 * i] = valid ? (double)__uint_as_float(w[i] << 16) : 0.0;
+      o[2 * i + 1] = valid ? (double)__uint_as_float(w[i] & 0xFFFF0000u) : 0.0;
+    }
+  }
+};
+template <>
+struct Raw8<float> {
+  float4 a, b;
+  __device__ __forceinline__ void load(const float* row, int k, int dim) {
+    const float4* p = reinterpret_cast<const float4*>(row + min(k, dim - 8));
+    a = p[0];
+    b = p[1];
+  }
+  __device__ __forceinline__ void get(double (&o)[8], bool valid) const {
+    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) o[e] = valid ? (double)v[e] : 0.0;
+  }
+};
+
 // ---------------------------------------------------------------------------
 // Coarse pass (Section 3.1): v_f, a_f and the query mean.
 // One block per (item, 512-element slice of the embedding, 8 per lane); the
@@ -175,8 +208,9 @@ __device__ double block_min(double v, double* sh) { return -block_max<NT>(-v, sh
 // read the same rows run together and each DRAM page is opened once.
 // The block's four waves take every fourth row of the frame's visual tokens,
 // of its audio bin (or of the clip's query span); their fp64 partial sums
-// meet in LDS and are added in wave order.  Four times the rows in flight of
-// one wave per slice keeps HBM busy on short clips.  The same pass leaves
+// meet in LDS and are added in wave order.  A wave loads eight of its rows
+// (four of the audio bin's) together as raw bits before widening any, so
+// that enough bytes are in flight for HBM.  The same pass leaves
 // each visual and audio row's sum of squares over the slice in
 // sqp[slice][row] (audio rows after the n_vis visual rows), so the token
 // norms need no second read of X_V and X_A.
@@ -222,41 +256,63 @@ __global__ __launch_bounds__(kBlk) void k_pool(const ClipDev* __restrict__ clips
     lo = ((int64_t)fr.f * c.n_audio) / c.n_frames;
     hi = (((int64_t)fr.f + 1) * c.n_audio + c.n_frames - 1) / c.n_frames;
     const int64_t row0 = c.vis_off + (int64_t)fr.f * c.per_frame;
-    const T* base = xv + row0 * dim + d0;
-    // The wave's rows rg, rg + 4, ... four at a time: the four loads are
-    // issued together (a row past the frame re-reads its last row and adds
-    // nothing), and the four sums of squares are reduced together.
+    // Lanes past dim load the row's last eight elements (Raw8 clamps) and
+    // widen them to zeros.
+    const T* vrow = xv + row0 * dim;
+    // The wave's rows rg, rg + 4, ... eight at a time: the eight loads are
+    // issued together as raw bits (a row past the frame re-reads its last
+    // row and adds nothing), then widened and added in row order; the sums
+    // of squares are reduced four rows at a time.
     const int P = c.per_frame;
-    for (int p0 = rg; p0 < P; p0 += 4 * kPoolWaves) {
-      double o4[4][8], s2[4];
+    for (int p0 = rg; p0 < P; p0 += 8 * kPoolWaves) {
+      Raw8<T> raw[8];
 #pragma unroll
-      for (int j = 0; j < 4; ++j) row8(base + (int64_t)min(p0 + j * kPoolWaves, P - 1) * dim, o4[j]);
+      for (int j = 0; j < 8; ++j) raw[j].load(vrow + (int64_t)min(p0 + j * kPoolWaves, P - 1) * dim, d0, dim);
+      double s2[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        s2[j] = 0.0;
+        if (p0 + j * kPoolWaves < P) {
+          double o8[8];
+          raw[j].get(o8, live);
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            av[e] += o8[e];
+            s2[j] = fma(o8[e], o8[e], s2[j]);
+          }
+        }
+      }
+#pragma unroll
+      for (int h = 0; h < 2; ++h) {
+        const double t = wave_sum4(*reinterpret_cast<const double(*)[4]>(&s2[4 * h]));
+        const int p = p0 + (4 * h + lane) * kPoolWaves;
+        if (lane < 4 && p < P) sq[row0 + p] = t;
+      }
+    }
+    // The audio bin's rows rg, rg + 4, ... four at a time, the same way.
+    // A row shared by two bins gets the same value from both.
+    const T* arow = xa + c.aud_off * dim;
+    for (int64_t r0 = lo + rg; r0 < hi; r0 += 4 * kPoolWaves) {
+      Raw8<T> raw[4];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) raw[j].load(arow + min(r0 + j * kPoolWaves, hi - 1) * dim, d0, dim);
+      double s2[4];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
         s2[j] = 0.0;
-        if (p0 + j * kPoolWaves < P) {
+        if (r0 + j * kPoolWaves < hi) {
+          double o8[8];
+          raw[j].get(o8, live);
 #pragma unroll
           for (int e = 0; e < 8; ++e) {
-            av[e] += o4[j][e];
-            s2[j] = fma(o4[j][e], o4[j][e], s2[j]);
+            aa[e] += o8[e];
+            s2[j] = fma(o8[e], o8[e], s2[j]);
           }
         }
       }
       const double t = wave_sum4(s2);
-      const int p = p0 + lane * kPoolWaves;
-      if (lane < 4 && p < P) sq[row0 + p] = t;
-    }
-    // A row shared by two bins gets the same value from both.
-    for (int64_t r = lo + rg; r < hi; r += kPoolWaves) {
-      row8(xa + (c.aud_off + r) * dim + d0, o);
-      double s2 = 0.0;
-#pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        aa[e] += o[e];
-        s2 = fma(o[e], o[e], s2);
-      }
-      s2 = wave_sum(s2);
-      if (lane == 0) sq[n_vis + c.aud_off + r] = s2;
+      const int64_t r = r0 + lane * kPoolWaves;
+      if (lane < 4 && r < hi) sq[n_vis + c.aud_off + r] = t;
     }
   } else {
     ci = (int)(item - total_frames);
@@ -918,40 +974,6 @@ constexpr int kGramAhead = 4;  // K steps in flight per wave
 
 // Eight consecutive input elements held as loaded, widened to fp64 on use.
 template <class T>
-struct Raw8;
-template <>
-struct Raw8<bf16_t> {
-  uint4 u;
-  // Always loads (from the row's last 8 elements when k is past dim - 8), so
-  // the loads carry no branch; get() zeroes a step past the limit.
-  __device__ __forceinline__ void load(const bf16_t* row, int k, int dim) {
-    u = *reinterpret_cast<const uint4*>(row + min(k, dim - 8));
-  }
-  __device__ __forceinline__ void get(double (&o)[8], bool valid) const {
-    const uint32_t w[4] = {u.x, u.y, u.z, u.w};
-#pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      o[2 * i] = valid ? (double)__uint_as_float(w[i] << 16) : 0.0;
-      o[2 * i + 1] = valid ? (double)__uint_as_float(w[i] & 0xFFFF0000u) : 0.0;
-    }
-  }
-};
-template <>
-struct Raw8<float> {
-  float4 a, b;
-  __device__ __forceinline__ void load(const float* row, int k, int dim) {
-    const float4* p = reinterpret_cast<const float4*>(row + min(k, dim - 8));
-    a = p[0];
-    b = p[1];
-  }
-  __device__ __forceinline__ void get(double (&o)[8], bool valid) const {
-    const float v[8] = {a.x, a.y, a.z, a.w, b.x, b.y, b.z, b.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) o[e] = valid ? (double)v[e] : 0.0;
-  }
-};
-
-template <class T>
 __global__ __launch_bounds__(kGramSplit * 64) void k_gram(const ClipDev* __restrict__ clips, int n_clips,
                                                           const int32_t* __restrict__ anchors,
                                                           const FramePlanDev* __restrict__ plan, int dim,
@@ -1188,19 +1210,6 @@ __global__ __launch_bounds__(kBlk) void k_spatial_reduce(const ClipDev* __restri
   for (int p = 0; p < c.per_frame; ++p) tr_v += nv[row0 + p];
   const double sa = sqrt(s_aa), sv = sqrt(s_vv);
   cka[f] = (sa <= kCkaDegenerate * tr_a || sv <= kCkaDegenerate * tr_v) ? 0.0 : s_av / (sa * sv);
-}
-
-// Lexicographic (value desc, index asc) argmax across a wave.
-__device__ __forceinline__ void wave_argmax(double& v, int& idx) {
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    const double ov = __shfl_xor(v, off);
-    const int oi = __shfl_xor(idx, off);
-    if (ov > v || (ov == v && oi < idx)) {
-      v = ov;
-      idx = oi;
-    }
-  }
 }
 
 // v_max_f64 / v_min_f64 as single instructions.  In IEEE mode the

@@ -189,6 +189,35 @@ def test_window_sizes(window):
     _compare(case, _run(case), want)
 
 
+@pytest.mark.parametrize("dafps_k", [1, 2, 3, 4, 6, 7, 8, 12, 32])
+def test_dafps_density_list_lengths(dafps_k):
+    """Every length of the DA-FPS density list (its mean over the dafps_k
+    largest cosines), on 40-token frames, so that 32 < P - 1."""
+    case = W.dynamics_small("offset", seed=81, frames=24, per_frame=40, audio=150)
+    case.params = {"window": 3, "r_pre": 0.5, "dafps_k": dafps_k}
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+def test_dafps_list_longer_than_the_frame():
+    """dafps_k = 32 on 16-token frames: the mean runs over the P - 1 others."""
+    case = W.dynamics_small("offset", seed=81, frames=24, per_frame=16, audio=150)
+    case.params = {"window": 3, "r_pre": 0.5, "dafps_k": 32}
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
+@pytest.mark.parametrize("cover,power", [(0.5, 1.0), (0.95, 0.0), (0.8, 2.0)])
+def test_dafps_cover_and_power(cover, power):
+    case = W.dynamics_small("shared", seed=84, frames=24, per_frame=24, audio=150)
+    case.params = {"window": 3, "r_pre": 0.5, "cover_thresh": cover, "dafps_power": power}
+    want = _oracle(case)
+    _certify(want)
+    _compare(case, _run(case), want)
+
+
 @pytest.mark.parametrize("r_pre", [1.0, 0.05, 0.6])
 def test_budget_extremes(r_pre):
     case = W.dynamics_small("offset", seed=31)

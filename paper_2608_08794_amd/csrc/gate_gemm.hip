@@ -47,6 +47,7 @@ constexpr int kWN = 4;                         // waves along the visual columns
 constexpr int kBI = kTile / (kWaves / kWN) / 32; // 32-row blocks per wave
 constexpr int kBJ = kTile / kWN / 32;            // 32-column blocks per wave
 constexpr int kLoadsPerWave = kOpB / 1024 / kWaves;  // 1 KiB loads per wave per operand
+static_assert(kBI * kBJ == 8 && kBI + kBJ == 6, "the K-slice schedule interleaves 6 fragment reads with 8 MFMAs");
 constexpr int kXcds = 8;
 
 // Chunk c of row r sits at chunk c ^ swz(r).  A 16-byte LDS read is served
@@ -142,14 +143,20 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
     for (int ks = 0; ks < kK / 16; ++ks) {
       const int h = ks & 1;
       if (ks + 1 < kK / 16) read(ks + 1, h ^ 1);
-      // Keep the reads of slice ks + 1 ahead of slice ks's MFMAs: the
-      // scheduler would otherwise sink each read to its first use.
-      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
       for (int i = 0; i < kBI; ++i)
 #pragma unroll
         for (int j = 0; j < kBJ; ++j)
           acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[h][i], fb[h][j], acc[i][j], 0, 0, 0);
+      // Slice ks + 1's six fragment reads go one after each of slice ks's
+      // first six MFMAs (the scheduler would otherwise sink each read to its
+      // first use); nothing crosses into the next slice.
+#pragma unroll
+      for (int g = 0; g < 6; ++g) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);   // one MFMA
+        __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);   // one LDS read
+      }
+      __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       __builtin_amdgcn_sched_barrier(0);
     }
   }

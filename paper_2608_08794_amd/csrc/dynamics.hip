@@ -1410,13 +1410,31 @@ __device__ __forceinline__ void dafps_pick(const DafpsLds& L, const double* __re
 #pragma unroll
     for (int u = 1; u < KU; ++u) kb = key[u] > kb ? key[u] : kb;
     const uint32_t mh = wave_max_u32((uint32_t)(kb >> 32));
-    const uint32_t ml = wave_max_u32((uint32_t)(kb >> 32) == mh ? (uint32_t)kb : 0u);
-    const uint64_t mk = ((uint64_t)__builtin_amdgcn_readfirstlane(mh) << 32) | (uint32_t)__builtin_amdgcn_readfirstlane(ml);
-    int best = 0x7FFFFFFF;
+    // Untaken tokens whose key has the maximal high word: when there is
+    // one (the usual case) it is the pick, and the low words need no
+    // reduction.
+    uint64_t hb[KU];
+    int cnt = 0;
 #pragma unroll
     for (int u = 0; u < KU; ++u) {
-      const uint64_t b = __ballot(!taken[u] && key[u] == mk);
-      if (b && best == 0x7FFFFFFF) best = 64 * u + (int)__builtin_ctzll(b);
+      hb[u] = __ballot(!taken[u] && (uint32_t)(key[u] >> 32) == mh);
+      cnt += __popcll(hb[u]);
+    }
+    int best = 0x7FFFFFFF;
+    if (cnt == 1) {
+#pragma unroll
+      for (int u = 0; u < KU; ++u)
+        if (hb[u]) best = 64 * u + (int)__builtin_ctzll(hb[u]);
+      return best;
+    }
+    if (cnt > 1) {
+      const uint32_t ml = wave_max_u32((uint32_t)(kb >> 32) == mh ? (uint32_t)kb : 0u);
+      const uint64_t mk = ((uint64_t)mh << 32) | ml;
+#pragma unroll
+      for (int u = 0; u < KU; ++u) {
+        const uint64_t b = __ballot(!taken[u] && key[u] == mk);
+        if (b && best == 0x7FFFFFFF) best = 64 * u + (int)__builtin_ctzll(b);
+      }
     }
     if (best == 0x7FFFFFFF) {
 #pragma unroll
@@ -1452,7 +1470,7 @@ __device__ __forceinline__ void dafps_pick(const DafpsLds& L, const double* __re
     }
     if (n + 1 >= k) break;
 #pragma unroll
-    for (int u = 0; u < KU; ++u) key[u] = taken[u] ? 0 : order_key((1.0 - smax[u]) * wgt[u]);
+    for (int u = 0; u < KU; ++u) key[u] = order_key((1.0 - smax[u]) * wgt[u]) & (taken[u] ? 0ull : ~0ull);
     pick = pick_of();
   }
   // Ascending output of the picked positions.

@@ -1390,16 +1390,19 @@ __device__ __forceinline__ void dafps_pick(const DafpsLds& L, const double* __re
   const int R = L.R;
   double wgt[KU], smax[KU], dt[KU], rt[KU];
   uint64_t key[KU];
-  bool taken[KU];
+  // Taken tokens as wave-wide lane masks (the same in every lane), one per
+  // u; tokens past P count as taken.
+  uint64_t tk[KU], pad[KU];
   int tc[KU];
 #pragma unroll
   for (int u = 0; u < KU; ++u) {
     const int t = lane + 64 * u;
-    taken[u] = t >= P;
+    pad[u] = tk[u] = __ballot(t >= P);
+    const bool tkn = t >= P;
     tc[u] = min(t, P - 1);
     const double rho = L.rho[tc[u]];
-    wgt[u] = taken[u] ? 0.0 : pow(rho, power);
-    key[u] = taken[u] ? 0 : order_key(rho);
+    wgt[u] = tkn ? 0.0 : pow(rho, power);
+    key[u] = tkn ? 0 : order_key(rho);
     smax[u] = -INFINITY;
     const double2 n = L.nrm[tc[u]];
     dt[u] = n.x;
@@ -1417,7 +1420,7 @@ __device__ __forceinline__ void dafps_pick(const DafpsLds& L, const double* __re
     int cnt = 0;
 #pragma unroll
     for (int u = 0; u < KU; ++u) {
-      hb[u] = __ballot(!taken[u] && (uint32_t)(key[u] >> 32) == mh);
+      hb[u] = __ballot((uint32_t)(key[u] >> 32) == mh) & ~tk[u];
       cnt += __popcll(hb[u]);
     }
     int best = 0x7FFFFFFF;
@@ -1432,14 +1435,14 @@ __device__ __forceinline__ void dafps_pick(const DafpsLds& L, const double* __re
       const uint64_t mk = ((uint64_t)mh << 32) | ml;
 #pragma unroll
       for (int u = 0; u < KU; ++u) {
-        const uint64_t b = __ballot(!taken[u] && key[u] == mk);
+        const uint64_t b = __ballot(key[u] == mk) & ~tk[u];
         if (b && best == 0x7FFFFFFF) best = 64 * u + (int)__builtin_ctzll(b);
       }
     }
     if (best == 0x7FFFFFFF) {
 #pragma unroll
       for (int u = 0; u < KU; ++u) {
-        const uint64_t b = __ballot(!taken[u]);
+        const uint64_t b = ~tk[u];
         if (b && best == 0x7FFFFFFF) best = 64 * u + (int)__builtin_ctzll(b);
       }
     }
@@ -1465,21 +1468,20 @@ __device__ __forceinline__ void dafps_pick(const DafpsLds& L, const double* __re
     }
 #pragma unroll
     for (int u = 0; u < KU; ++u) {
-      if (lane + 64 * u == pick) taken[u] = true;
+      if ((pick >> 6) == u) tk[u] |= 1ull << (pick & 63);
       smax[u] = max_f64(smax[u], sv[u]);
     }
     if (n + 1 >= k) break;
 #pragma unroll
-    for (int u = 0; u < KU; ++u) key[u] = order_key((1.0 - smax[u]) * wgt[u]) & (taken[u] ? 0ull : ~0ull);
+    for (int u = 0; u < KU; ++u)
+      key[u] = order_key((1.0 - smax[u]) * wgt[u]) & (__builtin_amdgcn_inverse_ballot_w64(tk[u]) ? 0ull : ~0ull);
     pick = pick_of();
   }
   // Ascending output of the picked positions.
 #pragma unroll
   for (int u = 0; u < KU; ++u) {
-    const int t = lane + 64 * u;
-    const bool kp = t < P && taken[u];
-    const uint64_t bal = __ballot(kp);
-    if (kp) kept[out + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(base + t);
+    const uint64_t bal = tk[u] & ~pad[u];
+    if ((bal >> lane) & 1ull) kept[out + __popcll(bal & ((1ull << lane) - 1ull))] = (int32_t)(base + lane + 64 * u);
     out += __popcll(bal);
   }
 }

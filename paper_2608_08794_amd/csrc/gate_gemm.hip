@@ -142,6 +142,10 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
 #pragma unroll
     for (int ks = 0; ks < kK / 16; ++ks) {
       const int h = ks & 1;
+      // Slices run at raised wave priority, so a wave in its MFMAs issues
+      // ahead of the other wave on the SIMD while that one waits at the
+      // stage barrier or issues loads.
+      __builtin_amdgcn_s_setprio(1);
       if (ks + 1 < kK / 16) read(ks + 1, h ^ 1);
 #pragma unroll
       for (int i = 0; i < kBI; ++i)
@@ -158,6 +162,7 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
       }
       __builtin_amdgcn_sched_group_barrier(0x008, 2, 0);
       __builtin_amdgcn_sched_barrier(0);
+      __builtin_amdgcn_s_setprio(0);
     }
   }
 

@@ -8,7 +8,8 @@
 //   k_cka        Eq. 1 per frame from the centred w x w window Grams, the
 //                clip mean and the gate of Eq. 2
 //   k_norms      squared norms of every visual and audio token of the clips
-//                (fp64), from k_pool's per-slice sums
+//                (fp64), from k_pool's per-slice sums, and 1/|x| of the
+//                visual tokens
 //   k_gate_gemm  only where the gate fired: X_A . X_V^T on bf16 MFMA, scaled
 //                by 1/|a_j|, max over audio tokens in-lane, merged across
 //                tiles by atomicMax on order-preserving uint keys
@@ -507,7 +508,8 @@ __global__ __launch_bounds__(kBlk) void k_cka(ClipDev* __restrict__ clips, int w
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kBlk) void k_norms(int64_t n_vis, int64_t n_aud, int slices,
                                                 const double* __restrict__ sqp, double* __restrict__ nv,
-                                                double* __restrict__ na, uint32_t* __restrict__ maxkey) {
+                                                double* __restrict__ rv, double* __restrict__ na,
+                                                uint32_t* __restrict__ maxkey) {
   const int64_t stride = n_vis + n_aud;
   const int64_t row = (int64_t)blockIdx.x * kBlk + threadIdx.x;
   if (row >= stride) return;
@@ -515,6 +517,7 @@ __global__ __launch_bounds__(kBlk) void k_norms(int64_t n_vis, int64_t n_aud, in
   for (int k = 0; k < slices; ++k) s += sqp[(int64_t)k * stride + row];
   if (row < n_vis) {
     nv[row] = s;
+    rv[row] = s > 0.0 ? 1.0 / sqrt(s) : 0.0;   // 1/|x| for the direct distance, 0 for a zero token
     maxkey[row] = 0u;
   } else {
     na[row - n_vis] = s;
@@ -776,7 +779,7 @@ constexpr int kPlanLdsBytes = kPlanLds * (9 * 8 + 4 * 8 + 3 * 4);
 __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, DynParamsDev prm,
                                                    const double* __restrict__ cka, const double* __restrict__ band_v,
                                                    const double* __restrict__ vq, const double* __restrict__ qq,
-                                                   const double* __restrict__ nv, const uint32_t* __restrict__ maxkey,
+                                                   const double* __restrict__ rv, const uint32_t* __restrict__ maxkey,
                                                    FramePlanDev* __restrict__ plan, int32_t* __restrict__ anchors,
                                                    double* scratch, int64_t scratch_n,
                                                    float* __restrict__ frame_score,
@@ -806,8 +809,8 @@ __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, 
       double sm = 0.0;
 #pragma unroll 6
       for (int p = sub; p < P; p += 8) {
-        const double nn = nv[row0 + p];
-        sm += nn > 0.0 ? (double)key_value(maxkey[row0 + p]) * (1.0 / sqrt(nn)) : 0.0;
+        const double r = rv[row0 + p];
+        sm += r > 0.0 ? (double)key_value(maxkey[row0 + p]) * r : 0.0;
       }
       sm += __shfl_xor(sm, 1);
       sm += __shfl_xor(sm, 2);
@@ -1727,7 +1730,7 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
   }
   if (n_vis + n_aud > 0) {
     hipLaunchKernelGGL(k_norms, dim3((unsigned)((n_vis + n_aud + kBlk - 1) / kBlk)), dim3(kBlk), 0, s, n_vis, n_aud,
-                       (int)dchunks, dp.sqp, dp.nv, dp.na, dp.maxkey);
+                       (int)dchunks, dp.sqp, dp.nv, dp.rv, dp.na, dp.maxkey);
     if ((st = launch_status("k_norms")) != APACK_OK) return st;
   }
   if (prm.alignment == APACK_ALIGN_SPATIAL_CKA && nf > 0) {
@@ -1757,7 +1760,7 @@ apack_status launch_t(const DynPlan& pl, const DynPtrs& dp, const DynParamsDev& 
       if ((st = launch_status("k_gate_gemm")) != APACK_OK) return st;
     }
   }
-  hipLaunchKernelGGL(k_plan, dim3(nc), dim3(kPlanBlk), 0, s, dp.clips, prm, dp.cka, dp.band_v, dp.vq, dp.qq, dp.nv,
+  hipLaunchKernelGGL(k_plan, dim3(nc), dim3(kPlanBlk), 0, s, dp.clips, prm, dp.cka, dp.band_v, dp.vq, dp.qq, dp.rv,
                      dp.maxkey, dp.plan, dp.anchors, dp.scratch, (int64_t)(pl.total_frames + nc), frame_score,
                      frame_budget,
                      segment_id);

@@ -129,6 +129,8 @@ apack_status build_dyn_plan(int32_t n_seq, const apack_av_seq* seqs, int32_t dim
   c.take<double>(frames);
   pl.off_nv = c.used;
   c.take<double>(vis_end);
+  pl.off_rv = c.used;
+  c.take<double>(vis_end);
   pl.off_na = c.used;
   c.take<double>(aud_end);
   pl.off_maxkey = c.used;
@@ -251,6 +253,7 @@ apack_status apack_score_dynamics(int32_t n_seq, const apack_av_seq* seqs, apack
   dp.qq = reinterpret_cast<double*>(ws + pl.off_qq);
   dp.cka = reinterpret_cast<double*>(ws + pl.off_cka);
   dp.nv = reinterpret_cast<double*>(ws + pl.off_nv);
+  dp.rv = reinterpret_cast<double*>(ws + pl.off_rv);
   dp.na = reinterpret_cast<double*>(ws + pl.off_na);
   dp.maxkey = reinterpret_cast<uint32_t*>(ws + pl.off_maxkey);
   dp.plan = reinterpret_cast<FramePlanDev*>(ws + pl.off_plan);

@@ -65,7 +65,7 @@ struct DynPlan {
   // Workspace layout (byte offsets).
   size_t off_clips = 0, off_frames = 0, off_gemm = 0, blob_bytes = 0;
   size_t off_v = 0, off_a = 0, off_q = 0, off_band_v = 0, off_band_a = 0, off_vq = 0, off_qq = 0;
-  size_t off_cka = 0, off_nv = 0, off_na = 0, off_maxkey = 0, off_plan = 0, off_gram = 0, off_scratch = 0;
+  size_t off_cka = 0, off_nv = 0, off_rv = 0, off_na = 0, off_maxkey = 0, off_plan = 0, off_gram = 0, off_scratch = 0;
   size_t off_spatial = 0, off_sim = 0, off_anchors = 0, off_sqp = 0;
   int64_t gram_items = 0;            // (frame, Gram tile) pairs over all clips: the anchor Gram's items at most
   size_t ws_bytes = 0;
@@ -101,7 +101,7 @@ struct DynPtrs {
   ClipDev* clips;
   FrameDev* frames;
   GemmTileDev* gemm;
-  double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *na, *gram, *scratch, *spatial, *sim;
+  double *v, *a, *q, *band_v, *band_a, *vq, *qq, *cka, *nv, *rv, *na, *gram, *scratch, *spatial, *sim;
   double* sqp;       // per-slice row sums of squares [slice][visual rows, then audio rows]
   uint32_t* maxkey;
   FramePlanDev* plan;

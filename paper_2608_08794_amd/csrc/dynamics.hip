@@ -807,10 +807,27 @@ __global__ __launch_bounds__(kPlanBlk) void k_plan(ClipDev* __restrict__ clips, 
     for (int f = tid >> 3; f < F; f += kPlanBlk / 8) {  // the eight threads of a frame share the trip count
       const int64_t row0 = c.vis_off + (int64_t)f * P;
       double sm = 0.0;
-#pragma unroll 6
-      for (int p = sub; p < P; p += 8) {
-        const double r = rv[row0 + p];
-        sm += r > 0.0 ? (double)key_value(maxkey[row0 + p]) * r : 0.0;
+      // Six rows per thread per batch, all twelve loads issued before the
+      // first is used: a zero-norm row has r == 0 and adds 0, a slot no
+      // audio column reached (key 0) reads as 0, and a row past the frame
+      // re-reads the frame's last row and is then zeroed, so nothing
+      // branches on a loaded value. The sum keeps the order of p.
+      constexpr int kU = 6;
+      for (int p0 = sub; p0 < P; p0 += 8 * kU) {
+        double r[kU];
+        uint32_t mk[kU];
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          const int p = min(p0 + 8 * u, P - 1);
+          r[u] = rv[row0 + p];
+          mk[u] = maxkey[row0 + p];
+        }
+#pragma unroll
+        for (int u = 0; u < kU; ++u) {
+          const float kv = mk[u] != 0u ? key_value(mk[u]) : 0.0f;
+          const double t = (double)kv * r[u];
+          sm += p0 + 8 * u < P ? t : 0.0;
+        }
       }
       sm += __shfl_xor(sm, 1);
       sm += __shfl_xor(sm, 2);

@@ -66,14 +66,13 @@ __global__ __launch_bounds__(kT) void k_select_pass(SeqDev* __restrict__ seqs, c
   uint8_t mt[kPer];
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int i = threadIdx.x * kPer + u;
-    bits[u] = 0;
-    mt[u] = 0xFF;
-    if (i < n) {
-      mt[u] = tg[r0 + i];
-      bits[u] = clamp_bits(scores[sq->tok_off + r0 + i]);
-    }
+    const int i = min((int)threadIdx.x * kPer + u, n - 1);
+    mt[u] = tg[r0 + i];
+    bits[u] = clamp_bits(scores[sq->tok_off + r0 + i]);
   }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u)
+    if ((int)threadIdx.x * kPer + u >= n) mt[u] = 0xFF;
   hist_pass(sq, hist + (int64_t)ft.seq * 2 * kBins1, bits, mt, pass, lh);
 }
 
@@ -84,28 +83,45 @@ __global__ __launch_bounds__(kT) void k_keep_count(const SeqDev* __restrict__ se
                                                    float* __restrict__ scores, uint32_t* __restrict__ cnt) {
   __shared__ uint32_t sh[kT / 64];
   const FTileDev ft = ftiles[blockIdx.x];
-  const SeqDev& sq = seqs[ft.seq];
+  const SeqDev sq = seqs[ft.seq];
   int64_t r0;
   int n;
   tile_rows(ft, sq, r0, n);
   const uint8_t* tg = tags + sq.tag_off;
+  const uint32_t thr[2] = {sq.thr[0], sq.thr[1]};
+  const bool no_cand = sq.n_cand == 0;
   uint32_t sure = 0, ea = 0, ev = 0;
+  // Tags and scores are loaded together (rows past the tile re-read its last
+  // row and are then skipped), so no score load waits for its tag.
+  uint8_t mt[kPer];
+  float sc[kPer];
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    const int i = min((int)threadIdx.x * kPer + u, n - 1);
+    mt[u] = tg[r0 + i];
+    sc[u] = scores[sq.tok_off + r0 + i];
+  }
+  // Counted without branches, so that the loads above are not moved into
+  // per-row branches (and waited for one row at a time).
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
     const int i = threadIdx.x * kPer + u;
-    if (i >= n) continue;
-    const uint8_t m = tg[r0 + i];
-    if (m == 0) {
-      // Scores of sequences with candidates are written by the score
-      // kernels; a sequence without any has no score workgroups.
-      if (sq.n_cand == 0) scores[sq.tok_off + r0 + i] = 0.f;
-      ++sure;
-      continue;
+    const uint8_t m = i < n ? mt[u] : 0xFF;
+    const uint32_t b = clamp_bits(sc[u]);
+    const uint32_t t = m == 2 ? thr[1] : thr[0];
+    const bool cand = m == 1 || m == 2;
+    sure += (m == 0 || (cand && b > t)) ? 1u : 0u;
+    ea += (m == 1 && b == t) ? 1u : 0u;
+    ev += (m == 2 && b == t) ? 1u : 0u;
+  }
+  // Scores of sequences with candidates are written by the score kernels; a
+  // sequence without any has no score workgroups.
+  if (no_cand) {
+#pragma unroll
+    for (int u = 0; u < kPer; ++u) {
+      const int i = threadIdx.x * kPer + u;
+      if (i < n && mt[u] == 0) scores[sq.tok_off + r0 + i] = 0.f;
     }
-    const uint32_t b = clamp_bits(scores[sq.tok_off + r0 + i]);
-    const uint32_t t = sq.thr[m - 1];
-    if (b > t) ++sure;
-    else if (b == t) (m == 1 ? ea : ev) += 1;
   }
   uint32_t tot;
   block_scan<kT>(sure, sh, tot);
@@ -126,12 +142,13 @@ __global__ __launch_bounds__(kT) void k_keep_write(const SeqDev* __restrict__ se
   __shared__ uint32_t sh[kT / 64];
   __shared__ uint64_t base_sh[3];
   const FTileDev ft = ftiles[blockIdx.x];
-  const SeqDev& sq = seqs[ft.seq];
+  const SeqDev sq = seqs[ft.seq];
   int64_t r0;
   int n;
   tile_rows(ft, sq, r0, n);
   const uint8_t* tg = tags + sq.tag_off;
-  const uint32_t need[2] = {(uint32_t)sq.need[0], (uint32_t)sq.need[1]};
+  const uint32_t need0 = (uint32_t)sq.need[0], need1 = (uint32_t)sq.need[1];
+  const uint32_t thr0 = sq.thr[0], thr1 = sq.thr[1];
   // Rows kept and ties seen by the tiles before this one.  The ties kept
   // before a tile add up to min(need, ties before it), so plain sums do.
   {
@@ -147,7 +164,7 @@ __global__ __launch_bounds__(kT) void k_keep_write(const SeqDev* __restrict__ se
     block_scan<kT>(a, sh, ta);
     block_scan<kT>(v, sh, tv);
     if (threadIdx.x == 0) {
-      base_sh[0] = (uint64_t)ts + min(ta, need[0]) + min(tv, need[1]);
+      base_sh[0] = (uint64_t)ts + min(ta, need0) + min(tv, need1);
       base_sh[1] = ta;
       base_sh[2] = tv;
     }
@@ -158,15 +175,16 @@ __global__ __launch_bounds__(kT) void k_keep_write(const SeqDev* __restrict__ se
   uint32_t ea = 0, ev = 0;
 #pragma unroll
   for (int u = 0; u < kPer; ++u) {
-    const int i = threadIdx.x * kPer + u;
-    mt[u] = 0xFF;
-    bits[u] = 0;
-    if (i < n) {
-      mt[u] = tg[r0 + i];
-      if (mt[u] != 0) bits[u] = clamp_bits(scores[sq.tok_off + r0 + i]);
-    }
-    if (mt[u] == 1 && bits[u] == sq.thr[0]) ++ea;
-    if (mt[u] == 2 && bits[u] == sq.thr[1]) ++ev;
+    const int i = min((int)threadIdx.x * kPer + u, n - 1);
+    mt[u] = tg[r0 + i];
+    bits[u] = __float_as_uint(scores[sq.tok_off + r0 + i]);
+  }
+#pragma unroll
+  for (int u = 0; u < kPer; ++u) {
+    if ((int)threadIdx.x * kPer + u >= n) mt[u] = 0xFF;
+    bits[u] = mt[u] != 0 ? clamp_bits(__uint_as_float(bits[u])) : 0u;
+    if (mt[u] == 1 && bits[u] == thr0) ++ea;
+    if (mt[u] == 2 && bits[u] == thr1) ++ev;
   }
   uint32_t tot;
   const uint32_t packed = ea | (ev << 16);
@@ -180,9 +198,9 @@ __global__ __launch_bounds__(kT) void k_keep_write(const SeqDev* __restrict__ se
     bool kp = false;
     if (m == 0) kp = true;
     else if (m == 1 || m == 2) {
-      const uint32_t t = sq.thr[m - 1];
+      const uint32_t t = m == 1 ? thr0 : thr1;
       if (bits[u] > t) kp = true;
-      else if (bits[u] == t) kp = (m == 1 ? rank_a++ : rank_v++) < need[m - 1];
+      else if (bits[u] == t) kp = (m == 1 ? rank_a++ : rank_v++) < (m == 1 ? need0 : need1);
     }
     keep[u] = kp;
     nk += kp;
@@ -234,9 +252,9 @@ __global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__
                                                       float* __restrict__ scores, int32_t* __restrict__ kept) {
   __shared__ uint32_t lh[2 * kBins1];
   __shared__ uint32_t sh[kST / 64];
-  __shared__ uint32_t s_prefix[2], s_kk[2], s_thr[2], s_need[2];
+  __shared__ uint32_t s_prefix[2], s_kk[2], s_thr[2], s_need[2], s_part[2];
   __shared__ uint32_t s_wave[2][kSWaves];
-  const SeqDev& sq = seqs[blockIdx.x];
+  const SeqDev sq = seqs[blockIdx.x];
   const int n = (int)sq.n_tokens;
   if (n == 0) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
@@ -244,25 +262,35 @@ __global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__
   const uint8_t* tg = tags + sq.tag_off;
   uint32_t bits[kSPer];
   uint8_t mt[kSPer];
+  // Every tag and score load is issued before the first is used: a row
+  // past the sequence re-reads its last row, and a score is kept only for a
+  // candidate row, so no load waits behind another (a score load behind a
+  // test of its tag had waited for the tag first, one row at a time).
 #pragma unroll
   for (int u = 0; u < kSPer; ++u) {
-    const int i = row0 + 64 * u;
-    mt[u] = i < n ? tg[i] : 0xFF;
+    const int i = min(row0 + 64 * u, n - 1);
+    mt[u] = tg[i];
+    bits[u] = __float_as_uint(scores[sq.tok_off + i]);
   }
 #pragma unroll
   for (int u = 0; u < kSPer; ++u) {
     const int i = row0 + 64 * u;
-    bits[u] = 0;
-    if (mt[u] == 1 || mt[u] == 2) bits[u] = clamp_bits(scores[sq.tok_off + i]);
-    // Scores of sequences with candidates are written by the score kernels;
-    // a sequence without any has no score workgroups.
-    if (mt[u] == 0 && sq.n_cand == 0) scores[sq.tok_off + i] = 0.f;
+    if (i >= n) mt[u] = 0xFF;
+    bits[u] = (mt[u] == 1 || mt[u] == 2) ? clamp_bits(__uint_as_float(bits[u])) : 0u;
+  }
+  // Scores of sequences with candidates are written by the score kernels; a
+  // sequence without any has no score workgroups.
+  if (sq.n_cand == 0) {
+#pragma unroll
+    for (int u = 0; u < kSPer; ++u)
+      if (mt[u] == 0) scores[sq.tok_off + row0 + 64 * u] = 0.f;
   }
   if (tid < 2) {
-    s_prefix[tid] = sq.prefix[tid];
-    s_kk[tid] = sq.kk[tid];
-    s_thr[tid] = sq.thr[tid];
-    s_need[tid] = (uint32_t)sq.need[tid];
+    s_prefix[tid] = tid ? sq.prefix[1] : sq.prefix[0];
+    s_kk[tid] = tid ? sq.kk[1] : sq.kk[0];
+    s_thr[tid] = tid ? sq.thr[1] : sq.thr[0];
+    s_need[tid] = (uint32_t)(tid ? sq.need[1] : sq.need[0]);
+    s_part[tid] = 0;   // a modality that does not select keeps all or none of its rows
   }
   __syncthreads();
   const bool act0 = sq.select[0] != 0, act1 = sq.select[1] != 0;
@@ -310,6 +338,7 @@ __global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__
             if (pass == 2) {
               s_thr[m] = prefix;
               s_need[m] = kk[m] - before;
+              s_part[m] = kk[m] - before != c[m][j] ? 1u : 0u;
             }
           }
           before += c[m][j];
@@ -318,35 +347,47 @@ __global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__
     }
     __syncthreads();
   }
-  // Ranks of the rows equal to each threshold, in row order: wave totals,
-  // then within the wave by u and by lane.
+  // Kept: every non-candidate row, every candidate above its modality's
+  // threshold and the first `need` rows equal to it in row order.  When
+  // every row equal to the threshold is kept (the usual case), no rank is
+  // formed.  The tests are bitwise (no short-circuit), so they compile to
+  // straight-line compares rather than nested branches.
   const uint32_t thr0 = s_thr[0], thr1 = s_thr[1], need0 = s_need[0], need1 = s_need[1];
-  uint32_t ta = 0, tv = 0;
-#pragma unroll
-  for (int u = 0; u < kSPer; ++u) {
-    ta += __popcll(__ballot(mt[u] == 1 && bits[u] == thr0));
-    tv += __popcll(__ballot(mt[u] == 2 && bits[u] == thr1));
-  }
-  if (lane == 0) {
-    s_wave[0][wave] = ta;
-    s_wave[1][wave] = tv;
-  }
-  uint32_t ra = wave_base(s_wave[0], wave), rv = wave_base(s_wave[1], wave);
   uint32_t keepbits = 0, nk = 0;
+  if (!(s_part[0] | s_part[1])) {
 #pragma unroll
-  for (int u = 0; u < kSPer; ++u) {
-    const uint64_t ma = __ballot(mt[u] == 1 && bits[u] == thr0);
-    const uint64_t mv = __ballot(mt[u] == 2 && bits[u] == thr1);
-    bool kp = false;
-    if (mt[u] == 0) kp = true;
-    else if (mt[u] == 1) kp = bits[u] > thr0 || (bits[u] == thr0 && ra + below(ma) < need0);
-    else if (mt[u] == 2) kp = bits[u] > thr1 || (bits[u] == thr1 && rv + below(mv) < need1);
-    ra += __popcll(ma);
-    rv += __popcll(mv);
-    keepbits |= (uint32_t)kp << u;
-    nk += __popcll(__ballot(kp));
+    for (int u = 0; u < kSPer; ++u) {
+      const bool kp = (mt[u] == 0) | ((mt[u] == 1) & (bits[u] >= thr0)) | ((mt[u] == 2) & (bits[u] >= thr1));
+      keepbits |= (uint32_t)kp << u;
+      nk += __popcll(__ballot(kp));
+    }
+  } else {
+    // Ranks of the rows equal to each threshold: wave totals, then within
+    // the wave by u and by lane.
+    uint32_t ta = 0, tv = 0;
+#pragma unroll
+    for (int u = 0; u < kSPer; ++u) {
+      ta += __popcll(__ballot((mt[u] == 1) & (bits[u] == thr0)));
+      tv += __popcll(__ballot((mt[u] == 2) & (bits[u] == thr1)));
+    }
+    if (lane == 0) {
+      s_wave[0][wave] = ta;
+      s_wave[1][wave] = tv;
+    }
+    uint32_t ra = wave_base(s_wave[0], wave), rv = wave_base(s_wave[1], wave);
+#pragma unroll
+    for (int u = 0; u < kSPer; ++u) {
+      const bool ea = (mt[u] == 1) & (bits[u] == thr0), ev = (mt[u] == 2) & (bits[u] == thr1);
+      const uint64_t ma = __ballot(ea), mv = __ballot(ev);
+      const bool kp = (mt[u] == 0) | ((mt[u] == 1) & (bits[u] > thr0)) | ((mt[u] == 2) & (bits[u] > thr1)) |
+                      (ea & (ra + below(ma) < need0)) | (ev & (rv + below(mv) < need1));
+      ra += __popcll(ma);
+      rv += __popcll(mv);
+      keepbits |= (uint32_t)kp << u;
+      nk += __popcll(__ballot(kp));
+    }
+    __syncthreads();   // every wave has read s_wave
   }
-  __syncthreads();   // every wave has read s_wave
   if (lane == 0) s_wave[0][wave] = nk;
   uint32_t pos = wave_base(s_wave[0], wave);
   int32_t* out = kept + sq.out_off;

@@ -127,7 +127,6 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
     else
       asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
     __syncthreads();
-    if (it + kStages - 1 < n_k) issue(it + kStages - 1);
     const char* la = lds + buf * kStageB;
     const char* lb = la + kOpB;
     // Fragments of K slice ks + 1 are read while slice ks's MFMAs run.
@@ -138,7 +137,13 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
 #pragma unroll
       for (int j = 0; j < kBJ; ++j) fb[h][j] = lds_frag(lb, wn * kBJ * 32 + j * 32 + (lane & 31), ks, lane);
     };
+    // The first slice's reads go out before the next stage's loads are
+    // issued, so their latency runs under the load issue rather than ahead
+    // of the first MFMA.
     read(0, 0);
+    __builtin_amdgcn_sched_barrier(0);
+    if (it + kStages - 1 < n_k) issue(it + kStages - 1);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < kK / 16; ++ks) {
       const int h = ks & 1;

@@ -140,7 +140,29 @@ struct KTileLoad {
   }
 };
 
-__device__ __forceinline__ void wait_tile_loads() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+// Waits until the tile consumed next has landed while `ahead` later tiles
+// (at most two) may still be in flight.  Each tile is kPer direct-to-LDS
+// loads per wave, and loads complete in issue order, so at most
+// ahead * kPer outstanding operations means the older tile is done (a
+// younger store only makes the wait longer).
+template <class T, int D, int NW>
+__device__ __forceinline__ void wait_tile_loads(int ahead) {
+  constexpr int kPer = KTileLoad<T, D, NW>::kPer;
+  if (ahead >= 2)
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kPer) : "memory");
+  else if (ahead == 1)
+    asm volatile("s_waitcnt vmcnt(%0)" ::"n"(kPer) : "memory");
+  else
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+}
+
+// LDS stages of the key tiles: four (three tiles in flight) where a few
+// query rows leave each tile little work, so that the loads of one
+// workgroup keep HBM busy; two otherwise.
+template <class T, int D, int NW>
+constexpr int key_stages() {
+  return (NW == 4 && TileGeom<T, D>::kTileBytes <= 32768) ? 4 : 2;
+}
 
 template <class T, int D>
 __device__ __forceinline__ typename Mma<T>::frag lds_frag(const char* lds, int key, int ks, int lane) {
@@ -266,7 +288,7 @@ __device__ __forceinline__ void merge(float& m, float& s, float mo, float so) {
 // Pass 1: per query row, online max and sum of exp2 over one key chunk.
 // C = K Q^T: lane (l % 32) owns a query column and 16 key rows per block.
 // ---------------------------------------------------------------------------
-template <class T, int D, int NW>
+template <class T, int D, int NW, int S>
 __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restrict__ seqs,
                                                          const TileDev* __restrict__ tiles,
                                                          const uint8_t* __restrict__ tags,
@@ -279,7 +301,8 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   using G = TileGeom<T, D>;
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
-  __shared__ __attribute__((aligned(16))) char lds[2][G::kTileBytes];
+  static_assert(S == 2 || KTileLoad<T, D, NW>::kLoads % NW == 0, "every wave issues the same loads per tile");
+  __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
   // Accumulator start (0 or -inf) of every key of the chunk, built once
   // before the loop so that no tile waits on a load of its tags.
   __shared__ __attribute__((aligned(16))) float lmask[kMaxChunk];
@@ -340,14 +363,17 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
       }
     }
   }
-  if (n_tiles > 0) KTileLoad<T, D, NW>::issue(lds[0], kbase, key_begin, key_end, wave, lane);
+  for (int p = 0; p < S - 1 && p < n_tiles; ++p)
+    KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
   for (int it = 0; it < n_tiles; ++it) {
-    const int buf = it & 1;
+    const int buf = it % S;
     const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
     const float* lm = lmask + it * kKeyTile;
-    wait_tile_loads();
+    wait_tile_loads<T, D, NW>(min(S - 2, n_tiles - 1 - it));
     __syncthreads();
-    if (it + 1 < n_tiles) KTileLoad<T, D, NW>::issue(lds[buf ^ 1], kbase, t0 + kKeyTile, key_end, wave, lane);
+    if (it + S - 1 < n_tiles)
+      KTileLoad<T, D, NW>::issue(lds[(it + S - 1) % S], kbase, t0 + (int64_t)(S - 1) * kKeyTile, key_end, wave,
+                                 lane);
     if (active) {
       // K fragments and mask of block kb+1 are read from LDS while block kb
       // computes.
@@ -449,7 +475,7 @@ __device__ __forceinline__ void col_flush(float (&red)[3][NW][NKB * 32], int slo
   }
 }
 
-template <class T, int D, int NW>
+template <class T, int D, int NW, int S>
 __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs,
                                                        const TileDev* __restrict__ tiles,
                                                        const uint8_t* __restrict__ tags,
@@ -462,7 +488,8 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   using G = TileGeom<T, D>;
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
-  __shared__ __attribute__((aligned(16))) char lds[2][G::kTileBytes];
+  static_assert(S == 2 || KTileLoad<T, D, NW>::kLoads % NW == 0, "every wave issues the same loads per tile");
+  __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
   __shared__ float red[3][NW][kKeyTile];
 
   const TileDev tl = tiles[blockIdx.x];
@@ -521,14 +548,17 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
     cs = 0.f;
   };
 
-  if (n_tiles > 0) KTileLoad<T, D, NW>::issue(lds[0], kbase, key_begin, key_end, wave, lane);
+  for (int p = 0; p < S - 1 && p < n_tiles; ++p)
+    KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
   for (int it = 0; it < n_tiles; ++it) {
-    const int buf = it & 1;
+    const int buf = it % S;
     const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
-    wait_tile_loads();
+    wait_tile_loads<T, D, NW>(min(S - 2, n_tiles - 1 - it));
     __syncthreads();
     if (it >= 2) col_flush<NKB, NW>(red, (it - 2) % 3, n_active, t0 - 2 * kKeyTile, key_end, out, tid);
-    if (it + 1 < n_tiles) KTileLoad<T, D, NW>::issue(lds[buf ^ 1], kbase, t0 + kKeyTile, key_end, wave, lane);
+    if (it + S - 1 < n_tiles)
+      KTileLoad<T, D, NW>::issue(lds[(it + S - 1) % S], kbase, t0 + (int64_t)(S - 1) * kKeyTile, key_end, wave,
+                                 lane);
     if (active) {
       const int slot = it % 3, prev_slot = (it + 2) % 3;
       // K fragments of block kb+1 are read from LDS while block kb computes.
@@ -640,17 +670,17 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
 // ---------------------------------------------------------------------------
 // Host launch sequence.
 // ---------------------------------------------------------------------------
-template <class T, int D, int NW>
+template <class T, int D, int NW, int S = key_stages<T, D, NW>()>
 apack_status launch_scores_t(const PrunePlan& pl, const DevPtrs& dp, const void* q, int64_t q_hs,
                              const void* k, int64_t k_hs, int n_rep, int hkv, float* scores, hipStream_t stream) {
   const float scale_log2 = (float)(1.4426950408889634 / std::sqrt((double)D));
   const int nt = (int)pl.tiles.size();
   if (nt > 0) {
-    hipLaunchKernelGGL((k_rowstats<T, D, NW>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles,
+    hipLaunchKernelGGL((k_rowstats<T, D, NW, S>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles,
                        dp.tags, (const T*)q, q_hs, (const T*)k, k_hs, n_rep, scale_log2, dp.stats, dp.bias,
                        dp.ctr, dp.hist, pl.any_select ? select_hist_words((int64_t)pl.seqs.size()) : (int64_t)0);
     APACK_CHECK(launch_status("k_rowstats") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
-    hipLaunchKernelGGL((k_colsum<T, D, NW>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles, dp.tags,
+    hipLaunchKernelGGL((k_colsum<T, D, NW, S>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles, dp.tags,
                        (const T*)q, q_hs, (const T*)k, k_hs, n_rep, hkv, scale_log2, dp.bias, dp.colpart, scores,
                        dp.hist, dp.ctr);
     APACK_CHECK(launch_status("k_colsum") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
@@ -661,9 +691,12 @@ apack_status launch_scores_t(const PrunePlan& pl, const DevPtrs& dp, const void*
 template <class T, int D>
 apack_status launch_scores_d(const PrunePlan& pl, const DevPtrs& dp, const void* q, int64_t q_hs,
                              const void* k, int64_t k_hs, int n_rep, int hkv, float* scores, hipStream_t stream) {
+  // Up to four waves of query rows run as four-wave workgroups: with one or
+  // two row waves the others only share the tile loads and the chunk's
+  // closing sums, and the tiles stream through four LDS stages.
   switch (pl.waves) {
-    case 1: return launch_scores_t<T, D, 1>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
-    case 2: return launch_scores_t<T, D, 2>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
+    case 1:
+    case 2:
     case 4: return launch_scores_t<T, D, 4>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
     case 7: return launch_scores_t<T, D, 7>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);
     default: return launch_scores_t<T, D, 8>(pl, dp, q, q_hs, k, k_hs, n_rep, hkv, scores, stream);

@@ -147,7 +147,9 @@ struct KTileLoad {
 // younger store only makes the wait longer).
 template <class T, int D, int NW>
 __device__ __forceinline__ void wait_tile_loads(int ahead) {
-  constexpr int kPer = KTileLoad<T, D, NW>::kPer;
+  // The fewest loads any wave issues per tile (a wave that issues more
+  // waits a little longer than it has to).
+  constexpr int kPer = KTileLoad<T, D, NW>::kLoads / NW;
   if (ahead >= 2)
     asm volatile("s_waitcnt vmcnt(%0)" ::"n"(2 * kPer) : "memory");
   else if (ahead == 1)
@@ -159,6 +161,8 @@ __device__ __forceinline__ void wait_tile_loads(int ahead) {
 // LDS stages of the key tiles: four (three tiles in flight) where a few
 // query rows leave each tile little work, so that the loads of one
 // workgroup keep HBM busy; two otherwise.
+// (Three stages for the seven- and eight-wave workgroups, whose tiles carry
+// enough arithmetic to hide a load, measured slightly slower.)
 template <class T, int D, int NW>
 constexpr int key_stages() {
   return (NW == 4 && TileGeom<T, D>::kTileBytes <= 32768) ? 4 : 2;
@@ -301,8 +305,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   using G = TileGeom<T, D>;
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
-  static_assert(S == 2 || KTileLoad<T, D, NW>::kLoads % NW == 0, "every wave issues the same loads per tile");
-  __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
+    __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
   // Accumulator start (0 or -inf) of every key of the chunk, built once
   // before the loop so that no tile waits on a load of its tags.
   __shared__ __attribute__((aligned(16))) float lmask[kMaxChunk];
@@ -488,8 +491,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   using G = TileGeom<T, D>;
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
-  static_assert(S == 2 || KTileLoad<T, D, NW>::kLoads % NW == 0, "every wave issues the same loads per tile");
-  __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
+    __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
   __shared__ float red[3][NW][kKeyTile];
 
   const TileDev tl = tiles[blockIdx.x];

@@ -245,21 +245,24 @@ def apack_prune_layer(q, k, seqs, scores=None, kept_rows=None, workspace=None, s
     arr, _keep = _seq_array(seqs)
     n = len(seqs)
     n_kept = (ctypes.c_int64 * max(1, n))()
-    wsb = ctypes.c_size_t(0)
-    _check(library().apack_prune_layer_query(n, arr, hq, hkv, d, n_kept, ctypes.byref(wsb)))
-    total = sum(int(n_kept[i]) for i in range(n))
-    with _alloc_on(stream):
-        if scores is None:
-            scores = torch.zeros(k_rows, dtype=torch.float32, device=k.device)
-        if kept_rows is None:
-            kept_rows = torch.empty(max(total, 1), dtype=torch.int32, device=k.device)
-        if workspace is None:
-            workspace = _workspace(wsb.value, k.device)
+    if scores is None or kept_rows is None or workspace is None:
+        # Output and workspace sizes (the call itself checks what it is given).
+        wsb = ctypes.c_size_t(0)
+        _check(library().apack_prune_layer_query(n, arr, hq, hkv, d, n_kept, ctypes.byref(wsb)))
+        total = sum(int(n_kept[i]) for i in range(n))
+        with _alloc_on(stream):
+            if scores is None:
+                scores = torch.zeros(k_rows, dtype=torch.float32, device=k.device)
+            if kept_rows is None:
+                kept_rows = torch.empty(max(total, 1), dtype=torch.int32, device=k.device)
+            if workspace is None:
+                workspace = _workspace(wsb.value, k.device)
     _check(library().apack_prune_layer(
         n, arr, _dtype_code(q), hq, hkv, d, _ptr(q), qhs, q_rows, _ptr(k), khs, k_rows,
         _ptr(scores), _ptr(kept_rows), kept_rows.numel(), n_kept,
         _ptr(workspace), workspace.numel(), _stream(stream)))
-    return scores, kept_rows[:total], [int(n_kept[i]) for i in range(n)]
+    counts = [int(n_kept[i]) for i in range(n)]
+    return scores, kept_rows[:sum(counts)], counts
 
 
 def apack_compact_kv(src_rows, n_in, k_in=(), v_in=(), k_out=(), v_out=(), hidden_in=None,

@@ -165,26 +165,36 @@ def main():
     torch.cuda.synchronize()
     log(f"warmup done ({args.warmup} steps)")
 
-    # Every timed step records its own events on the launch stream; they are
-    # read only after the timed region.
-    step_events = [events() for _ in range(args.steps)]
+    # The timed steps carry no markers between their launches (on some runs
+    # each timing event between two kernels cost ~9 us); the phases are timed
+    # in a second pass of the same K steps, each step recording its own events
+    # on the launch stream, read only after that pass.
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
     torch.cuda.synchronize()
     start.record()
-    for ev in step_events:
-        run_step(ev)
+    for _ in range(args.steps):
+        run_step(None)
     stop.record()
     torch.cuda.synchronize()
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
+    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+    step_events = [events() for _ in range(args.steps)]
+    start_p = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start_p.record()
+    for ev in step_events:
+        run_step(ev)
+    torch.cuda.synchronize()
     # The scores/select phase of prune i runs from the previous gather's end
     # (the step's start for the first prune) to the event after it.
-    prev = [start] + [ev[-1][1] for ev in step_events[:-1]]
+    prev = [start_p] + [ev[-1][1] for ev in step_events[:-1]]
     prune_ms = [sum((p if i == 0 else ev[i - 1][1]).elapsed_time(ev[i][0]) for p, ev in zip(prev, step_events))
                 for i in range(len(steps))]
     gather_ms = [sum(ev[i][0].elapsed_time(ev[i][1]) for ev in step_events) for i in range(len(steps))]
-    log(f"timed {args.steps} steps: {ms_per_step:.3f} ms/step")
+    phase_ms = start_p.elapsed_time(step_events[-1][-1][1]) / args.steps
+    log(f"phase pass: {phase_ms:.3f} ms/step with its markers")
     cold_ms = cold_steps(torch, run_step, args.steps)
     log(f"cold: {cold_ms:.3f} ms/step")
 
@@ -240,7 +250,9 @@ def main():
             "how": "the same K steps, each after a 512 MiB device write (twice the Infinity Cache) that lies "
                    "outside its events; value and ms_per_step above are the back-to-back (warm) steps",
         },
-        "per_prune_step_ms": {"score_select": [round(x, 4) for x in p_ms], "compact": [round(x, 4) for x in g_ms]},
+        "per_prune_step_ms": {"score_select": [round(x, 4) for x in p_ms], "compact": [round(x, 4) for x in g_ms],
+                              "how": "a second pass of the same steps with an event after each select and each "
+                                     "gather; that pass took %.4f ms per step" % phase_ms},
         "prefill_flops": prefill_flops(A, n_layers, n0, case.prune_layers, [st["n_out"] for st in steps]),
         "algorithmic_bytes_per_step": step_bytes,
     }

@@ -32,11 +32,15 @@ apack_status launch_status(const char* what) {
 // ---------------------------------------------------------------------------
 // Pinned staging pool.  Blocks are reused once the event recorded after their
 // last upload has completed; a busy pool grows instead of waiting, up to
-// kMaxStaging blocks per device.  Past that, a call waits for the oldest
-// block's upload and takes it (growing it if it is too small), so a caller
-// that queues many calls ahead holds at most that many pinned blocks.
+// kMaxStaging blocks per device.  Past that, a call waits for the upload of
+// the oldest block that is large enough and takes it, so a caller that queues
+// many calls ahead holds at most that many pinned blocks.  Only when no block
+// is large enough is the oldest one freed and allocated again: freeing pinned
+// memory waits for the device, which would drain the caller's queue.  Blocks
+// are at least kMinStaging bytes, so calls of different sizes share them.
 // ---------------------------------------------------------------------------
 constexpr int kMaxStaging = 32;
+constexpr size_t kMinStaging = size_t(1) << 18;
 struct Staging {
   void* host = nullptr;
   void* mapped = nullptr;  // device address of `host`
@@ -79,15 +83,17 @@ static apack_status staging_alloc(Staging* s, size_t cap) {
 apack_status staging_acquire(size_t bytes, Staging** blk, void** host) {
   int dev = 0;
   APACK_HIP(hipGetDevice(&dev));
-  const size_t want = align_up(bytes < 65536 ? 65536 : bytes, 65536);
+  const size_t want = align_up(bytes < kMinStaging ? kMinStaging : bytes, 65536);
   std::lock_guard<std::mutex> lk(g_pool_mu);
   int on_dev = 0;
-  Staging* oldest = nullptr;
+  Staging* oldest = nullptr;      // oldest block on this device
+  Staging* oldest_fit = nullptr;  // oldest block large enough for this call
   for (Staging* s : g_pool) {
     if (s->device != dev) continue;
     ++on_dev;
     if (!oldest || s->stamp < oldest->stamp) oldest = s;
     if (s->cap < bytes) continue;
+    if (!oldest_fit || s->stamp < oldest_fit->stamp) oldest_fit = s;
     if (s->busy) {
       hipError_t q = hipEventQuery(s->done);
       if (q == hipErrorNotReady) continue;
@@ -101,9 +107,9 @@ apack_status staging_acquire(size_t bytes, Staging** blk, void** host) {
     return APACK_OK;
   }
   if (on_dev >= kMaxStaging) {
-    // At the cap: wait until the oldest block's upload has been read, then
-    // reuse it, reallocated if it is too small.
-    Staging* s = oldest;
+    // At the cap: wait until the upload of the oldest block that fits has
+    // been read and reuse it; reallocate the oldest block only if none fits.
+    Staging* s = oldest_fit ? oldest_fit : oldest;
     if (s->busy) APACK_HIP(hipEventSynchronize(s->done));
     s->busy = false;
     if (s->cap < bytes) {

@@ -283,6 +283,18 @@ def test_ragged_batch_interleaved_spans(dtype, d):
     _parity(case)
 
 
+@pytest.mark.parametrize("dtype,hq,hkv,d,q_len,n", [("bf16", 28, 4, 128, 32, 30011), ("bf16", 8, 2, 128, 40, 40013),
+                                                     ("f32", 8, 2, 64, 48, 40013)])
+def test_four_wave_workgroups_over_four_stages(dtype, hq, hkv, d, q_len, n):
+    # Up to four waves of query rows per group (here 224, 160 and 192 rows)
+    # run four-wave workgroups whose key tiles stream through four LDS stages
+    # (bf16, and f32 at head dim 64); at these lengths each workgroup's key
+    # chunk is three or four tiles, the last one ragged.
+    specs = [([(0, 8000, A_), (8000, n - 8200, V_)], n, q_len, (0.5, 0.3))]
+    case = _synthetic(dtype, hq, hkv, d, specs, seed=18)
+    _parity(case)
+
+
 def test_exact_ties_keep_lowest_rows():
     specs = [([(0, 100, A_), (100, 250, V_)], 400, 7, (0.33, 0.5))]
     case = _synthetic("bf16", 8, 2, 128, specs, seed=12, zero_keys=True)

@@ -305,7 +305,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   using G = TileGeom<T, D>;
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
-    __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
+  __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
   // Accumulator start (0 or -inf) of every key of the chunk, built once
   // before the loop so that no tile waits on a load of its tags.
   __shared__ __attribute__((aligned(16))) float lmask[kMaxChunk];
@@ -318,6 +318,16 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   const int row0 = tl.rg * sq.rows_per_rg + wave * kRowsPerWave;
   const bool active = row0 < rg_end;
 
+  const int64_t key_begin = (int64_t)tl.chunk * sq.chunk;
+  int64_t key_end = key_begin + sq.chunk;
+  if (key_end > sq.n_tokens) key_end = sq.n_tokens;
+  const int n_tiles = (int)((key_end - key_begin + kKeyTile - 1) / kKeyTile);
+  const T* kbase = k + (int64_t)tl.g * k_hs + sq.tok_off * D;
+  // The first key tiles are requested before anything else, so their loads
+  // run under the clearing, the query loads and the mask build.
+  for (int p = 0; p < S - 1 && p < n_tiles; ++p)
+    KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
+
   // This workgroup's share of clearing the radix histograms used by the
   // score finalisation at the end of the pass-2 kernel.
   {
@@ -329,12 +339,6 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   QFrags<T, D> qfr;
   auto& qf = qfr.v;
   if (active) load_q<T, D>(qfr, q, q_hs, sq, tl.g, n_rep, row0, lane);
-
-  const int64_t key_begin = (int64_t)tl.chunk * sq.chunk;
-  int64_t key_end = key_begin + sq.chunk;
-  if (key_end > sq.n_tokens) key_end = sq.n_tokens;
-  const int n_tiles = (int)((key_end - key_begin + kKeyTile - 1) / kKeyTile);
-  const T* kbase = k + (int64_t)tl.g * k_hs + sq.tok_off * D;
   const uint8_t* tg = tags + sq.tag_off;
 
   float m_run[kRB], s_run[kRB];
@@ -347,8 +351,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   }
 
   // Tags are read in batches of 8 per thread, all in flight together (the
-  // index is clamped to a valid row; rows past the chunk get -inf), before
-  // the first K tile is requested.
+  // index is clamped to a valid row; rows past the chunk get -inf).
   {
     constexpr int kB = 8;
     const int n_mask = n_tiles * kKeyTile;
@@ -366,8 +369,6 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
       }
     }
   }
-  for (int p = 0; p < S - 1 && p < n_tiles; ++p)
-    KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
   for (int it = 0; it < n_tiles; ++it) {
     const int buf = it % S;
     const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
@@ -433,25 +434,46 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   // padding rows get +inf so they contribute exp2(-inf) = 0 in pass 2.
   if (!arrive_last<NW * kWave>(ctr + sq.ctr_off + tl.g * sq.n_rg + tl.rg, (uint32_t)sq.n_chunks)) return;
   const int r_lo = tl.rg * sq.rows_per_rg;
-  for (int rho = r_lo + tid; rho < r_lo + sq.rows_per_rg; rho += NW * kWave) {
-    float m = -FLT_MAX, s = 0.f;
-    if (rho < rows_g) {
-      // Partials are [g][chunk][row]: a wave's loads of one chunk are
-      // contiguous.  Loads in batches (all in flight together), merged in
-      // chunk order.
-      const float2* p = stats + sq.stats_off + (int64_t)tl.g * sq.n_chunks * sq.rows_pad + rho;
-      constexpr int CB = 16;
-      for (int c0 = 0; c0 < sq.n_chunks; c0 += CB) {
-        float2 v[CB];
+  // Partials are [g][chunk][row]: a wave's loads of one chunk are contiguous.
+  // Chunks [c_lo, c_hi) of row rho, loaded in batches (all in flight
+  // together) and merged in chunk order.
+  auto merge_run = [&](int rho, int c_lo, int c_hi, float& m, float& s) {
+    const float2* p = stats + sq.stats_off + (int64_t)tl.g * sq.n_chunks * sq.rows_pad + rho;
+    constexpr int CB = 16;
+    for (int c0 = c_lo; c0 < c_hi; c0 += CB) {
+      float2 v[CB];
 #pragma unroll
-        for (int i = 0; i < CB; ++i)
-          v[i] = c0 + i < sq.n_chunks ? ld_agent(p + (int64_t)(c0 + i) * sq.rows_pad) : make_float2(0.f, 0.f);
+      for (int i = 0; i < CB; ++i)
+        v[i] = c0 + i < c_hi ? ld_agent(p + (int64_t)(c0 + i) * sq.rows_pad) : make_float2(0.f, 0.f);
 #pragma unroll
-        for (int i = 0; i < CB; ++i)
-          if (c0 + i < sq.n_chunks) merge(m, s, v[i].x, v[i].y);
-      }
+      for (int i = 0; i < CB; ++i)
+        if (c0 + i < c_hi) merge(m, s, v[i].x, v[i].y);
     }
-    bias[sq.bias_off + (int64_t)tl.g * sq.rows_pad + rho] = (s > 0.f) ? m + log2f(s) : INFINITY;
+  };
+  const int R = sq.rows_per_rg, nthr = NW * kWave;
+  const int ng = R <= nthr / 4 ? 4 : R <= nthr / 2 ? 2 : 1;
+  if (ng == 1) {
+    for (int rho = r_lo + tid; rho < r_lo + R; rho += nthr) {
+      float m = -FLT_MAX, s = 0.f;
+      if (rho < rows_g) merge_run(rho, 0, sq.n_chunks, m, s);
+      bias[sq.bias_off + (int64_t)tl.g * sq.rows_pad + rho] = (s > 0.f) ? m + log2f(s) : INFINITY;
+    }
+    return;
+  }
+  // Fewer rows than threads: ng threads share a row, each merging a
+  // contiguous run of chunks (one load batch instead of ng in a row), and
+  // the runs are combined in order in LDS (the key tiles are done).
+  float2* part = reinterpret_cast<float2*>(&lds[0][0]);
+  const int grp = tid / R, r = tid - grp * R, rho = r_lo + r;
+  const int cpg = (sq.n_chunks + ng - 1) / ng;
+  float m = -FLT_MAX, s = 0.f;
+  if (grp < ng && rho < rows_g) merge_run(rho, grp * cpg, min(sq.n_chunks, (grp + 1) * cpg), m, s);
+  if (grp < ng) part[grp * R + r] = make_float2(m, s);
+  __syncthreads();
+  if (tid < R) {
+    float mm = part[r].x, ss = part[r].y;
+    for (int q = 1; q < ng; ++q) merge(mm, ss, part[q * R + r].x, part[q * R + r].y);
+    bias[sq.bias_off + (int64_t)tl.g * sq.rows_pad + rho] = (ss > 0.f) ? mm + log2f(ss) : INFINITY;
   }
 }
 
@@ -491,7 +513,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   using G = TileGeom<T, D>;
   using M = Mma<T>;
   constexpr int NKB = kKeyTile / 32;
-    __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
+  __shared__ __attribute__((aligned(16))) char lds[S][G::kTileBytes];
   __shared__ float red[3][NW][kKeyTile];
 
   const TileDev tl = tiles[blockIdx.x];
@@ -502,6 +524,15 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   const int row0 = tl.rg * sq.rows_per_rg + wave * kRowsPerWave;
   const bool active = row0 < rg_end;
   const int n_active = (rg_end - tl.rg * sq.rows_per_rg + kRowsPerWave - 1) / kRowsPerWave;
+
+  const int64_t key_begin = (int64_t)tl.chunk * sq.chunk;
+  int64_t key_end = key_begin + sq.chunk;
+  if (key_end > sq.n_tokens) key_end = sq.n_tokens;
+  const int n_tiles = (int)((key_end - key_begin + kKeyTile - 1) / kKeyTile);
+  const T* kbase = k + (int64_t)tl.g * k_hs + sq.tok_off * D;
+  // The first key tiles are requested before the query and bias loads.
+  for (int p = 0; p < S - 1 && p < n_tiles; ++p)
+    KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
 
   QFrags<T, D> qfr;
   auto& qf = qfr.v;
@@ -521,11 +552,6 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
       }
   }
 
-  const int64_t key_begin = (int64_t)tl.chunk * sq.chunk;
-  int64_t key_end = key_begin + sq.chunk;
-  if (key_end > sq.n_tokens) key_end = sq.n_tokens;
-  const int n_tiles = (int)((key_end - key_begin + kKeyTile - 1) / kKeyTile);
-  const T* kbase = k + (int64_t)tl.g * k_hs + sq.tok_off * D;
   float* out = colpart + sq.colpart_off + (int64_t)(tl.g * sq.n_rg + tl.rg) * sq.n_tokens;
 
   // The pipeline unit is one (key block, row block) pair: its MFMAs run
@@ -550,8 +576,6 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
     cs = 0.f;
   };
 
-  for (int p = 0; p < S - 1 && p < n_tiles; ++p)
-    KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
   for (int it = 0; it < n_tiles; ++it) {
     const int buf = it % S;
     const int64_t t0 = key_begin + (int64_t)it * kKeyTile;

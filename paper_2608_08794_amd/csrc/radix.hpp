@@ -70,26 +70,33 @@ __device__ void pick_bins(SeqDev* sq, uint32_t* hist, int pass) {
   __shared__ uint32_t sh[NT / 64];
   const int tid = threadIdx.x;
   const int nb = pass == 2 ? 512 : kRadixBins;
-  for (int m = 0; m < 2; ++m) {
-    if (!sq->select[m]) continue;
-    uint32_t* h = hist + m * kRadixBins;
-    uint32_t c[B], sum = 0;
+  const bool act[2] = {sq->select[0] != 0, sq->select[1] != 0};
+  // Both modalities' bins, ranks and prefixes are read first (one round
+  // trip for the bins); the scans' barriers keep every read ahead of the
+  // one thread that overwrites a rank or prefix below.
+  uint32_t c[2][B];
+#pragma unroll
+  for (int m = 0; m < 2; ++m)
 #pragma unroll
     for (int j = 0; j < B; ++j) {
       const int b = nb - 1 - (tid * B + j);
-      c[j] = b >= 0 ? ld_agent(h + b) : 0u;
-      sum += c[j];
+      c[m][j] = act[m] && b >= 0 ? ld_agent(hist + m * kRadixBins + b) : 0u;
     }
-    // Read the rank and prefix before the scan: its barrier keeps every
-    // thread's read ahead of the one thread that overwrites them below.
-    const uint32_t kk = sq->kk[m], prefix0 = sq->prefix[m];
+  const uint32_t kk2[2] = {sq->kk[0], sq->kk[1]}, prefix2[2] = {sq->prefix[0], sq->prefix[1]};
+  for (int m = 0; m < 2; ++m) {
+    if (!act[m]) continue;
+    uint32_t* h = hist + m * kRadixBins;
+    const uint32_t kk = kk2[m], prefix0 = prefix2[m];
+    uint32_t sum = 0;
+#pragma unroll
+    for (int j = 0; j < B; ++j) sum += c[m][j];
     uint32_t total;
     const uint32_t incl = block_scan<NT>(sum, sh, total);
     uint32_t before = incl - sum;
     if (before < kk && incl >= kk) {
 #pragma unroll
       for (int j = 0; j < B; ++j) {
-        if (before < kk && before + c[j] >= kk) {
+        if (before < kk && before + c[m][j] >= kk) {
           const uint32_t b = (uint32_t)(nb - 1 - (tid * B + j));
           const uint32_t prefix = pass == 0 ? b : (prefix0 << (pass == 1 ? 11 : 9)) | b;
           sq->prefix[m] = prefix;
@@ -97,10 +104,10 @@ __device__ void pick_bins(SeqDev* sq, uint32_t* hist, int pass) {
           if (pass == 2) {
             sq->thr[m] = prefix;
             sq->need[m] = (int32_t)(kk - before);
-            sq->all_eq[m] = (kk - before == c[j]) ? 1 : 0;
+            sq->all_eq[m] = (kk - before == c[m][j]) ? 1 : 0;
           }
         }
-        before += c[j];
+        before += c[m][j];
       }
     }
     __syncthreads();

@@ -20,6 +20,7 @@
 // list are formed by the kernels of select.hip.
 #include <cfloat>
 #include <cmath>
+#include <type_traits>
 #include <vector>
 
 #include "common.hpp"
@@ -281,6 +282,21 @@ __device__ __forceinline__ void row_update(const f32x16& x, float scale, float& 
   m_run = m_new;
 }
 
+// Σ exp2 of one query row's 16 logits against a fixed reference m0 (no
+// per-block maximum or rescale).  m0 is the row's running maximum when the
+// wave switches to this form, plus 64: a term overflows only for a logit
+// more than 191 above that maximum (the caller then redoes the chunk with
+// row_update) and underflows only below 2^-62 of it, far under the fp32
+// resolution of the sum.
+__device__ __forceinline__ void row_update_ref(const f32x16& x, float scale, float m0, float& s_run) {
+  float p[4];
+#pragma unroll
+  for (int e = 0; e < 4; ++e) p[e] = fast_exp2(fmaf(x[e], scale, -m0));
+#pragma unroll
+  for (int e = 4; e < 16; ++e) p[e & 3] += fast_exp2(fmaf(x[e], scale, -m0));
+  s_run += (p[0] + p[1]) + (p[2] + p[3]);
+}
+
 // Fixed-order combination of two (max, sum exp2) partials of one row.
 __device__ __forceinline__ void merge(float& m, float& s, float mo, float so) {
   const float mm = fmaxf(m, mo);
@@ -341,15 +357,6 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
   if (active) load_q<T, D>(qfr, q, q_hs, sq, tl.g, n_rep, row0, lane);
   const uint8_t* tg = tags + sq.tag_off;
 
-  float m_run[kRB], s_run[kRB];
-  f32x16 pend[kRB];  // logits of the block whose VALU work is still due
-#pragma unroll
-  for (int rb = 0; rb < kRB; ++rb) {
-    m_run[rb] = -FLT_MAX;
-    s_run[rb] = 0.f;
-    pend[rb] = neg_inf16();
-  }
-
   // Tags are read in batches of 8 per thread, all in flight together (the
   // index is clamped to a valid row; rows past the chunk get -inf).
   {
@@ -369,32 +376,45 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
       }
     }
   }
-  for (int it = 0; it < n_tiles; ++it) {
-    const int buf = it % S;
-    const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
-    const float* lm = lmask + it * kKeyTile;
-    wait_tile_loads<T, D, NW>(min(S - 2, n_tiles - 1 - it));
-    __syncthreads();
-    if (it + S - 1 < n_tiles)
-      KTileLoad<T, D, NW>::issue(lds[(it + S - 1) % S], kbase, t0 + (int64_t)(S - 1) * kKeyTile, key_end, wave,
-                                 lane);
-    if (active) {
+  // One pass over the chunk's key tiles: with exact = false each lane sums
+  // against its fixed reference (row_update_ref), with exact = true it keeps
+  // the online maximum (row_update).  The first is taken; the second redoes
+  // the chunk only if some lane's sum overflowed.
+  float m_run[kRB], s_run[kRB];
+  auto run_chunk = [&](auto exact_tag) {
+    constexpr bool kExactOnly = decltype(exact_tag)::value;
+    f32x16 pend[kRB];  // logits of the block whose VALU work is still due
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) {
+      m_run[rb] = -FLT_MAX;
+      s_run[rb] = 0.f;
+      pend[rb] = neg_inf16();
+    }
+    // A wave sums with the online maximum until every lane has seen a
+    // candidate key (checked at each tile start), then against a fixed
+    // reference per lane: m_run + 64, with the sum rescaled once.  (The fp32
+    // inputs keep the online form: their larger fragments leave no registers
+    // for a second loop body.)
+    constexpr bool kUseRef = sizeof(T) == 2;
+    bool ref = false;
+    auto tile_body = [&](auto exact_body_tag, const char* tile, const float* lm) {
+      constexpr bool kExact = decltype(exact_body_tag)::value;
       // K fragments and mask of block kb+1 are read from LDS while block kb
       // computes.
       constexpr int NB = kPrefetchFrags<T> ? 2 : 1;
       KFrags<T, D> kf[NB];
       f32x16 init[NB];
-      kf[0].load(lds[buf], 0, lane);
+      kf[0].load(tile, 0, lane);
       init[0] = mask_init(lm, 0, lane);
 #pragma unroll
       for (int kb = 0; kb < NKB; ++kb) {
         const int c = kb % NB;
         if (NB == 1 && kb > 0) {
-          kf[0].load(lds[buf], kb, lane);
+          kf[0].load(tile, kb, lane);
           init[0] = mask_init(lm, kb, lane);
         }
         if (NB == 2 && kb + 1 < NKB) {
-          kf[(kb + 1) % NB].load(lds[buf], kb + 1, lane);
+          kf[(kb + 1) % NB].load(tile, kb + 1, lane);
           init[(kb + 1) % NB] = mask_init(lm, kb + 1, lane);
         }
         f32x16 cur[kRB];
@@ -407,18 +427,73 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
         // cur[rb][e]: query column (lane % 32) of block rb, key row
         // kb*32 + 8*(e/4) + 4*(lane/32) + e%4.
 #pragma unroll
-        for (int rb = 0; rb < kRB; ++rb) row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
+        for (int rb = 0; rb < kRB; ++rb) {
+          if constexpr (kExact)
+            row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
+          else
+            row_update_ref(pend[rb], scale_log2, m_run[rb], s_run[rb]);
+        }
         interleave_hint<T, kRB * G::kSteps, APACK_RS_VALU_PER_MFMA, APACK_RS_TRANS_PER_MFMA>();
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) pend[rb] = cur[rb];
         __builtin_amdgcn_sched_barrier(0);  // keep later blocks' LDS reads out of this one
       }
+    };
+    for (int it = 0; it < n_tiles; ++it) {
+      const int buf = it % S;
+      const int64_t t0 = key_begin + (int64_t)it * kKeyTile;
+      const float* lm = lmask + it * kKeyTile;
+      wait_tile_loads<T, D, NW>(min(S - 2, n_tiles - 1 - it));
+      __syncthreads();
+      if (it + S - 1 < n_tiles)
+        KTileLoad<T, D, NW>::issue(lds[(it + S - 1) % S], kbase, t0 + (int64_t)(S - 1) * kKeyTile, key_end, wave,
+                                   lane);
+      if (active) {
+        if (kUseRef && !kExactOnly && !ref) {
+          bool unset = false;
+#pragma unroll
+          for (int rb = 0; rb < kRB; ++rb) unset |= m_run[rb] == -FLT_MAX;
+          if (__ballot(unset) == 0) {
+            ref = true;
+#pragma unroll
+            for (int rb = 0; rb < kRB; ++rb) {
+              m_run[rb] += 64.f;
+              s_run[rb] *= 0x1p-64f;
+            }
+          }
+        }
+        if (ref)
+          tile_body(std::false_type{}, lds[buf], lm);
+        else
+          tile_body(std::true_type{}, lds[buf], lm);
+      }
     }
+    if (active) {
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb) {
+        if (ref)
+          row_update_ref(pend[rb], scale_log2, m_run[rb], s_run[rb]);
+        else
+          row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
+      }
+    }
+  };
+  run_chunk(std::false_type{});
+  bool overflow = false;
+  if (active) {
+#pragma unroll
+    for (int rb = 0; rb < kRB; ++rb) overflow |= !(s_run[rb] < INFINITY);
+  }
+  if (sizeof(T) == 2 && __syncthreads_or(overflow)) {
+    // A logit far above its lane's reference: the whole workgroup streams the
+    // chunk again with the online maximum (the tile buffers are free).
+    for (int p = 0; p < S - 1 && p < n_tiles; ++p)
+      KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
+    run_chunk(std::true_type{});
   }
   if (active) {
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
-      row_update(pend[rb], scale_log2, m_run[rb], s_run[rb]);
       const float mo = __shfl_xor(m_run[rb], 32);
       const float so = __shfl_xor(s_run[rb], 32);
       const float mm = fmaxf(m_run[rb], mo);

@@ -295,6 +295,27 @@ def test_four_wave_workgroups_over_four_stages(dtype, hq, hkv, d, q_len, n):
     _parity(case)
 
 
+@pytest.mark.parametrize("q_len,seed", [(16, 20), (112, 19)])
+def test_row_sums_redone_when_a_logit_overflows_the_reference(q_len, seed):
+    # Pass 1 sums each query row's exponentials against a fixed reference
+    # (its running maximum after the first tile, plus 64) and redoes the
+    # chunk with the online maximum when a sum overflows.  One key of KV
+    # group 0, in the third tile of its chunk, is set along the first query
+    # row so that its logit is ~170-190 (natural units) above the rest: the
+    # reference sum of that row overflows and the workgroup (one or seven row
+    # waves) takes the second pass.  Scores and kept rows match the oracle.
+    n = 40013
+    specs = [([(0, 8000, A_), (8000, n - 8200, V_)], n, q_len, (0.5, 0.3))]
+    case = _synthetic("bf16", 8, 2, 128, specs, seed=seed)
+    q = widen(case.q, "bf16")
+    u = q[0, 0] / np.linalg.norm(q[0, 0])
+    row = 384 * 10 + 300          # chunks of 384 keys at this length: chunk 10, tile 2
+    case.k[0, row] = W.to_bf16_bits((2000.0 * u).astype(np.float32))
+    logit = float(q[0, 0] @ widen(case.k, "bf16")[0, row]) / math.sqrt(case.d)
+    assert logit > 150.0
+    _parity(case)
+
+
 def test_exact_ties_keep_lowest_rows():
     specs = [([(0, 100, A_), (100, 250, V_)], 400, 7, (0.33, 0.5))]
     case = _synthetic("bf16", 8, 2, 128, specs, seed=12, zero_keys=True)

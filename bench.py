@@ -77,8 +77,8 @@ def main():
                          "byte counters) and exit")
     args = ap.parse_args()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py measures one GPU: the prune path needs no collective, and runs with "
-              "--gpus > 1 are not part of this build", file=sys.stderr)
+        print("bench.py measures one GPU: the prune path needs no collective, and runs on "
+              "more than one GPU (--gpus > 1) are not implemented", file=sys.stderr)
         sys.exit(2)
 
     import torch

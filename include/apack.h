@@ -56,7 +56,7 @@ typedef enum apack_status {
   APACK_E_WORKSPACE = 4,  /* workspace missing, misaligned or too small     */
   APACK_E_ALIAS = 5,      /* an output overlaps an input                    */
   APACK_E_HIP = 6,        /* a HIP runtime call failed                      */
-  APACK_E_UNSUPPORTED = 7 /* valid but outside what this build implements  */
+  APACK_E_UNSUPPORTED = 7 /* valid but outside what the library implements */
 } apack_status;
 
 /* The two bounding enumerators make every int32 value a valid apack_dtype,

@@ -381,7 +381,7 @@ std::array<void*, kMaxDevices> g_scratch{};   // device address of scratch, per 
 apack_status static_scratch(void** ptr) {
   int dev = 0;
   APACK_HIP(hipGetDevice(&dev));
-  APACK_CHECK(dev >= 0 && dev < kMaxDevices, APACK_E_UNSUPPORTED, "device %d beyond the %d this build tracks", dev,
+  APACK_CHECK(dev >= 0 && dev < kMaxDevices, APACK_E_UNSUPPORTED, "device %d beyond the %d the library tracks", dev,
               kMaxDevices);
   std::lock_guard<std::mutex> lk(g_scratch_mu);
   if (!g_scratch[dev]) {

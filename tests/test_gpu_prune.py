@@ -316,6 +316,17 @@ def test_row_sums_redone_when_a_logit_overflows_the_reference(q_len, seed):
     _parity(case)
 
 
+def test_reference_sums_start_late_after_non_candidate_runs():
+    # Chunks whose first tiles hold only non-candidate rows (300 text rows at
+    # the start, a 700-row text run in the middle): a wave keeps the online
+    # maximum until every lane has seen a candidate key, which here happens
+    # one or more tiles into its chunk.
+    n = 40013
+    spans = [(300, 9000, A_), (10000, n - 10200, V_)]
+    case = _synthetic("bf16", 28, 4, 128, [(spans, n, 64, (0.5, 0.3))], seed=21)
+    _parity(case)
+
+
 def test_exact_ties_keep_lowest_rows():
     specs = [([(0, 100, A_), (100, 250, V_)], 400, 7, (0.33, 0.5))]
     case = _synthetic("bf16", 8, 2, 128, specs, seed=12, zero_keys=True)

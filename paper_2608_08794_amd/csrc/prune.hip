@@ -6,11 +6,13 @@
 // ascending list of kept rows.
 //
 // Kernels (all on the caller's stream, no host synchronisation):
-//   k_rowstats   pass 1: per query row, online (max, sum exp2) over a chunk
-//                of keys; logits from MFMA with Q fragments resident in VGPRs
-//                and K tiles staged through LDS.  The last chunk of each row
-//                group to finish combines the chunk partials (fixed order)
-//                into b_r = max_r + log2(Z_r).
+//   k_rowstats   pass 1: per query row, (reference, sum exp2) over a chunk
+//                of keys: the online maximum until each lane has seen a
+//                candidate key, then a fixed reference (see row_update_ref);
+//                logits from MFMA with Q fragments resident in VGPRs and K
+//                tiles staged through LDS.  The last chunk of each row group
+//                to finish combines the chunk partials (fixed order) into
+//                b_r = max_r + log2(Z_r).
 //   k_colsum     pass 2: recomputes the logits with the roles of the MFMA
 //                operands swapped so the per-key sum over query rows is
 //                lane-local, then a fixed-order cross-wave sum through LDS.

@@ -18,9 +18,10 @@
 // column maxima into order-preserving keys with atomicMax.
 //
 // Workgroups are dealt to the eight XCDs round-robin by index, so the host
-// lists the tiles so that each XCD gets whole column blocks (all their row
-// tiles) and the workgroups resident on one XCD share their operands in
-// that XCD's L2.
+// lists the tiles so that each XCD gets whole column blocks of one band of
+// at most eight row tiles, and the workgroups resident on one XCD share
+// both operands in that XCD's L2: a band's audio rows and a few column
+// blocks of visual rows.
 #include <algorithm>
 #include <cmath>
 
@@ -206,8 +207,12 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
 }  // namespace
 
 std::vector<GemmTileDev> gate_gemm256_tiles(const std::vector<ClipDev>& clips) {
-  // Column blocks (clip, n0) are dealt to the XCDs in turn; an XCD's share
-  // lists every row tile of its blocks, block after block.
+  // A clip's row tiles are cut into bands of at most kBandRows (as even as
+  // possible); per band, column blocks (clip, n0) are dealt to the XCDs in
+  // turn, and an XCD's share lists the band's row tiles of its blocks, block
+  // after block.  A tall clip's audio then passes through each XCD's L2 once
+  // per band and column block rather than once per column block.
+  constexpr int kBandRows = 8;
   std::vector<std::vector<GemmTileDev>> share(kXcds);
   int next = 0;
   for (size_t s = 0; s < clips.size(); ++s) {
@@ -215,8 +220,12 @@ std::vector<GemmTileDev> gate_gemm256_tiles(const std::vector<ClipDev>& clips) {
     const int64_t nv = (int64_t)c.n_frames * c.per_frame;
     if (nv == 0 || c.n_audio == 0) continue;
     const int mb = (int)((c.n_audio + kTile - 1) / kTile), nb = (int)((nv + kTile - 1) / kTile);
-    for (int n = 0; n < nb; ++n, next = (next + 1) % kXcds)
-      for (int m = 0; m < mb; ++m) share[next].push_back({(int32_t)s, m * kTile, n * kTile, 0});
+    const int n_band = (mb + kBandRows - 1) / kBandRows;
+    for (int b = 0; b < n_band; ++b) {
+      const int m0 = b * mb / n_band, m1 = (b + 1) * mb / n_band;
+      for (int n = 0; n < nb; ++n, next = (next + 1) % kXcds)
+        for (int m = m0; m < m1; ++m) share[next].push_back({(int32_t)s, m * kTile, n * kTile, 0});
+    }
   }
   size_t rounds = 0;
   for (auto& q : share) rounds = std::max(rounds, q.size());

@@ -10,14 +10,15 @@
 //                of keys: the online maximum until each lane has seen a
 //                candidate key, then a fixed reference (see row_update_ref);
 //                logits from MFMA with Q fragments resident in VGPRs and K
-//                tiles staged through LDS.  The last chunk of each row group
-//                to finish combines the chunk partials (fixed order) into
-//                b_r = max_r + log2(Z_r).
-//   k_colsum     pass 2: recomputes the logits with the roles of the MFMA
-//                operands swapped so the per-key sum over query rows is
-//                lane-local, then a fixed-order cross-wave sum through LDS.
-//                The last workgroup of each key chunk sums the per-group
-//                partials into I_j and counts its first radix digit.
+//                tiles staged through LDS; one (max, sum) partial per row
+//                and chunk.
+//   k_colsum     pass 2: each workgroup first combines its rows' chunk
+//                partials (fixed order) into b_r = max_r + log2(Z_r), then
+//                recomputes the logits with the roles of the MFMA operands
+//                swapped so the per-key sum over query rows is lane-local,
+//                then a fixed-order cross-wave sum through LDS.  The last
+//                workgroup of each key chunk sums the per-group partials
+//                into I_j and counts its first radix digit.
 // The remaining radix digits, the per-modality top-k and the ordered kept
 // list are formed by the kernels of select.hip.
 #include <cfloat>
@@ -317,8 +318,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
                                                          const T* __restrict__ q, int64_t q_hs,
                                                          const T* __restrict__ k, int64_t k_hs,
                                                          int n_rep, float scale_log2,
-                                                         float2* __restrict__ stats, float* __restrict__ bias,
-                                                         uint32_t* __restrict__ ctr, uint32_t* __restrict__ zero,
+                                                         float2* __restrict__ stats, uint32_t* __restrict__ zero,
                                                          int64_t zero_n) {
   using G = TileGeom<T, D>;
   using M = Mma<T>;
@@ -493,6 +493,8 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
       KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
     run_chunk(std::true_type{});
   }
+  // The chunk's (max, sum) of each row, combined over the two lane halves;
+  // pass 2 merges the chunks of its rows.
   if (active) {
 #pragma unroll
     for (int rb = 0; rb < kRB; ++rb) {
@@ -502,55 +504,8 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
       const float ss = s_run[rb] * fast_exp2(m_run[rb] - mm) + so * fast_exp2(mo - mm);
       const int rho = row0 + rb * 32 + lane;
       if (lane < 32 && rho < rg_end)
-        st_agent(&stats[sq.stats_off + ((int64_t)tl.g * sq.n_chunks + tl.chunk) * sq.rows_pad + rho],
-                 make_float2(mm, ss));
+        stats[sq.stats_off + ((int64_t)tl.g * sq.n_chunks + tl.chunk) * sq.rows_pad + rho] = make_float2(mm, ss);
     }
-  }
-  // The last chunk of this (group, row group) to finish combines every
-  // chunk's partials of its rows, in chunk order, into b = M + log2(Z);
-  // padding rows get +inf so they contribute exp2(-inf) = 0 in pass 2.
-  if (!arrive_last<NW * kWave>(ctr + sq.ctr_off + tl.g * sq.n_rg + tl.rg, (uint32_t)sq.n_chunks)) return;
-  const int r_lo = tl.rg * sq.rows_per_rg;
-  // Partials are [g][chunk][row]: a wave's loads of one chunk are contiguous.
-  // Chunks [c_lo, c_hi) of row rho, loaded in batches (all in flight
-  // together) and merged in chunk order.
-  auto merge_run = [&](int rho, int c_lo, int c_hi, float& m, float& s) {
-    const float2* p = stats + sq.stats_off + (int64_t)tl.g * sq.n_chunks * sq.rows_pad + rho;
-    constexpr int CB = 16;
-    for (int c0 = c_lo; c0 < c_hi; c0 += CB) {
-      float2 v[CB];
-#pragma unroll
-      for (int i = 0; i < CB; ++i)
-        v[i] = c0 + i < c_hi ? ld_agent(p + (int64_t)(c0 + i) * sq.rows_pad) : make_float2(0.f, 0.f);
-#pragma unroll
-      for (int i = 0; i < CB; ++i)
-        if (c0 + i < c_hi) merge(m, s, v[i].x, v[i].y);
-    }
-  };
-  const int R = sq.rows_per_rg, nthr = NW * kWave;
-  const int ng = R <= nthr / 4 ? 4 : R <= nthr / 2 ? 2 : 1;
-  if (ng == 1) {
-    for (int rho = r_lo + tid; rho < r_lo + R; rho += nthr) {
-      float m = -FLT_MAX, s = 0.f;
-      if (rho < rows_g) merge_run(rho, 0, sq.n_chunks, m, s);
-      bias[sq.bias_off + (int64_t)tl.g * sq.rows_pad + rho] = (s > 0.f) ? m + log2f(s) : INFINITY;
-    }
-    return;
-  }
-  // Fewer rows than threads: ng threads share a row, each merging a
-  // contiguous run of chunks (one load batch instead of ng in a row), and
-  // the runs are combined in order in LDS (the key tiles are done).
-  float2* part = reinterpret_cast<float2*>(&lds[0][0]);
-  const int grp = tid / R, r = tid - grp * R, rho = r_lo + r;
-  const int cpg = (sq.n_chunks + ng - 1) / ng;
-  float m = -FLT_MAX, s = 0.f;
-  if (grp < ng && rho < rows_g) merge_run(rho, grp * cpg, min(sq.n_chunks, (grp + 1) * cpg), m, s);
-  if (grp < ng) part[grp * R + r] = make_float2(m, s);
-  __syncthreads();
-  if (tid < R) {
-    float mm = part[r].x, ss = part[r].y;
-    for (int q = 1; q < ng; ++q) merge(mm, ss, part[q * R + r].x, part[q * R + r].y);
-    bias[sq.bias_off + (int64_t)tl.g * sq.rows_pad + rho] = (ss > 0.f) ? mm + log2f(ss) : INFINITY;
   }
 }
 
@@ -584,7 +539,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
                                                        const T* __restrict__ q, int64_t q_hs,
                                                        const T* __restrict__ k, int64_t k_hs,
                                                        int n_rep, int hkv, float scale_log2,
-                                                       const float* __restrict__ bias,
+                                                       const float2* __restrict__ stats,
                                                        float* __restrict__ colpart, float* __restrict__ scores,
                                                        uint32_t* __restrict__ hist, uint32_t* __restrict__ ctr) {
   using G = TileGeom<T, D>;
@@ -607,26 +562,57 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   if (key_end > sq.n_tokens) key_end = sq.n_tokens;
   const int n_tiles = (int)((key_end - key_begin + kKeyTile - 1) / kKeyTile);
   const T* kbase = k + (int64_t)tl.g * k_hs + sq.tok_off * D;
-  // The first key tiles are requested before the query and bias loads.
+  // The first key tiles are requested before the query loads and the row-partial merge.
   for (int p = 0; p < S - 1 && p < n_tiles; ++p)
     KTileLoad<T, D, NW>::issue(lds[p], kbase, key_begin + (int64_t)p * kKeyTile, key_end, wave, lane);
 
   QFrags<T, D> qfr;
   auto& qf = qfr.v;
+  if (active) load_q<T, D>(qfr, q, q_hs, sq, tl.g, n_rep, row0, lane);
+  // b_r = M_r + log2(Z_r) of the row group's rows, combined from pass 1's
+  // chunk partials in chunk order (padding rows get +inf, so they add
+  // exp2(-inf) = 0).  With fewer rows than threads, ng threads share a row,
+  // each merging a contiguous run of chunks, and the runs are combined in
+  // order.  The column-sum slots hold the values until the loop starts.
   float b[kRB][16];
-  if (active) {
-    load_q<T, D>(qfr, q, q_hs, sq, tl.g, n_rep, row0, lane);
-    const float* bb = bias + sq.bias_off + (int64_t)tl.g * sq.rows_pad + row0 + 4 * (lane >> 5);
+  {
+    const int R = sq.rows_per_rg, nthr = NW * kWave, r_lo = tl.rg * sq.rows_per_rg;
+    const int ng = R <= nthr / 4 ? 4 : R <= nthr / 2 ? 2 : 1;
+    float* lb = &red[0][0][0];
+    float2* part = reinterpret_cast<float2*>(lb + R);
+    const float2* p0 = stats + sq.stats_off + (int64_t)tl.g * sq.n_chunks * sq.rows_pad;
+    const int cpg = (sq.n_chunks + ng - 1) / ng;
+    if (tid < ng * R) {
+      const int grp = tid / R, r = tid - grp * R, rho = r_lo + r;
+      float m = -FLT_MAX, s = 0.f;
+      if (rho < rows_g) {
+        const int c_lo = grp * cpg, c_hi = min(sq.n_chunks, (grp + 1) * cpg);
+        constexpr int CB = 16;
+        for (int c0 = c_lo; c0 < c_hi; c0 += CB) {
+          float2 v[CB];
 #pragma unroll
-    for (int rb = 0; rb < kRB; ++rb)
+          for (int i = 0; i < CB; ++i) v[i] = p0[(int64_t)min(c0 + i, c_hi - 1) * sq.rows_pad + rho];
 #pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float4 v = *reinterpret_cast<const float4*>(bb + rb * 32 + 8 * i);
-        b[rb][4 * i + 0] = v.x;
-        b[rb][4 * i + 1] = v.y;
-        b[rb][4 * i + 2] = v.z;
-        b[rb][4 * i + 3] = v.w;
+          for (int i = 0; i < CB; ++i)
+            if (c0 + i < c_hi) merge(m, s, v[i].x, v[i].y);
+        }
       }
+      part[grp * R + r] = make_float2(m, s);
+    }
+    __syncthreads();
+    for (int r = tid; r < R; r += nthr) {
+      float mm = part[r].x, ss = part[r].y;
+      for (int g2 = 1; g2 < ng; ++g2) merge(mm, ss, part[g2 * R + r].x, part[g2 * R + r].y);
+      lb[r] = (ss > 0.f) ? mm + log2f(ss) : INFINITY;
+    }
+    __syncthreads();
+    if (active) {
+      const float* bb = lb + (row0 - r_lo) + 4 * (lane >> 5);
+#pragma unroll
+      for (int rb = 0; rb < kRB; ++rb)
+#pragma unroll
+        for (int e = 0; e < 16; ++e) b[rb][e] = bb[rb * 32 + 8 * (e >> 2) + (e & 3)];
+    }
   }
 
   float* out = colpart + sq.colpart_off + (int64_t)(tl.g * sq.n_rg + tl.rg) * sq.n_tokens;
@@ -708,7 +694,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   // rather than kept live across the main loop.
   SeqDev* sr = &seqs[tl.seq];
   const int planes = hkv * sr->n_rg;
-  if (!arrive_last<NW * kWave>(ctr + sr->ctr_off + planes + tl.chunk, (uint32_t)planes)) return;
+  if (!arrive_last<NW * kWave>(ctr + sr->ctr_off + tl.chunk, (uint32_t)planes)) return;
   const bool sel = sr->select[0] || sr->select[1];
   uint32_t* lh = reinterpret_cast<uint32_t*>(&lds[0][0]);  // 2 x 2048 bins; the key tiles are done
   if (sel) {
@@ -766,7 +752,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
   __syncthreads();
   uint32_t* gh = hist + (int64_t)tl.seq * 2 * kRadixBins;
   merge_hist<NW * kWave>(lh, gh);
-  if (arrive_last<NW * kWave>(ctr + sr->ctr_off + planes + sr->n_chunks, (uint32_t)sr->n_chunks))
+  if (arrive_last<NW * kWave>(ctr + sr->ctr_off + sr->n_chunks, (uint32_t)sr->n_chunks))
     pick_bins<NW * kWave>(sr, gh, 0);
 }
 
@@ -780,11 +766,11 @@ apack_status launch_scores_t(const PrunePlan& pl, const DevPtrs& dp, const void*
   const int nt = (int)pl.tiles.size();
   if (nt > 0) {
     hipLaunchKernelGGL((k_rowstats<T, D, NW, S>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles,
-                       dp.tags, (const T*)q, q_hs, (const T*)k, k_hs, n_rep, scale_log2, dp.stats, dp.bias,
-                       dp.ctr, dp.hist, pl.any_select ? select_hist_words((int64_t)pl.seqs.size()) : (int64_t)0);
+                       dp.tags, (const T*)q, q_hs, (const T*)k, k_hs, n_rep, scale_log2, dp.stats, dp.hist,
+                       pl.any_select ? select_hist_words((int64_t)pl.seqs.size()) : (int64_t)0);
     APACK_CHECK(launch_status("k_rowstats") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
     hipLaunchKernelGGL((k_colsum<T, D, NW, S>), dim3(nt), dim3(NW * kWave), 0, stream, dp.seqs, dp.tiles, dp.tags,
-                       (const T*)q, q_hs, (const T*)k, k_hs, n_rep, hkv, scale_log2, dp.bias, dp.colpart, scores,
+                       (const T*)q, q_hs, (const T*)k, k_hs, n_rep, hkv, scale_log2, dp.stats, dp.colpart, scores,
                        dp.hist, dp.ctr);
     APACK_CHECK(launch_status("k_colsum") == APACK_OK, APACK_E_HIP, "%s", apack_last_error());
   }

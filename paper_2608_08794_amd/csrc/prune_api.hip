@@ -21,7 +21,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
   pl = PrunePlan();
   pl.seqs.resize(n_seq);
   pl.n_kept.resize(n_seq);
-  int64_t tag = 0, stats = 0, rows = 0, colpart = 0, kept = 0;
+  int64_t tag = 0, stats = 0, colpart = 0, kept = 0;
   int waves = 1;
   // Total work units so the chunk length can target a few workgroups per CU.
   int64_t weighted = 0;
@@ -99,8 +99,6 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     sd.rows_per_rg = (int32_t)((per + kRowsPerWave - 1) / kRowsPerWave * kRowsPerWave);
     sd.rows_pad = sd.n_rg * sd.rows_per_rg;
     waves = std::max<int>(waves, sd.rows_per_rg / kRowsPerWave);
-    sd.bias_off = rows;
-    rows += (int64_t)hkv * sd.rows_pad;
     if (sd.n_cand > 0) weighted += a.n_tokens * (int64_t)hkv * sd.n_rg;
   }
   // Sequences may not overlap in K (their scores would collide).
@@ -129,7 +127,7 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
     sd.colpart_off = colpart;
     colpart += (int64_t)hkv * sd.n_rg * sd.n_tokens;
     sd.ctr_off = (int32_t)pl.total_ctr;
-    pl.total_ctr += (int64_t)hkv * sd.n_rg + sd.n_chunks + 1;
+    pl.total_ctr += sd.n_chunks + 1;
     // Tiles: chunks of one (g, rg) eight apart so that both query-row
     // groups of a key chunk land on the same XCD's L2.
     for (int g = 0; g < hkv; ++g)
@@ -139,7 +137,6 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
   }
   pl.waves = waves <= 1 ? 1 : waves <= 2 ? 2 : waves <= 4 ? 4 : waves == 7 ? 7 : 8;
   pl.total_tok = tag;
-  pl.total_rows = rows;
   pl.total_stats = stats;
   pl.total_colpart = colpart;
   pl.total_kept = kept;
@@ -157,8 +154,6 @@ apack_status build_prune_plan(int32_t n_seq, const apack_seq* seqs, int32_t hq, 
   pl.blob_bytes = c.used;
   pl.off_stats = c.used;
   c.take<float2>(pl.total_stats);
-  pl.off_bias = c.used;
-  c.take<float>(pl.total_rows);
   pl.off_colpart = c.used;
   c.take<float>(pl.total_colpart);
   pl.off_hist = c.used;
@@ -262,7 +257,6 @@ apack_status apack_prune_layer(int32_t n_seq, const apack_seq* seqs, apack_dtype
   dp.ctr = reinterpret_cast<uint32_t*>(ws + pl.off_ctr);
   dp.tags = reinterpret_cast<uint8_t*>(ws + pl.off_tags);
   dp.stats = reinterpret_cast<float2*>(ws + pl.off_stats);
-  dp.bias = reinterpret_cast<float*>(ws + pl.off_bias);
   dp.colpart = reinterpret_cast<float*>(ws + pl.off_colpart);
   const apack_status ls = launch_prune(pl, dp, dtype, d, hq, hkv, q, q_head_stride, k, k_head_stride, scores,
                                        kept_rows, hs);

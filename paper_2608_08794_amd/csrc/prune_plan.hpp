@@ -37,7 +37,6 @@ struct SeqDev {
   int64_t n_kept;       // kept rows of the sequence (bound on the scan's writes)
   int64_t tag_off;      // first byte of the sequence in the tag array
   int64_t stats_off;    // first (max, sum) partial: [g][chunk][rows_pad]
-  int64_t bias_off;     // first b entry: [g][rows_pad], row rho = (h % n_rep)*q_len + t
   int64_t colpart_off;  // first per-group column partial: [g*n_rg + rg][n_tokens]
   int32_t q_len;
   int32_t n_rg;         // query-row groups per KV head
@@ -56,7 +55,7 @@ struct SeqDev {
   uint32_t kk[2];       // rank of the k-th value inside the chosen bucket
   uint32_t done_cnt;    // row tiles finished in the current select pass
   int32_t n_ftiles;     // row tiles of the sequence
-  int32_t ctr_off;      // arrival counters: [hkv*n_rg row groups][n_chunks key chunks][1]
+  int32_t ctr_off;      // arrival counters: [n_chunks key chunks][1 sequence]
 };
 
 struct FTileDev {
@@ -74,7 +73,6 @@ struct PrunePlan {
   std::vector<int64_t> n_kept;
   int64_t total_tok = 0;    // sum of n_tokens (tag bytes)
   int64_t max_tokens = 0;   // longest sequence
-  int64_t total_rows = 0;   // sum of hkv * rows_pad (padded query rows)
   int64_t total_stats = 0;  // (max, sum) partials
   int64_t total_colpart = 0;
   int64_t total_kept = 0;
@@ -83,7 +81,7 @@ struct PrunePlan {
   bool any_select = false;
   // Workspace layout (byte offsets).
   size_t off_seqs = 0, off_tiles = 0, off_ftiles = 0, off_tags = 0, off_ctr = 0, blob_bytes = 0;
-  size_t off_stats = 0, off_bias = 0, off_colpart = 0, off_hist = 0, off_cnt = 0, ws_bytes = 0;
+  size_t off_stats = 0, off_colpart = 0, off_hist = 0, off_cnt = 0, ws_bytes = 0;
 };
 
 struct DevPtrs {
@@ -92,7 +90,6 @@ struct DevPtrs {
   uint8_t* tags;
   FTileDev* ftiles;
   float2* stats;
-  float* bias;
   float* colpart;
   uint32_t* hist;       // [n_seq][2][2048] radix histograms
   uint32_t* cnt;        // [n_ftiles][3] per-tile keep counts

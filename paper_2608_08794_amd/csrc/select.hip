@@ -379,8 +379,9 @@ __global__ __launch_bounds__(kST) void k_select_small(const SeqDev* __restrict__
     for (int u = 0; u < kSPer; ++u) {
       const bool ea = (mt[u] == 1) & (bits[u] == thr0), ev = (mt[u] == 2) & (bits[u] == thr1);
       const uint64_t ma = __ballot(ea), mv = __ballot(ev);
-      const bool kp = (mt[u] == 0) | ((mt[u] == 1) & (bits[u] > thr0)) | ((mt[u] == 2) & (bits[u] > thr1)) |
-                      (ea & (ra + below(ma) < need0)) | (ev & (rv + below(mv) < need1));
+      const int kp = (int)(mt[u] == 0) | ((int)(mt[u] == 1) & (int)(bits[u] > thr0)) |
+                     ((int)(mt[u] == 2) & (int)(bits[u] > thr1)) | ((int)ea & (int)(ra + below(ma) < need0)) |
+                     ((int)ev & (int)(rv + below(mv) < need1));
       ra += __popcll(ma);
       rv += __popcll(mv);
       keepbits |= (uint32_t)kp << u;

@@ -435,7 +435,11 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
           else
             row_update_ref(pend[rb], scale_log2, m_run[rb], s_run[rb]);
         }
-        interleave_hint<T, kRB * G::kSteps, APACK_RS_VALU_PER_MFMA, APACK_RS_TRANS_PER_MFMA>();
+        // The first block's fragments are read at the tile start; the
+        // grouping hint there made the compiler issue one row block's MFMA
+        // chain back to back, so that block is left to the default schedule
+        // (which alternates the two chains with the VALU work).
+        if (kb > 0) interleave_hint<T, kRB * G::kSteps, APACK_RS_VALU_PER_MFMA, APACK_RS_TRANS_PER_MFMA>();
 #pragma unroll
         for (int rb = 0; rb < kRB; ++rb) pend[rb] = cur[rb];
         __builtin_amdgcn_sched_barrier(0);  // keep later blocks' LDS reads out of this one

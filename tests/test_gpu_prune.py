@@ -295,6 +295,19 @@ def test_four_wave_workgroups_over_four_stages(dtype, hq, hkv, d, q_len, n):
     _parity(case)
 
 
+@pytest.mark.parametrize("hq,hkv,q_len", [(8, 2, 32), (28, 4, 8), (28, 4, 1)])
+def test_row_partials_merged_by_several_threads_per_row(hq, hkv, q_len):
+    # Pass 2 starts by combining each query row's per-chunk (max, sum)
+    # partials from pass 1.  With 128 rows per group (here 4 x 32) two
+    # threads of the four-wave workgroup share a row, with 56 or 7 rows four
+    # do, each merging a contiguous run of the chunks before the
+    # runs are combined in order (63 to 105 key chunks per group here).
+    n = 40013
+    specs = [([(0, 8000, A_), (8000, n - 8200, V_)], n, q_len, (0.5, 0.3))]
+    case = _synthetic("bf16", hq, hkv, 128, specs, seed=23)
+    _parity(case)
+
+
 @pytest.mark.parametrize("q_len,seed", [(16, 20), (112, 19)])
 def test_row_sums_redone_when_a_logit_overflows_the_reference(q_len, seed):
     # Pass 1 sums each query row's exponentials against a fixed reference

@@ -126,8 +126,13 @@ struct KTileLoad {
   static constexpr int kLoads = G::kTileBytes / 1024;
   static constexpr int kPer = (kLoads + NW - 1) / NW;
   static_assert(G::kTileBytes % 1024 == 0, "tile must be a whole number of 1 KiB loads");
+  // wave must be uniform (readfirstlane), so that the LDS addresses and the
+  // tile's base are scalar and each load costs a clamp and a 32-bit offset.
   __device__ __forceinline__ static void issue(char* lds, const T* kbase, int64_t row0, int64_t n_rows, int wave,
                                                int lane) {
+    const char* base = reinterpret_cast<const char*>(kbase + row0 * D);
+    // Last row of the tile that exists (rows past it repeat it).
+    const int last = (int)min<int64_t>(n_rows - 1 - row0, kKeyTile - 1);
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int j = wave + i * NW;
@@ -135,10 +140,8 @@ struct KTileLoad {
         const int byte = j * 1024 + lane * 16;
         const int r = byte / G::kRowBytes;
         const int c = ((byte % G::kRowBytes) >> 4) ^ (r & G::kSwz);
-        int64_t row = row0 + r;
-        if (row >= n_rows) row = n_rows - 1;
-        const char* src = reinterpret_cast<const char*>(kbase + row * D) + c * 16;
-        __builtin_amdgcn_global_load_lds((glb_ptr_t)src, (lds_ptr_t)(lds + j * 1024), 16, 0, 0);
+        const uint32_t off = (uint32_t)min(r, last) * G::kRowBytes + c * 16;
+        __builtin_amdgcn_global_load_lds((glb_ptr_t)(base + off), (lds_ptr_t)(lds + j * 1024), 16, 0, 0);
       }
     }
   }
@@ -330,7 +333,7 @@ __global__ __launch_bounds__(NW * kWave) void k_rowstats(const SeqDev* __restric
 
   const TileDev tl = tiles[blockIdx.x];
   const SeqDev sq = seqs[tl.seq];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rows_g = n_rep * sq.q_len;
   const int rg_end = min(rows_g, (tl.rg + 1) * sq.rows_per_rg);
   const int row0 = tl.rg * sq.rows_per_rg + wave * kRowsPerWave;
@@ -554,7 +557,7 @@ __global__ __launch_bounds__(NW * kWave) void k_colsum(SeqDev* __restrict__ seqs
 
   const TileDev tl = tiles[blockIdx.x];
   const SeqDev sq = seqs[tl.seq];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int rows_g = n_rep * sq.q_len;
   const int rg_end = min(rows_g, (tl.rg + 1) * sq.rows_per_rg);
   const int row0 = tl.rg * sq.rows_per_rg + wave * kRowsPerWave;

@@ -132,7 +132,8 @@ struct KTileLoad {
                                                int lane) {
     const char* base = reinterpret_cast<const char*>(kbase + row0 * D);
     // Last row of the tile that exists (rows past it repeat it).
-    const int last = (int)min<int64_t>(n_rows - 1 - row0, kKeyTile - 1);
+    const int64_t left = n_rows - 1 - row0;
+    const int last = left < kKeyTile - 1 ? (int)left : kKeyTile - 1;
 #pragma unroll
     for (int i = 0; i < kPer; ++i) {
       const int j = wave + i * NW;

@@ -62,19 +62,29 @@ __device__ __forceinline__ int swz(int r) { return (r / kRowsPer256) & (kChunks 
 // One operand's stage: rows r0 .. r0+255 (clamped to the last valid row),
 // elements [k0, k0 + kK).  Load j fills LDS bytes [1024 j, 1024 j + 1024);
 // lane l's 16 bytes land at row r = (1024 j + 16 l) / kRowB, chunk c, and
-// come from global chunk c ^ swz(r).
-__device__ __forceinline__ void issue_operand(char* lds, const uint16_t* base, int64_t r0, int64_t n_rows, int dim,
-                                              int k0, int wave, int lane) {
+// come from global chunk c ^ swz(r).  off[i] is lane l's byte offset of load
+// i from the stage's first byte (row r0, element k0), the same for every
+// stage, so a stage only moves the scalar base.
+__device__ __forceinline__ void operand_offsets(int64_t r0, int64_t n_rows, int dim, int wave, int lane,
+                                                uint32_t (&off)[kLoadsPerWave]) {
 #pragma unroll
   for (int i = 0; i < kLoadsPerWave; ++i) {
     const int j = wave * kLoadsPerWave + i;
     const int byte = j * 1024 + lane * 16;
     const int r = byte / kRowB;
     const int c = ((byte % kRowB) >> 4) ^ swz(r);
-    int64_t row = r0 + r;
-    if (row >= n_rows) row = n_rows - 1;
-    const char* src = reinterpret_cast<const char*>(base + row * dim + k0) + c * 16;
-    __builtin_amdgcn_global_load_lds((glb_ptr_t)src, (lds_ptr_t)(lds + j * 1024), 16, 0, 0);
+    const int64_t left = n_rows - 1 - r0;
+    const int rr = left < r ? (int)left : r;
+    off[i] = (uint32_t)rr * (uint32_t)dim * 2u + (uint32_t)c * 16u;
+  }
+}
+
+__device__ __forceinline__ void issue_operand(char* lds, const char* base, const uint32_t (&off)[kLoadsPerWave],
+                                              int wave) {
+#pragma unroll
+  for (int i = 0; i < kLoadsPerWave; ++i) {
+    const int j = wave * kLoadsPerWave + i;
+    __builtin_amdgcn_global_load_lds((glb_ptr_t)(base + off[i]), (lds_ptr_t)(lds + j * 1024), 16, 0, 0);
   }
 }
 
@@ -97,7 +107,7 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
   const int64_t n_a = c.n_audio, n_v = (int64_t)c.n_frames * c.per_frame;
   const uint16_t* A = xa + c.aud_off * dim;
   const uint16_t* B = xv + c.vis_off * dim;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int wm = wave / kWN, wn = wave % kWN;
 
   f32x16 acc[kBI][kBJ];
@@ -107,10 +117,15 @@ __global__ __launch_bounds__(kWaves * 64) __attribute__((amdgpu_waves_per_eu(2, 
     for (int j = 0; j < kBJ; ++j) acc[i][j] = f32x16{};
 
   const int n_k = dim / kK;
+  uint32_t off_a[kLoadsPerWave], off_b[kLoadsPerWave];
+  operand_offsets(tl.m0, n_a, dim, wave, lane, off_a);
+  operand_offsets(tl.n0, n_v, dim, wave, lane, off_b);
+  const char* base_a = reinterpret_cast<const char*>(A + tl.m0 * dim);
+  const char* base_b = reinterpret_cast<const char*>(B + tl.n0 * dim);
   auto issue = [&](int k_stage) {
     char* st = lds + (k_stage % kStages) * kStageB;
-    issue_operand(st, A, tl.m0, n_a, dim, k_stage * kK, wave, lane);
-    issue_operand(st + kOpB, B, tl.n0, n_v, dim, k_stage * kK, wave, lane);
+    issue_operand(st, base_a + (size_t)k_stage * kK * 2, off_a, wave);
+    issue_operand(st + kOpB, base_b + (size_t)k_stage * kK * 2, off_b, wave);
   };
   // Loads run kStages - 1 stages ahead of the MFMAs.
   for (int p = 0; p < kStages - 1 && p < n_k; ++p) issue(p);
